@@ -1,0 +1,154 @@
+/*
+ * dprc.h -- randomized per-sample gradient-norm estimation for DP-SGD with
+ * randomized clipping (DP-SGD-RC), for AMD Instinct MI355X (gfx950).
+ *
+ * The calls follow the problem statement of the paper "Efficient DP-SGD for
+ * LLMs with Randomized Clipping":
+ *   - Algorithm 2 (Norm-Estimation-Routine): per-sample squared-norm estimates
+ *     of a bias-free linear layer S = A W from its activations A[B,T,d] and
+ *     output gradients E = dL/dS [B,T,p], by the Hutchinson estimator
+ *     (dprc_norm_hutch) or by Hutch++ (dprc_norm_hutchpp);
+ *   - Algorithm 1 (DP-SGD-RC step): the squared norms summed over layers, the
+ *     clip factors min(1, C/sqrt(n_i)) (dprc_clip_scale), the clipped gradient
+ *     sum_i c_i A_i^T E_i that the second backward pass produces for a linear
+ *     layer (dprc_clip_accumulate), and the Gaussian noise sigma*C*N(0,I)
+ *     (dprc_add_noise).
+ *
+ * Conventions for every call:
+ *   - Pointers named A, E, n2, c, grad, ws, out are DEVICE pointers; the
+ *     dprc_layer array itself is HOST memory and is read during the call only.
+ *   - Every call is asynchronous on `stream` (0 = the null stream) and returns
+ *     after enqueueing; results are valid once the stream reaches that point.
+ *   - The library never allocates or frees memory and keeps no global state.
+ *     Scratch space is the caller's `ws` buffer of at least the size returned
+ *     by the matching *_workspace() query, 256-byte aligned.  Calls that share
+ *     a workspace must be ordered (same stream, or synchronised).
+ *   - Arguments are validated on the host before anything is enqueued; a
+ *     failed check returns a non-zero dprc_status and enqueues nothing.  A
+ *     failed launch returns DPRC_ERROR_HIP.  No C++ exception crosses the ABI.
+ *   - Tensors are row-major with token rows: element (i, t, j) of A is at
+ *     A + (i*T + t)*lda + j.  bf16 inputs need 16-byte aligned base pointers
+ *     and strides that are multiples of 8 elements; fp32 inputs need 4-byte
+ *     alignment.  Otherwise DPRC_ERROR_NOT_SUPPORTED.
+ *
+ * Probes: +-1 (Rademacher) entries from Philox4x32-10 (Salmon et al., SC'11)
+ * keyed by (seed, layer_id, stream), shared by all samples of a layer and
+ * fresh per layer; the caller folds the training step into `seed`.  Column j,
+ * rows 32w..32w+31 of a layer's probe matrix in stream s is word (w mod 4) of
+ * Philox(counter = (w div 4, j, layer_id, s), key = (seed lo, seed hi)); bit b
+ * gives row 32w+b, 0 -> +1, 1 -> -1.  Streams: 0 = Hutchinson probes (also
+ * the Hutch++ residual probes), 1 = Hutch++ sketch, 2 = Gaussian noise.
+ */
+#ifndef DPRC_H
+#define DPRC_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  DPRC_SUCCESS = 0,
+  DPRC_ERROR_INVALID_VALUE = 1,      /* null pointer, non-positive size, bad enum, ...   */
+  DPRC_ERROR_NOT_SUPPORTED = 2,      /* alignment / stride / size outside supported range */
+  DPRC_ERROR_WORKSPACE_TOO_SMALL = 3,
+  DPRC_ERROR_HIP = 4                 /* a HIP runtime call or launch failed              */
+} dprc_status;
+
+typedef enum { DPRC_F32 = 0, DPRC_BF16 = 1 } dprc_dtype;
+
+/* Which dimension the probes sketch.  OUT sketches the p side (Z is p x k,
+ * Algorithm 2 as printed), IN sketches the d side (Z is d x k; the text notes
+ * the two are equivalent since ||A^T E||_F = ||E^T A||_F), AUTO sketches the
+ * larger dimension (the paper's proof sketch projects the larger one), ties
+ * going to OUT. */
+typedef enum { DPRC_SIDE_OUT = 0, DPRC_SIDE_IN = 1, DPRC_SIDE_AUTO = 2 } dprc_side;
+
+/* Probe family.  RADEMACHER: the counter-generated +-1 probes above.
+ * HADAMARD: the deterministic Sylvester-Hadamard signs z(u,j) =
+ * (-1)^popcount(u & j) (verification: with k = 2^q >= the sketched dimension
+ * the estimate equals the exact squared norm). */
+typedef enum { DPRC_PROBE_RADEMACHER = 0, DPRC_PROBE_HADAMARD = 1 } dprc_probe;
+
+/* One bias-free linear layer S = A W (section "Proposed Method"). */
+typedef struct {
+  const void* A;      /* activations [B,T,d], device                       */
+  const void* E;      /* output gradients dL/dS [B,T,p], device            */
+  int64_t B, T, d, p; /* all >= 1                                          */
+  int64_t lda, lde;   /* token-row strides in elements, lda >= d, lde >= p */
+  dprc_dtype dtype;   /* both tensors share it                             */
+  uint32_t layer_id;  /* probe-key component; unique per layer in a step   */
+} dprc_layer;
+
+/* ---- Hutchinson (Algorithm 2, Hutch branch) --------------------------------
+ * For each layer and sample i: Y_i = X_i Z (X the sketched operand, T x m,
+ * Z the m x k probes), W_i = X'_i^T Y_i (X' the other operand), estimate
+ * ||W_i||_F^2 / k, an unbiased estimate of ||A_i^T E_i||_F^2.
+ *   n2[B]                 : = (accumulate == 0) or += (accumulate != 0) the
+ *                           sum over the layers of the estimates (Algorithm 1,
+ *                           layer-wise summation).  fp32, device.
+ *   n2_layers[num_layers*B]: optional (may be NULL) per-layer estimates.
+ *   k in [1, 256].  All layers must have the same B.
+ * Workspace: dprc_norm_hutch_workspace() bytes for the same arguments. */
+size_t dprc_norm_hutch_workspace(const dprc_layer* layers, int32_t num_layers, int32_t k,
+                                 dprc_side side);
+dprc_status dprc_norm_hutch(const dprc_layer* layers, int32_t num_layers, int32_t k,
+                            dprc_probe probe, uint64_t seed, dprc_side side, float* n2,
+                            float* n2_layers, int32_t accumulate, void* ws, size_t ws_bytes,
+                            hipStream_t stream);
+
+/* ---- Hutch++ (Algorithm 2, Hutch++ branch; estimator section) --------------
+ * With M_i = X'_i^T X_i (m probed columns): sketch O S = M_i^T (M_i S) with s
+ * sketch probes (stream 1), Q = orthonormal basis of its columns (Householder
+ * QR), U = M_i Q, V = M_i P - U (Q^T P) with r residual probes P (stream 0),
+ * estimate ||U||_F^2 + ||V||_F^2 / r.  s in [0, 64], r in [1, 256],
+ * s + r <= 256, s <= the sketched dimension.  s = 0 gives Hutchinson with r
+ * probes.  Outputs as for dprc_norm_hutch. */
+size_t dprc_norm_hutchpp_workspace(const dprc_layer* layers, int32_t num_layers, int32_t s,
+                                   int32_t r, dprc_side side);
+dprc_status dprc_norm_hutchpp(const dprc_layer* layers, int32_t num_layers, int32_t s, int32_t r,
+                              uint64_t seed, dprc_side side, float* n2, float* n2_layers,
+                              int32_t accumulate, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ---- clip factors (Algorithm 1, scaled loss) ---------------------------------
+ * c[i] = min(1, C / sqrt(n2[i])); n2 = 0 gives 1; a NaN, infinite or negative
+ * n2 gives 0 (the sample is dropped).  C > 0 and finite.  Device n2[B], c[B]. */
+dprc_status dprc_clip_scale(const float* n2, int64_t B, float C, float* c, hipStream_t stream);
+
+/* ---- clipped accumulation (Algorithm 1, second backward pass) ----------------
+ * grad[j*ldg + u] (=|+=) sum_i c[i] * sum_t A[i,t,j] * E[i,t,u]   (d x p, fp32)
+ * i.e. the weight gradient of S = A W for the loss sum_i c_i L_i with the c_i
+ * held constant.  Samples with c[i] == 0 are skipped entirely.  bf16 inputs
+ * run on bf16 matrix cores with fp32 accumulation; the per-sample factor is
+ * applied to the fp32 accumulator, never to the bf16 inputs.  ldg >= p. */
+size_t dprc_clip_accumulate_workspace(const dprc_layer* layer);
+dprc_status dprc_clip_accumulate(const dprc_layer* layer, const float* c, float* grad,
+                                 int64_t ldg, int32_t accumulate, void* ws, size_t ws_bytes,
+                                 hipStream_t stream);
+
+/* ---- Gaussian noise (Algorithm 1) ---------------------------------------------
+ * grad[e] += sigma * C * xi_e for e in [0, numel), xi_e standard normal from
+ * Philox (stream 2) keyed by (seed, tensor_id): element e uses words of
+ * block e div 4 through the Box-Muller transform with uniforms
+ * (floor(x / 2^9) + 1/2) * 2^-23.  sigma >= 0, C > 0, both finite. */
+dprc_status dprc_add_noise(float* grad, int64_t numel, float sigma, float C, uint64_t seed,
+                           uint32_t tensor_id, hipStream_t stream);
+
+/* ---- probe bits (verification) -------------------------------------------------
+ * out[j*ceil(m/32) + w] = packed probe word w of column j (k columns), bits of
+ * rows >= m cleared.  probe selects the family; for HADAMARD, seed, layer_id
+ * and stream_id are ignored.  Device out. */
+dprc_status dprc_probe_bits(dprc_probe probe, uint64_t seed, uint32_t layer_id,
+                            uint32_t stream_id, int64_t m, int32_t k, uint32_t* out,
+                            hipStream_t stream);
+
+const char* dprc_status_string(dprc_status status);
+const char* dprc_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DPRC_H */

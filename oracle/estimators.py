@@ -147,6 +147,42 @@ def hutchpp_layer(A, E, s, r, seed, layer_id, side=SIDE_OUT, ZS=None, ZP=None):
     return out
 
 
+def hutch_sample_projected(A_i, E_i, Z, side=SIDE_OUT):
+    """One sample's Hutchinson estimate in the association order of Algorithm 2,
+    Y = A_i^T (E_i Z), without forming G_i (O(T k (d+p)) work).  Used for
+    sampled checks at full workload sizes; pinned to ``hutch_layer``."""
+    A_i, E_i = as_f64(A_i), as_f64(E_i)
+    X, Xo = (E_i, A_i) if side == SIDE_OUT else (A_i, E_i)
+    W = Xo.T @ (X @ Z)
+    return float(np.sum(W * W)) / Z.shape[1]
+
+
+def hutchpp_sample_projected(A_i, E_i, ZS, ZP, side=SIDE_OUT):
+    """One sample's Hutch++ estimate in the association order of Algorithm 2:
+    Q = orth(G^T (A (A^T (G S)))) with the roles of A and E set by ``side``,
+    U = A^T (G Q), V = A^T (G P) - U (Q^T P).  Pinned to ``hutchpp_layer``."""
+    A_i, E_i = as_f64(A_i), as_f64(E_i)
+    X, Xo = (E_i, A_i) if side == SIDE_OUT else (A_i, E_i)
+    r = ZP.shape[1]
+    if ZS.shape[1] == 0:
+        V = Xo.T @ (X @ ZP)
+        return float(np.sum(V * V)) / r
+    OS = X.T @ (Xo @ (Xo.T @ (X @ ZS)))
+    Q, _ = np.linalg.qr(OS, mode="reduced")
+    U = Xo.T @ (X @ Q)
+    V = Xo.T @ (X @ ZP) - U @ (Q.T @ ZP)
+    return float(np.sum(U * U) + np.sum(V * V) / r)
+
+
+def clip_accumulate_rows(A, E, c, rows):
+    """Rows ``rows`` of the clipped gradient sum_i c_i A_i^T E_i (for sampled checks)."""
+    out = np.zeros((len(rows), E.shape[2]))
+    for i in range(A.shape[0]):
+        if c[i] != 0.0:
+            out += c[i] * (as_f64(A[i][:, rows]).T @ as_f64(E[i]))
+    return out
+
+
 def exact_layer(A, E):
     """Exact squared per-sample norms of one layer, [B]."""
     A, E = as_f64(A), as_f64(E)

@@ -1,0 +1,72 @@
+"""Build libdprc.so for gfx950 with hipcc (in-tree, next to this file).
+
+    python -m paper_2605_24879_amd.build [--jobs N] [--debug]
+
+Every .hip source under csrc/ is compiled to an object in _build/ (in
+parallel) and linked into paper_2605_24879_amd/libdprc.so.  Packed-fp32 VALU
+instructions are disabled for the device code.
+"""
+
+import argparse
+import concurrent.futures as cf
+import os
+import subprocess
+import sys
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(HERE)
+CSRC = os.path.join(HERE, "csrc")
+BUILD = os.path.join(HERE, "_build")
+LIB = os.path.join(HERE, "libdprc.so")
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+ARCH = "gfx950"
+
+COMMON = [
+    f"--offload-arch={ARCH}", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-result",
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-I", os.path.join(ROOT, "include"), "-I", CSRC,
+]
+
+
+def sources():
+    return sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".hip"))
+
+
+def _compile(src, opt):
+    obj = os.path.join(BUILD, os.path.basename(src)[:-4] + ".o")
+    cmd = [HIPCC, *COMMON, opt, "-c", src, "-o", obj]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    msgs = "\n".join(l for l in (r.stdout + r.stderr).splitlines()
+                     if "packed-fp32-ops" not in l and "not a recognized feature" not in l)
+    return src, obj, r.returncode, msgs
+
+
+def build(jobs=None, debug=False, verbose=False):
+    os.makedirs(BUILD, exist_ok=True)
+    opt = "-O1" if debug else "-O3"
+    srcs = sources()
+    objs = []
+    with cf.ThreadPoolExecutor(max_workers=jobs or min(8, len(srcs))) as ex:
+        for src, obj, rc, msgs in ex.map(lambda s: _compile(s, opt), srcs):
+            if msgs.strip() and (rc != 0 or verbose):
+                print(msgs, file=sys.stderr)
+            if rc != 0:
+                raise RuntimeError(f"hipcc failed on {os.path.basename(src)}")
+            objs.append(obj)
+    tmp = LIB + ".tmp"
+    cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        print(r.stdout + r.stderr, file=sys.stderr)
+        raise RuntimeError("link of libdprc.so failed")
+    os.replace(tmp, LIB)
+    return LIB
+
+
+if __name__ == "__main__":
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--jobs", type=int, default=None)
+    ap.add_argument("--debug", action="store_true")
+    ap.add_argument("-v", "--verbose", action="store_true")
+    a = ap.parse_args()
+    print(build(a.jobs, a.debug, a.verbose))

@@ -1,0 +1,530 @@
+// C-ABI entry points of libdprc (declared in include/dprc.h): argument
+// validation, side resolution, workspace planning and the launch sequence of
+// each call.  Nothing here allocates device memory or synchronises the stream.
+#include <cmath>
+#include <cstring>
+#include <vector>
+
+#include "../../include/dprc.h"
+#include "kernels.hpp"
+
+using namespace dprc;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+struct Arena {  // carves 256-byte aligned regions out of the caller's workspace
+  char* base;
+  size_t off = 0;
+  explicit Arena(void* b) : base(static_cast<char*>(b)) {}
+  template <class T>
+  T* take(size_t count) {
+    off = (off + kAlign - 1) / kAlign * kAlign;
+    T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+    off += count * sizeof(T);
+    return p;
+  }
+};
+
+// A layer after side resolution: X is sketched (m columns = probe rows), Xo is the other operand.
+struct View {
+  const void* X;
+  int64_t ldx, m;
+  const void* Xo;
+  int64_t ldo, n;
+  int64_t B, T;
+  dprc_dtype dtype;
+  uint32_t layer_id;
+};
+
+dprc_side resolve(const dprc_layer& L, dprc_side side) {
+  if (side == DPRC_SIDE_AUTO) return L.d > L.p ? DPRC_SIDE_IN : DPRC_SIDE_OUT;
+  return side;
+}
+
+View view_of(const dprc_layer& L, dprc_side side) {
+  View v;
+  if (resolve(L, side) == DPRC_SIDE_OUT) {
+    v.X = L.E; v.ldx = L.lde; v.m = L.p;
+    v.Xo = L.A; v.ldo = L.lda; v.n = L.d;
+  } else {
+    v.X = L.A; v.ldx = L.lda; v.m = L.d;
+    v.Xo = L.E; v.ldo = L.lde; v.n = L.p;
+  }
+  v.B = L.B; v.T = L.T; v.dtype = L.dtype; v.layer_id = L.layer_id;
+  return v;
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// bf16 token rows starting on 16-byte boundaries take the 16-byte load path
+int rows16(const void* p, int64_t ld) { return aligned(p, 16) && ld % 8 == 0; }
+
+dprc_status check_layer(const dprc_layer& L) {
+  if (!L.A || !L.E) return DPRC_ERROR_INVALID_VALUE;
+  if (L.B < 1 || L.T < 1 || L.d < 1 || L.p < 1) return DPRC_ERROR_INVALID_VALUE;
+  if (L.lda < L.d || L.lde < L.p) return DPRC_ERROR_INVALID_VALUE;
+  if (L.dtype != DPRC_F32 && L.dtype != DPRC_BF16) return DPRC_ERROR_INVALID_VALUE;
+  if (L.B > 65535 || L.T > (1LL << 30) || L.d > (1LL << 30) || L.p > (1LL << 30))
+    return DPRC_ERROR_NOT_SUPPORTED;
+  if (L.B * L.T > (1LL << 31)) return DPRC_ERROR_NOT_SUPPORTED;
+  const size_t elem = L.dtype == DPRC_BF16 ? 2 : 4;
+  if (!aligned(L.A, elem) || !aligned(L.E, elem)) return DPRC_ERROR_NOT_SUPPORTED;
+  return DPRC_SUCCESS;
+}
+
+dprc_status check_layers(const dprc_layer* layers, int32_t num, dprc_side side) {
+  if (!layers || num < 1) return DPRC_ERROR_INVALID_VALUE;
+  if (side != DPRC_SIDE_OUT && side != DPRC_SIDE_IN && side != DPRC_SIDE_AUTO) return DPRC_ERROR_INVALID_VALUE;
+  for (int32_t l = 0; l < num; ++l) {
+    dprc_status s = check_layer(layers[l]);
+    if (s != DPRC_SUCCESS) return s;
+    if (layers[l].B != layers[0].B) return DPRC_ERROR_INVALID_VALUE;
+  }
+  return DPRC_SUCCESS;
+}
+
+void key_of(uint64_t seed, uint32_t& k0, uint32_t& k1) {
+  k0 = (uint32_t)(seed & 0xFFFFFFFFu);
+  k1 = (uint32_t)(seed >> 32);
+}
+
+// column blocks of 16 the kernels are instantiated for
+int pad_cols(int ncols) {
+  static const int nbs[] = {1, 2, 3, 4, 5, 6, 8, 12, 16};
+  const int need = (ncols + 15) / 16;
+  for (int nb : nbs)
+    if (nb >= need) return 16 * nb;
+  return -1;
+}
+
+int rows_per_wg(int64_t rows, int ncols_pad) {
+  const int nb = ncols_pad / 16;
+  int rb = 1;
+  if (rows >= 64 * 1024) rb = 4;
+  else if (rows >= 32 * 1024) rb = 2;
+  while (rb > 1 && rb * nb > 8) rb >>= 1;
+  return 16 * rb;
+}
+
+int words_per_chunk(int64_t m, int nz) {
+  const int64_t all = round_up(ceil_div(m, 32), 4);
+  if (nz <= 0) return (int)all;
+  return (int)std::min<int64_t>(all, std::max(4, (8192 / nz) & ~3));
+}
+
+// Token-reduction geometry for one (operand width n, columns) pass.
+struct TokPlan {
+  int32_t ntiles, S, sps, T_pad;
+};
+TokPlan tok_plan(int64_t B, int64_t T, int64_t n) {
+  TokPlan p;
+  p.T_pad = (int32_t)round_up(T, kStage);
+  p.ntiles = (int32_t)ceil_div(n, kTile);
+  const int64_t stages = p.T_pad / kStage;
+  const int64_t base = B * p.ntiles;
+  int64_t S = std::max<int64_t>(1, ceil_div(512, base));
+  S = std::min<int64_t>(S, std::max<int64_t>(1, stages / 4));  // >= 4 stages (256 tokens) per split
+  p.sps = (int32_t)ceil_div(stages, S);
+  p.S = (int32_t)ceil_div(stages, p.sps);
+  return p;
+}
+
+struct TokBufs {
+  float* part;
+  float* tilesq;
+  uint32_t* cnt;  // [B*ntiles] tile counters, then [B] sample counters
+};
+
+TokBufs take_tok(Arena& ar, int64_t B, const TokPlan& tp, int ncols_pad) {
+  TokBufs b;
+  b.part = tp.S > 1 ? ar.take<float>((size_t)B * tp.ntiles * tp.S * ncols_pad * kTile) : nullptr;
+  b.tilesq = ar.take<float>((size_t)B * tp.ntiles);
+  b.cnt = ar.take<uint32_t>((size_t)B * tp.ntiles + B);
+  return b;
+}
+
+dprc_status hip_status(hipError_t e) { return e == hipSuccess ? DPRC_SUCCESS : DPRC_ERROR_HIP; }
+
+// ---- one projection + token-reduction pass (bf16) --------------------------------------------
+struct PassSpec {
+  const uint16_t* X; int64_t ldx, m;      // projected operand
+  const uint16_t* Xo; int64_t ldo, n;     // reduced operand
+  int32_t nd; const uint16_t* Rhi; const uint16_t* Rlo; int64_t ld_r;   // dense columns
+  int32_t nz; uint32_t stream_id; int probe_kind;                       // generated columns
+  int mode; float scale; float* n2; float* n2_layer; int accumulate;    // mode 0
+  float* M; int64_t m_ld; uint16_t* Mhi; uint16_t* Mlo; int64_t mh_ld;  // mode 1
+};
+
+size_t pass_ws(Arena& ar, int64_t B, int64_t T, int64_t n, int ncols_pad, uint16_t** Yt, TokBufs* tb,
+               TokPlan* tpo) {
+  const TokPlan tp = tok_plan(B, T, n);
+  uint16_t* y = ar.take<uint16_t>((size_t)2 * ncols_pad * B * tp.T_pad);
+  TokBufs t = take_tok(ar, B, tp, ncols_pad);
+  if (Yt) *Yt = y;
+  if (tb) *tb = t;
+  if (tpo) *tpo = tp;
+  return ar.off;
+}
+
+dprc_status run_pass(const PassSpec& ps, int64_t B, int64_t T, uint32_t k0, uint32_t k1, uint32_t layer,
+                     void* ws, hipStream_t st) {
+  const int ncols = ps.nd + ps.nz;
+  const int ncols_pad = pad_cols(ncols);
+  Arena ar(ws);
+  uint16_t* Yt;
+  TokBufs tb;
+  TokPlan tp;
+  pass_ws(ar, B, T, ps.n, ncols_pad, &Yt, &tb, &tp);
+
+  ProjectArgs pa;
+  pa.X = ps.X; pa.ldx = ps.ldx; pa.x_ss = T * ps.ldx;
+  pa.B = (int32_t)B; pa.T = (int32_t)T; pa.m = (int32_t)ps.m; pa.T_pad = tp.T_pad;
+  pa.nd = ps.nd; pa.nz = ps.nz; pa.ncols_pad = ncols_pad;
+  pa.Rhi = ps.Rhi; pa.Rlo = ps.Rlo; pa.ld_r = ps.ld_r; pa.r_ss = (int64_t)ps.nd * ps.ld_r;
+  pa.probe_kind = ps.probe_kind; pa.key0 = k0; pa.key1 = k1; pa.layer_id = layer; pa.stream_id = ps.stream_id;
+  pa.words_per_chunk = words_per_chunk(ps.m, ps.nz);
+  pa.Yt = Yt; pa.yt_ld = B * tp.T_pad;
+  pa.zero_ptr = tb.cnt; pa.zero_count = (int32_t)(B * tp.ntiles + B);
+  pa.vec = rows16(ps.X, ps.ldx);
+  hipError_t e = launch_project(pa, rows_per_wg(B * tp.T_pad, ncols_pad), st);
+  if (e != hipSuccess) return DPRC_ERROR_HIP;
+
+  TokredArgs ta;
+  ta.X = ps.Xo; ta.ldx = ps.ldo; ta.x_ss = T * ps.ldo;
+  ta.B = (int32_t)B; ta.T = (int32_t)T; ta.n = (int32_t)ps.n;
+  ta.Yt = Yt; ta.yt_ld = B * tp.T_pad; ta.T_pad = tp.T_pad; ta.ncols = ncols; ta.ncols_pad = ncols_pad;
+  ta.ntiles = tp.ntiles; ta.S = tp.S; ta.stages_per_split = tp.sps;
+  ta.mode = ps.mode;
+  ta.part = tb.part; ta.cnt_tile = tb.cnt; ta.tilesq = tb.tilesq; ta.cnt_sample = tb.cnt + B * tp.ntiles;
+  ta.scale = ps.scale; ta.n2 = ps.n2; ta.n2_layer = ps.n2_layer; ta.accumulate = ps.accumulate;
+  ta.M = ps.M; ta.m_ld = ps.m_ld; ta.m_ss = (int64_t)ncols * ps.m_ld;
+  ta.Mhi = ps.Mhi; ta.Mlo = ps.Mlo; ta.mh_ld = ps.mh_ld; ta.mh_ss = (int64_t)ncols * ps.mh_ld;
+  ta.vec = rows16(ps.Xo, ps.ldo);
+  return hip_status(launch_tokred(ta, st));
+}
+
+size_t pass_ws_bytes(int64_t B, int64_t T, int64_t n, int ncols) {
+  Arena ar(nullptr);
+  return pass_ws(ar, B, T, n, pad_cols(ncols), nullptr, nullptr, nullptr);
+}
+
+// ---- Hutchinson ---------------------------------------------------------------------------------
+size_t hutch_layer_ws(const View& v, int32_t k) {
+  if (v.dtype == DPRC_BF16) return pass_ws_bytes(v.B, v.T, v.n, k);
+  Arena ar(nullptr);
+  ar.take<uint32_t>((size_t)k * ceil_div(v.m, 32));
+  ar.take<float>((size_t)v.B * v.T * k);
+  ar.take<float>((size_t)v.B * k * v.n);
+  return ar.off;
+}
+
+dprc_status hutch_layer(const View& v, int32_t k, int probe, uint32_t k0, uint32_t k1, float* n2,
+                        float* n2_layer, int accumulate, void* ws, hipStream_t st) {
+  if (v.dtype == DPRC_BF16) {
+    PassSpec ps{};
+    ps.X = (const uint16_t*)v.X; ps.ldx = v.ldx; ps.m = v.m;
+    ps.Xo = (const uint16_t*)v.Xo; ps.ldo = v.ldo; ps.n = v.n;
+    ps.nd = 0; ps.nz = k; ps.stream_id = 0; ps.probe_kind = probe;
+    ps.mode = 0; ps.scale = 1.0f / (float)k; ps.n2 = n2; ps.n2_layer = n2_layer; ps.accumulate = accumulate;
+    return run_pass(ps, v.B, v.T, k0, k1, v.layer_id, ws, st);
+  }
+  Arena ar(ws);
+  uint32_t* zb = ar.take<uint32_t>((size_t)k * ceil_div(v.m, 32));
+  float* Y = ar.take<float>((size_t)v.B * v.T * k);
+  float* M = ar.take<float>((size_t)v.B * k * v.n);
+  hipError_t e = launch_probe_bits(probe, k0, k1, v.layer_id, 0, v.m, k, zb, st);
+  if (e != hipSuccess) return DPRC_ERROR_HIP;
+  ProjectF32Args pa{(const float*)v.X, v.ldx, v.T * v.ldx, (int32_t)v.B, (int32_t)v.T, (int32_t)v.m,
+                    0, k, k, nullptr, 0, 0, zb, Y};
+  if ((e = launch_project_f32(pa, st)) != hipSuccess) return DPRC_ERROR_HIP;
+  TokredF32Args ta{(const float*)v.Xo, v.ldo, v.T * v.ldo, (int32_t)v.B, (int32_t)v.T, (int32_t)v.n, Y, k,
+                   M, v.n, (int64_t)k * v.n};
+  if ((e = launch_tokred_f32(ta, st)) != hipSuccess) return DPRC_ERROR_HIP;
+  return hip_status(launch_sample_sq(M, v.n, (int64_t)k * v.n, (int32_t)v.B, k, (int32_t)v.n,
+                                     1.0f / (float)k, n2, n2_layer, accumulate, st));
+}
+
+// ---- Hutch++ -------------------------------------------------------------------------------------
+struct PPBufs {
+  uint16_t *WShi, *WSlo; int64_t ld_ws;   // pass-1 result, dense operand of pass 2 (bf16)
+  float* WS32;                             // same, fp32 path
+  float* OS;                               // [B][s][m]
+  double* qrwork;                          // [B][2][s][m]
+  float* Q;                                // [B][s][m]
+  uint16_t *Qhi, *Qlo; int64_t ld_q;       // bf16 path
+  float* UW;                               // [B][s+r][n]
+  uint32_t* zb;                            // fp32 path: probe bits (s or r columns)
+  float* Y32;                              // fp32 path
+  void* pass_ws;                           // bf16 path: scratch of one pass
+};
+
+size_t hutchpp_layout(const View& v, int32_t s, int32_t r, void* ws, PPBufs* out) {
+  Arena ar(ws);
+  PPBufs b{};
+  const int64_t B = v.B;
+  if (s > 0) {
+    if (v.dtype == DPRC_BF16) {
+      b.ld_ws = ceil_div(v.n, kTile) * kTile;
+      b.WShi = ar.take<uint16_t>((size_t)B * s * b.ld_ws);
+      b.WSlo = ar.take<uint16_t>((size_t)B * s * b.ld_ws);
+      b.ld_q = ceil_div(v.m, kTile) * kTile;
+      b.Qhi = ar.take<uint16_t>((size_t)B * s * b.ld_q);
+      b.Qlo = ar.take<uint16_t>((size_t)B * s * b.ld_q);
+    } else {
+      b.WS32 = ar.take<float>((size_t)B * s * v.n);
+    }
+    b.OS = ar.take<float>((size_t)B * s * v.m);
+    b.qrwork = ar.take<double>((size_t)B * 2 * s * v.m);
+    b.Q = ar.take<float>((size_t)B * s * v.m);
+    b.UW = ar.take<float>((size_t)B * (s + r) * v.n);
+  }
+  if (v.dtype == DPRC_BF16) {
+    b.pass_ws = ar.base ? ar.base + ((ar.off + kAlign - 1) / kAlign) * kAlign : nullptr;
+    ar.off = (ar.off + kAlign - 1) / kAlign * kAlign;
+    size_t need = std::max(pass_ws_bytes(B, v.T, v.n, std::max(s, 1)), pass_ws_bytes(B, v.T, v.m, std::max(s, 1)));
+    need = std::max(need, pass_ws_bytes(B, v.T, v.n, s + r));
+    ar.off += need;
+  } else {
+    b.zb = ar.take<uint32_t>((size_t)std::max(s, r) * ceil_div(std::max(v.m, v.n), 32));
+    b.Y32 = ar.take<float>((size_t)B * v.T * (s + r));
+    if (s == 0) b.UW = ar.take<float>((size_t)B * r * v.n);
+  }
+  if (out) *out = b;
+  return ar.off;
+}
+
+dprc_status hutchpp_layer(const View& v, int32_t s, int32_t r, uint32_t k0, uint32_t k1, float* n2,
+                          float* n2_layer, int accumulate, void* ws, hipStream_t st) {
+  PPBufs b;
+  hutchpp_layout(v, s, r, ws, &b);
+  const int64_t B = v.B, T = v.T;
+  hipError_t e;
+  if (v.dtype == DPRC_BF16) {
+    const uint16_t* X = (const uint16_t*)v.X;
+    const uint16_t* Xo = (const uint16_t*)v.Xo;
+    if (s == 0) {  // Hutchinson with the r residual probes
+      PassSpec ps{};
+      ps.X = X; ps.ldx = v.ldx; ps.m = v.m; ps.Xo = Xo; ps.ldo = v.ldo; ps.n = v.n;
+      ps.nz = r; ps.stream_id = 0; ps.probe_kind = 0;
+      ps.mode = 0; ps.scale = 1.0f / (float)r; ps.n2 = n2; ps.n2_layer = n2_layer; ps.accumulate = accumulate;
+      return run_pass(ps, B, T, k0, k1, v.layer_id, b.pass_ws, st);
+    }
+    // pass 1: W_S = Xo^T (X S)
+    PassSpec p1{};
+    p1.X = X; p1.ldx = v.ldx; p1.m = v.m; p1.Xo = Xo; p1.ldo = v.ldo; p1.n = v.n;
+    p1.nz = s; p1.stream_id = 1; p1.probe_kind = 0;
+    p1.mode = 1; p1.Mhi = b.WShi; p1.Mlo = b.WSlo; p1.mh_ld = b.ld_ws;
+    dprc_status stt = run_pass(p1, B, T, k0, k1, v.layer_id, b.pass_ws, st);
+    if (stt != DPRC_SUCCESS) return stt;
+    // pass 2: O S = X^T (Xo W_S)
+    PassSpec p2{};
+    p2.X = Xo; p2.ldx = v.ldo; p2.m = v.n; p2.Xo = X; p2.ldo = v.ldx; p2.n = v.m;
+    p2.nd = s; p2.Rhi = b.WShi; p2.Rlo = b.WSlo; p2.ld_r = b.ld_ws;
+    p2.mode = 1; p2.M = b.OS; p2.m_ld = v.m;
+    if ((stt = run_pass(p2, B, T, k0, k1, v.layer_id, b.pass_ws, st)) != DPRC_SUCCESS) return stt;
+    // Q = orth(O S)
+    e = launch_qr(b.OS, v.m, (int64_t)s * v.m, (int32_t)B, (int32_t)v.m, s, b.qrwork, b.Q, v.m,
+                  (int64_t)s * v.m, b.Qhi, b.Qlo, b.ld_q, (int64_t)s * b.ld_q, st);
+    if (e != hipSuccess) return DPRC_ERROR_HIP;
+    // pass 3: [U | W_P] = Xo^T (X [Q | P])
+    PassSpec p3{};
+    p3.X = X; p3.ldx = v.ldx; p3.m = v.m; p3.Xo = Xo; p3.ldo = v.ldo; p3.n = v.n;
+    p3.nd = s; p3.Rhi = b.Qhi; p3.Rlo = b.Qlo; p3.ld_r = b.ld_q;
+    p3.nz = r; p3.stream_id = 0; p3.probe_kind = 0;
+    p3.mode = 1; p3.M = b.UW; p3.m_ld = v.n;
+    if ((stt = run_pass(p3, B, T, k0, k1, v.layer_id, b.pass_ws, st)) != DPRC_SUCCESS) return stt;
+  } else {
+    const float* X = (const float*)v.X;
+    const float* Xo = (const float*)v.Xo;
+    if (s > 0) {
+      if ((e = launch_probe_bits(0, k0, k1, v.layer_id, 1, v.m, s, b.zb, st)) != hipSuccess) return DPRC_ERROR_HIP;
+      ProjectF32Args a1{X, v.ldx, T * v.ldx, (int32_t)B, (int32_t)T, (int32_t)v.m, 0, s, s, nullptr, 0, 0, b.zb, b.Y32};
+      if ((e = launch_project_f32(a1, st)) != hipSuccess) return DPRC_ERROR_HIP;
+      TokredF32Args t1{Xo, v.ldo, T * v.ldo, (int32_t)B, (int32_t)T, (int32_t)v.n, b.Y32, s, b.WS32, v.n, (int64_t)s * v.n};
+      if ((e = launch_tokred_f32(t1, st)) != hipSuccess) return DPRC_ERROR_HIP;
+      ProjectF32Args a2{Xo, v.ldo, T * v.ldo, (int32_t)B, (int32_t)T, (int32_t)v.n, s, 0, s, b.WS32, v.n,
+                        (int64_t)s * v.n, nullptr, b.Y32};
+      if ((e = launch_project_f32(a2, st)) != hipSuccess) return DPRC_ERROR_HIP;
+      TokredF32Args t2{X, v.ldx, T * v.ldx, (int32_t)B, (int32_t)T, (int32_t)v.m, b.Y32, s, b.OS, v.m, (int64_t)s * v.m};
+      if ((e = launch_tokred_f32(t2, st)) != hipSuccess) return DPRC_ERROR_HIP;
+      e = launch_qr(b.OS, v.m, (int64_t)s * v.m, (int32_t)B, (int32_t)v.m, s, b.qrwork, b.Q, v.m,
+                    (int64_t)s * v.m, nullptr, nullptr, 0, 0, st);
+      if (e != hipSuccess) return DPRC_ERROR_HIP;
+    }
+    if ((e = launch_probe_bits(0, k0, k1, v.layer_id, 0, v.m, r, b.zb, st)) != hipSuccess) return DPRC_ERROR_HIP;
+    ProjectF32Args a3{X, v.ldx, T * v.ldx, (int32_t)B, (int32_t)T, (int32_t)v.m, s, r, s + r, b.Q, v.m,
+                      (int64_t)s * v.m, b.zb, b.Y32};
+    if ((e = launch_project_f32(a3, st)) != hipSuccess) return DPRC_ERROR_HIP;
+    TokredF32Args t3{Xo, v.ldo, T * v.ldo, (int32_t)B, (int32_t)T, (int32_t)v.n, b.Y32, s + r, b.UW, v.n,
+                     (int64_t)(s + r) * v.n};
+    if ((e = launch_tokred_f32(t3, st)) != hipSuccess) return DPRC_ERROR_HIP;
+    if (s == 0)
+      return hip_status(launch_sample_sq(b.UW, v.n, (int64_t)r * v.n, (int32_t)B, r, (int32_t)v.n,
+                                         1.0f / (float)r, n2, n2_layer, accumulate, st));
+  }
+  return hip_status(launch_hutchpp_final(b.UW, v.n, (int64_t)(s + r) * v.n, b.Q, v.m, (int64_t)s * v.m,
+                                         (int32_t)B, (int32_t)v.n, (int32_t)v.m, s, r, k0, k1, v.layer_id,
+                                         n2, n2_layer, accumulate, st));
+}
+
+// ---- clipped accumulation ----------------------------------------------------------------------------
+struct GemmPlan {
+  int32_t S, sps, spl;
+};
+GemmPlan gemm_plan(const dprc_layer& L) {
+  GemmPlan g;
+  g.sps = (int32_t)ceil_div(L.T, kStage);
+  const int64_t total = L.B * g.sps;
+  const int64_t tiles = ceil_div(L.d, 128) * ceil_div(L.p, 128);
+  int64_t S = 1;
+  if (tiles < 256) S = std::min<int64_t>(ceil_div(512, tiles), std::max<int64_t>(1, total / 8));
+  g.spl = (int32_t)ceil_div(total, S);
+  g.S = (int32_t)ceil_div(total, g.spl);
+  return g;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* dprc_status_string(dprc_status s) {
+  switch (s) {
+    case DPRC_SUCCESS: return "DPRC_SUCCESS";
+    case DPRC_ERROR_INVALID_VALUE: return "DPRC_ERROR_INVALID_VALUE: invalid argument";
+    case DPRC_ERROR_NOT_SUPPORTED: return "DPRC_ERROR_NOT_SUPPORTED: unsupported alignment, stride or size";
+    case DPRC_ERROR_WORKSPACE_TOO_SMALL: return "DPRC_ERROR_WORKSPACE_TOO_SMALL: workspace smaller than the query";
+    case DPRC_ERROR_HIP: return "DPRC_ERROR_HIP: a HIP runtime call or kernel launch failed";
+  }
+  return "unknown dprc_status";
+}
+
+const char* dprc_version(void) { return "dprc 0.1.0 (gfx950)"; }
+
+size_t dprc_norm_hutch_workspace(const dprc_layer* layers, int32_t num_layers, int32_t k, dprc_side side) {
+  if (check_layers(layers, num_layers, side) != DPRC_SUCCESS || k < 1 || k > 256) return 0;
+  size_t need = 0;
+  for (int32_t l = 0; l < num_layers; ++l) need = std::max(need, hutch_layer_ws(view_of(layers[l], side), k));
+  return need;
+}
+
+dprc_status dprc_norm_hutch(const dprc_layer* layers, int32_t num_layers, int32_t k, dprc_probe probe,
+                            uint64_t seed, dprc_side side, float* n2, float* n2_layers, int32_t accumulate,
+                            void* ws, size_t ws_bytes, hipStream_t stream) {
+  dprc_status s = check_layers(layers, num_layers, side);
+  if (s != DPRC_SUCCESS) return s;
+  if (k < 1 || k > 256 || !n2) return DPRC_ERROR_INVALID_VALUE;
+  if (probe != DPRC_PROBE_RADEMACHER && probe != DPRC_PROBE_HADAMARD) return DPRC_ERROR_INVALID_VALUE;
+  const size_t need = dprc_norm_hutch_workspace(layers, num_layers, k, side);
+  if (ws_bytes < need) return DPRC_ERROR_WORKSPACE_TOO_SMALL;
+  if (!ws || !aligned(ws, kAlign)) return DPRC_ERROR_INVALID_VALUE;
+  uint32_t k0, k1;
+  key_of(seed, k0, k1);
+  const int64_t B = layers[0].B;
+  for (int32_t l = 0; l < num_layers; ++l) {
+    s = hutch_layer(view_of(layers[l], side), k, (int)probe, k0, k1, n2,
+                    n2_layers ? n2_layers + (int64_t)l * B : nullptr, (accumulate || l > 0) ? 1 : 0, ws, stream);
+    if (s != DPRC_SUCCESS) return s;
+  }
+  return DPRC_SUCCESS;
+}
+
+size_t dprc_norm_hutchpp_workspace(const dprc_layer* layers, int32_t num_layers, int32_t s, int32_t r,
+                                   dprc_side side) {
+  if (check_layers(layers, num_layers, side) != DPRC_SUCCESS) return 0;
+  if (s < 0 || s > 64 || r < 1 || r > 256 || s + r > 256) return 0;
+  size_t need = 0;
+  for (int32_t l = 0; l < num_layers; ++l) {
+    const View v = view_of(layers[l], side);
+    if (s > v.m) return 0;
+    need = std::max(need, hutchpp_layout(v, s, r, nullptr, nullptr));
+  }
+  return need;
+}
+
+dprc_status dprc_norm_hutchpp(const dprc_layer* layers, int32_t num_layers, int32_t s, int32_t r, uint64_t seed,
+                              dprc_side side, float* n2, float* n2_layers, int32_t accumulate, void* ws,
+                              size_t ws_bytes, hipStream_t stream) {
+  dprc_status st = check_layers(layers, num_layers, side);
+  if (st != DPRC_SUCCESS) return st;
+  if (s < 0 || s > 64 || r < 1 || r > 256 || s + r > 256 || !n2) return DPRC_ERROR_INVALID_VALUE;
+  for (int32_t l = 0; l < num_layers; ++l)
+    if (s > view_of(layers[l], side).m) return DPRC_ERROR_INVALID_VALUE;
+  const size_t need = dprc_norm_hutchpp_workspace(layers, num_layers, s, r, side);
+  if (ws_bytes < need) return DPRC_ERROR_WORKSPACE_TOO_SMALL;
+  if (!ws || !aligned(ws, kAlign)) return DPRC_ERROR_INVALID_VALUE;
+  uint32_t k0, k1;
+  key_of(seed, k0, k1);
+  const int64_t B = layers[0].B;
+  for (int32_t l = 0; l < num_layers; ++l) {
+    st = hutchpp_layer(view_of(layers[l], side), s, r, k0, k1, n2, n2_layers ? n2_layers + (int64_t)l * B : nullptr,
+                       (accumulate || l > 0) ? 1 : 0, ws, stream);
+    if (st != DPRC_SUCCESS) return st;
+  }
+  return DPRC_SUCCESS;
+}
+
+dprc_status dprc_clip_scale(const float* n2, int64_t B, float C, float* c, hipStream_t stream) {
+  if (!n2 || !c || B < 1 || !(C > 0.f) || std::isinf(C)) return DPRC_ERROR_INVALID_VALUE;
+  return hip_status(launch_clip_scale(n2, B, C, c, stream));
+}
+
+size_t dprc_clip_accumulate_workspace(const dprc_layer* L) {
+  if (!L || check_layer(*L) != DPRC_SUCCESS) return 0;
+  if (L->dtype == DPRC_F32) return 0;
+  const GemmPlan g = gemm_plan(*L);
+  return g.S > 1 ? (size_t)g.S * L->d * L->p * sizeof(float) : 0;
+}
+
+dprc_status dprc_clip_accumulate(const dprc_layer* L, const float* c, float* grad, int64_t ldg, int32_t accumulate,
+                                 void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!L) return DPRC_ERROR_INVALID_VALUE;
+  dprc_status s = check_layer(*L);
+  if (s != DPRC_SUCCESS) return s;
+  if (!c || !grad || ldg < L->p) return DPRC_ERROR_INVALID_VALUE;
+  if (L->d * L->p > (1LL << 40)) return DPRC_ERROR_NOT_SUPPORTED;
+  const size_t need = dprc_clip_accumulate_workspace(L);
+  if (ws_bytes < need) return DPRC_ERROR_WORKSPACE_TOO_SMALL;
+  if (need && (!ws || !aligned(ws, kAlign))) return DPRC_ERROR_INVALID_VALUE;
+  if (L->dtype == DPRC_F32)
+    return hip_status(launch_gemm_f32((const float*)L->A, L->lda, L->T * L->lda, (const float*)L->E, L->lde,
+                                      L->T * L->lde, (int32_t)L->B, (int32_t)L->T, (int32_t)L->d, (int32_t)L->p, c,
+                                      grad, ldg, accumulate, stream));
+  const GemmPlan g = gemm_plan(*L);
+  GemmArgs a;
+  a.A = (const uint16_t*)L->A; a.lda = L->lda; a.a_ss = L->T * L->lda;
+  a.E = (const uint16_t*)L->E; a.lde = L->lde; a.e_ss = L->T * L->lde;
+  a.B = (int32_t)L->B; a.T = (int32_t)L->T; a.d = (int32_t)L->d; a.p = (int32_t)L->p;
+  a.c = c; a.out = grad; a.ldo = ldg; a.accumulate = accumulate;
+  a.S = g.S; a.stages_per_sample = g.sps; a.stages_per_split = g.spl;
+  a.part = (float*)ws;
+  a.vec_a = rows16(L->A, L->lda);
+  a.vec_e = rows16(L->E, L->lde);
+  hipError_t e = launch_gemm(a, stream);
+  if (e != hipSuccess) return DPRC_ERROR_HIP;
+  if (g.S > 1) return hip_status(launch_splitk_reduce(a.part, g.S, a.d, a.p, grad, ldg, accumulate, stream));
+  return DPRC_SUCCESS;
+}
+
+dprc_status dprc_add_noise(float* grad, int64_t numel, float sigma, float C, uint64_t seed, uint32_t tensor_id,
+                           hipStream_t stream) {
+  if (numel < 0 || (numel > 0 && !grad)) return DPRC_ERROR_INVALID_VALUE;
+  if (!(sigma >= 0.f) || std::isinf(sigma) || !(C > 0.f) || std::isinf(C)) return DPRC_ERROR_INVALID_VALUE;
+  if (!aligned(grad, 4)) return DPRC_ERROR_NOT_SUPPORTED;
+  if (numel == 0) return DPRC_SUCCESS;
+  uint32_t k0, k1;
+  key_of(seed, k0, k1);
+  return hip_status(launch_noise(grad, numel, sigma * C, k0, k1, tensor_id, stream));
+}
+
+dprc_status dprc_probe_bits(dprc_probe probe, uint64_t seed, uint32_t layer_id, uint32_t stream_id, int64_t m,
+                            int32_t k, uint32_t* out, hipStream_t stream) {
+  if (!out || m < 1 || k < 1 || m > (1LL << 36)) return DPRC_ERROR_INVALID_VALUE;
+  if (probe != DPRC_PROBE_RADEMACHER && probe != DPRC_PROBE_HADAMARD) return DPRC_ERROR_INVALID_VALUE;
+  uint32_t k0, k1;
+  key_of(seed, k0, k1);
+  return hip_status(launch_probe_bits((int)probe, k0, k1, layer_id, stream_id, m, k, out, stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,133 @@
+// Device-side building blocks shared by the dprc kernels (gfx950 / CDNA4).
+//
+//  * Philox4x32-10 (Salmon et al., SC'11) and the probe / noise streams;
+//  * bf16 <-> fp32 conversions and the hi/lo split of an fp32 value into two
+//    bf16 values (operands of the bf16 matrix cores);
+//  * wrappers for the bf16 MFMA with K = 32 and for the LDS transpose read.
+//
+// Lane layouts used below (wave64, checked on gfx950):
+//  mfma 16x16x32 bf16  A[16x32]: lane l holds A[l%16][8*(l/16) + j], j = 0..7
+//                      B[32x16]: lane l holds B[8*(l/16) + j][l%16]
+//                      D[16x16]: lane l holds D[4*(l/16) + i][l%16], i = 0..3
+//  ds_read_tr16_b64    within each 16-lane group, lane 4r+c passes the address
+//                      of 4 consecutive 16-bit elements (row r of a 4x16
+//                      block, columns 4c..4c+3); lane j of the group receives
+//                      column j of the 4 rows.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dprc {
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
+typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4_t;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4_t;
+typedef __attribute__((address_space(3))) bf16x4_t lds_bf16x4_t;
+
+struct u32x4 {
+  uint32_t x, y, z, w;
+};
+
+// ---- Philox4x32-10 -----------------------------------------------------------
+__device__ __forceinline__ u32x4 philox4x32_10(u32x4 c, uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int round = 0; round < 10; ++round) {
+    if (round) {
+      k0 += 0x9E3779B9u;
+      k1 += 0xBB67AE85u;
+    }
+    const uint32_t a = c.x, b = c.z;
+    const uint32_t lo0 = 0xD2511F53u * a, hi0 = __umulhi(0xD2511F53u, a);
+    const uint32_t lo1 = 0xCD9E8D57u * b, hi1 = __umulhi(0xCD9E8D57u, b);
+    c = u32x4{hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0};
+  }
+  return c;
+}
+
+enum : uint32_t { kStreamProbe = 0, kStreamSketch = 1, kStreamNoise = 2 };
+enum : int { kProbeRademacher = 0, kProbeHadamard = 1 };
+
+// Four consecutive probe words (rows 128*blk .. 128*blk+127) of column j.
+__device__ __forceinline__ u32x4 rademacher_block(uint32_t key0, uint32_t key1, uint32_t layer,
+                                                  uint32_t stream, uint32_t blk, uint32_t col) {
+  return philox4x32_10(u32x4{blk, col, layer, stream}, key0, key1);
+}
+
+// Word w (rows 32w .. 32w+31) of column j of the Sylvester-Hadamard sign pattern.
+__device__ __forceinline__ uint32_t hadamard_word(uint32_t w, uint32_t col) {
+  uint32_t pat = 0;
+#pragma unroll
+  for (uint32_t b = 0; b < 32; ++b) pat |= (uint32_t)(__popc(b & col) & 1) << b;
+  const uint32_t hi = (uint32_t)(__popc((w << 5) & col) & 1);
+  return hi ? ~pat : pat;
+}
+
+__device__ __forceinline__ uint32_t tail_mask(int64_t m, int64_t w) {
+  const int64_t rem = m - 32 * w;
+  return rem >= 32 ? 0xFFFFFFFFu : (rem <= 0 ? 0u : ((1u << rem) - 1u));
+}
+
+// ---- bf16 ----------------------------------------------------------------------
+__device__ __forceinline__ float bf16_to_f32(uint32_t h) { return __uint_as_float(h << 16); }
+
+// round to nearest even; NaN stays NaN
+__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (u >> 16) | 0x40u;
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+// f = hi + lo + O(2^-17 |f|), both bf16
+__device__ __forceinline__ void split_bf16(float f, uint32_t& hi, uint32_t& lo) {
+  hi = f32_to_bf16(f);
+  lo = f32_to_bf16(f - bf16_to_f32(hi));
+}
+
+// 8 signs (bit set -> -1) to 8 bf16 values +-1 packed in four dwords
+__device__ __forceinline__ uint4 signs_to_bf16x8(uint32_t byte) {
+  uint4 r;
+  r.x = 0x3F803F80u | ((byte & 1u) << 15) | ((byte & 2u) << 30);
+  r.y = 0x3F803F80u | ((byte & 4u) << 13) | ((byte & 8u) << 28);
+  r.z = 0x3F803F80u | ((byte & 16u) << 11) | ((byte & 32u) << 26);
+  r.w = 0x3F803F80u | ((byte & 64u) << 9) | ((byte & 128u) << 24);
+  return r;
+}
+
+// Eight consecutive bf16 of a token row starting at column u (u a multiple of 8),
+// zero past `lim`; 16-byte load when the row is 16-byte aligned, element loads otherwise.
+__device__ __forceinline__ uint4 load_bf16x8(const uint16_t* row, int64_t u, int64_t lim, bool vec) {
+  if (u >= lim) return uint4{0, 0, 0, 0};
+  if (vec && u + 8 <= lim) return *reinterpret_cast<const uint4*>(row + u);
+  uint32_t h[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) h[j] = (u + j < lim) ? (uint32_t)row[u + j] : 0u;
+  return uint4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
+}
+
+// ---- matrix cores and LDS ------------------------------------------------------------
+__device__ __forceinline__ f32x4_t mfma16x16x32(const uint4& a, const uint4& b, f32x4_t c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                  __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+}
+
+__device__ __forceinline__ uint2 lds_read_tr16(const uint16_t* p) {
+  bf16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(p));
+  return __builtin_bit_cast(uint2, v);
+}
+
+__device__ __forceinline__ uint4 make_u4(uint2 a, uint2 b) { return uint4{a.x, a.y, b.x, b.y}; }
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+}  // namespace dprc

@@ -1,0 +1,138 @@
+// Kernel argument blocks and launch wrappers (host <-> device interface inside
+// the library).  Every launch wrapper enqueues on the given stream and returns
+// hipGetLastError().
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dprc {
+
+constexpr int kWave = 64;
+constexpr int kBlock = 256;        // threads per workgroup of the streaming kernels
+constexpr int kStage = 64;         // tokens per pipeline stage of the token reduction
+constexpr int kTile = 128;         // result rows per token-reduction workgroup
+constexpr int kLdsLd = kTile + 8;  // padded LDS row (elements) of a staged 64 x 128 bf16 tile
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
+
+// Y = X R on matrix cores.  X: bf16 token rows [B][T][ldx] (width m).  R has
+// `nd` dense columns per sample (bf16 hi/lo pairs, Rhi/Rlo[i][c][ld_r]) followed
+// by `nz` generated +-1 columns.  Output Yt: bf16 hi/lo, column-major per
+// sample: Yt[h][c][i*T_pad + t], h = 0 hi, 1 lo; zero for t >= T and for
+// columns >= nd + nz.
+struct ProjectArgs {
+  const uint16_t* X;
+  int64_t ldx, x_ss;
+  int32_t B, T, m, T_pad;
+  int32_t nd, nz, ncols_pad;
+  const uint16_t* Rhi;
+  const uint16_t* Rlo;
+  int64_t ld_r, r_ss;
+  int32_t probe_kind;
+  uint32_t key0, key1, layer_id, stream_id;
+  int32_t words_per_chunk;  // probe words per column staged in LDS at a time
+  uint16_t* Yt;
+  int64_t yt_ld;            // B * T_pad
+  uint32_t* zero_ptr;       // counters cleared by workgroup (0,0) (may be null)
+  int32_t zero_count;
+  int32_t vec;              // token rows of X are 16-byte aligned: 16-byte loads
+};
+
+// M_i = X_i^T Y_i per sample (result rows = the n columns of X; result
+// columns = the ncols columns of Y), reduced over tokens in splits.
+// mode 0: squared-norm estimate -> n2; mode 1: store M (fp32 and/or bf16 hi/lo).
+struct TokredArgs {
+  const uint16_t* X;
+  int64_t ldx, x_ss;
+  int32_t B, T, n;
+  const uint16_t* Yt;
+  int64_t yt_ld;
+  int32_t T_pad, ncols, ncols_pad;
+  int32_t ntiles, S, stages_per_split;
+  int32_t mode;
+  float* part;            // [B][ntiles][S][ncols_pad][kTile] (S > 1)
+  uint32_t* cnt_tile;     // [B][ntiles]
+  float* tilesq;          // [B][ntiles]
+  uint32_t* cnt_sample;   // [B]
+  float scale;            // estimate = scale * ||M_i||^2
+  float* n2;
+  float* n2_layer;
+  int32_t accumulate;
+  float* M;               // M[i*m_ss + c*m_ld + j]
+  int64_t m_ld, m_ss;
+  uint16_t* Mhi;          // Mhi/Mlo[i*mh_ss + c*mh_ld + j]
+  uint16_t* Mlo;
+  int64_t mh_ld, mh_ss;
+  int32_t vec;            // token rows of X are 16-byte aligned
+};
+
+struct GemmArgs {
+  const uint16_t* A;
+  int64_t lda, a_ss;
+  const uint16_t* E;
+  int64_t lde, e_ss;
+  int32_t B, T, d, p;
+  const float* c;
+  float* out;
+  int64_t ldo;
+  int32_t accumulate;
+  int32_t S, stages_per_sample, stages_per_split;
+  float* part;            // [S][d][p] (S > 1)
+  int32_t vec_a, vec_e;   // token rows 16-byte aligned
+};
+
+// fp32 (SIMT) variants, used for fp32 inputs.
+struct ProjectF32Args {
+  const float* X;
+  int64_t ldx, x_ss;
+  int32_t B, T, m;
+  int32_t nd, nz, ncols;
+  const float* Rd;        // dense columns [i][c][ld_r]
+  int64_t ld_r, r_ss;
+  const uint32_t* zbits;  // generated columns, packed [c][ceil(m/32)]
+  float* Y;               // [B][T][ncols]
+};
+
+struct TokredF32Args {
+  const float* X;
+  int64_t ldx, x_ss;
+  int32_t B, T, n;
+  const float* Y;         // [B][T][ncols]
+  int32_t ncols;
+  float* M;               // M[i*m_ss + c*m_ld + j]
+  int64_t m_ld, m_ss;
+};
+
+hipError_t launch_probe_bits(int probe_kind, uint32_t key0, uint32_t key1, uint32_t layer,
+                             uint32_t stream_id, int64_t m, int32_t k, uint32_t* out,
+                             hipStream_t st);
+hipError_t launch_fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t st);
+hipError_t launch_project(const ProjectArgs& a, int rows_per_wg, hipStream_t st);
+hipError_t launch_tokred(const TokredArgs& a, hipStream_t st);
+hipError_t launch_project_f32(const ProjectF32Args& a, hipStream_t st);
+hipError_t launch_tokred_f32(const TokredF32Args& a, hipStream_t st);
+// n2 (=|+=) scale * sum_{c<ncols, j<n} M[i][c][j]^2 (+ optional per-layer copy)
+hipError_t launch_sample_sq(const float* M, int64_t m_ld, int64_t m_ss, int32_t B, int32_t ncols,
+                            int32_t n, float scale, float* n2, float* n2_layer, int accumulate,
+                            hipStream_t st);
+hipError_t launch_qr(const float* OS, int64_t os_ld, int64_t os_ss, int32_t B, int32_t m,
+                     int32_t s, double* work, float* Q, int64_t q_ld, int64_t q_ss, uint16_t* Qhi,
+                     uint16_t* Qlo, int64_t qh_ld, int64_t qh_ss, hipStream_t st);
+hipError_t launch_hutchpp_final(const float* UW, int64_t uw_ld, int64_t uw_ss, const float* Q,
+                                int64_t q_ld, int64_t q_ss, int32_t B, int32_t n, int32_t m,
+                                int32_t s, int32_t r, uint32_t key0, uint32_t key1,
+                                uint32_t layer, float* n2, float* n2_layer, int accumulate,
+                                hipStream_t st);
+hipError_t launch_clip_scale(const float* n2, int64_t B, float C, float* c, hipStream_t st);
+hipError_t launch_gemm(const GemmArgs& a, hipStream_t st);
+hipError_t launch_gemm_f32(const float* A, int64_t lda, int64_t a_ss, const float* E, int64_t lde,
+                           int64_t e_ss, int32_t B, int32_t T, int32_t d, int32_t p,
+                           const float* c, float* out, int64_t ldo, int accumulate,
+                           hipStream_t st);
+hipError_t launch_splitk_reduce(const float* part, int32_t S, int32_t d, int32_t p, float* out,
+                                int64_t ldo, int accumulate, hipStream_t st);
+hipError_t launch_noise(float* g, int64_t numel, float scale, uint32_t key0, uint32_t key1,
+                        uint32_t tensor_id, hipStream_t st);
+
+}  // namespace dprc

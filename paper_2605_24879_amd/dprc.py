@@ -1,0 +1,204 @@
+"""Python binding of libdprc (include/dprc.h): argument marshalling only.
+
+Each function has the name of the C entry point it calls and takes torch
+tensors on the GPU; every step of the computation runs in the HIP kernels of
+libdprc.so.  Outputs and workspaces that the caller does not pass are
+allocated with torch on the tensors' device, and calls are enqueued on torch's
+current stream.  A missing library or a non-zero dprc_status raises
+RuntimeError; there is no fallback.
+"""
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libdprc.so")
+
+SUCCESS = 0
+F32, BF16 = 0, 1
+SIDE_OUT, SIDE_IN, SIDE_AUTO = 0, 1, 2
+PROBE_RADEMACHER, PROBE_HADAMARD = 0, 1
+STREAM_PROBE, STREAM_SKETCH, STREAM_NOISE = 0, 1, 2
+
+EXPORTS = ["dprc_norm_hutch_workspace", "dprc_norm_hutch", "dprc_norm_hutchpp_workspace",
+           "dprc_norm_hutchpp", "dprc_clip_scale", "dprc_clip_accumulate_workspace",
+           "dprc_clip_accumulate", "dprc_add_noise", "dprc_probe_bits", "dprc_status_string",
+           "dprc_version"]
+
+
+class Layer(ctypes.Structure):
+    """Mirror of dprc_layer."""
+    _fields_ = [("A", ctypes.c_void_p), ("E", ctypes.c_void_p),
+                ("B", ctypes.c_int64), ("T", ctypes.c_int64), ("d", ctypes.c_int64), ("p", ctypes.c_int64),
+                ("lda", ctypes.c_int64), ("lde", ctypes.c_int64),
+                ("dtype", ctypes.c_int), ("layer_id", ctypes.c_uint32)]
+
+
+_lib = None
+
+
+def lib():
+    """Load libdprc.so (built in-tree by paper_2605_24879_amd.build)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2605_24879_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        P, I32, I64, U32, U64, F, SZ = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32,
+                                         ctypes.c_uint64, ctypes.c_float, ctypes.c_size_t)
+        LP = ctypes.POINTER(Layer)
+        sig = {
+            "dprc_norm_hutch_workspace": (SZ, [LP, I32, I32, ctypes.c_int]),
+            "dprc_norm_hutch": (ctypes.c_int, [LP, I32, I32, ctypes.c_int, U64, ctypes.c_int, P, P, I32, P, SZ, P]),
+            "dprc_norm_hutchpp_workspace": (SZ, [LP, I32, I32, I32, ctypes.c_int]),
+            "dprc_norm_hutchpp": (ctypes.c_int, [LP, I32, I32, I32, U64, ctypes.c_int, P, P, I32, P, SZ, P]),
+            "dprc_clip_scale": (ctypes.c_int, [P, I64, F, P, P]),
+            "dprc_clip_accumulate_workspace": (SZ, [LP]),
+            "dprc_clip_accumulate": (ctypes.c_int, [LP, P, P, I64, I32, P, SZ, P]),
+            "dprc_add_noise": (ctypes.c_int, [P, I64, F, F, U64, U32, P]),
+            "dprc_probe_bits": (ctypes.c_int, [ctypes.c_int, U64, U32, U32, I64, I32, P, P]),
+            "dprc_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+            "dprc_version": (ctypes.c_char_p, []),
+        }
+        for name, (res, args) in sig.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _check(status):
+    if status != SUCCESS:
+        raise RuntimeError(lib().dprc_status_string(status).decode())
+
+
+def _stream(dev):
+    return ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
+
+
+def _dtype_code(t):
+    if t.dtype == torch.bfloat16:
+        return BF16
+    if t.dtype == torch.float32:
+        return F32
+    raise TypeError(f"unsupported dtype {t.dtype}; use bfloat16 or float32")
+
+
+def make_layer(A, E, layer_id):
+    """dprc_layer for activations A [B,T,d] and output gradients E [B,T,p] (token rows)."""
+    if A.dim() != 3 or E.dim() != 3:
+        raise ValueError("A and E must be [B, T, features]")
+    if not (A.is_cuda and E.is_cuda):
+        raise ValueError("A and E must be GPU tensors")
+    if A.dtype != E.dtype:
+        raise TypeError("A and E must share a dtype")
+    B, T, d = A.shape
+    if E.shape[0] != B or E.shape[1] != T:
+        raise ValueError("A and E must agree on B and T")
+    p = E.shape[2]
+    for X in (A, E):
+        if X.stride(2) != 1 or X.stride(0) != T * X.stride(1):
+            raise ValueError("tensors must have contiguous features, token rows of stride ld, samples of stride T*ld")
+    return Layer(A.data_ptr(), E.data_ptr(), B, T, d, p, A.stride(1), E.stride(1), _dtype_code(A), layer_id)
+
+
+def _layers(pairs):
+    """pairs: list of (A, E, layer_id); returns (ctypes array, count, B, device)."""
+    arr = (Layer * len(pairs))(*[make_layer(A, E, lid) for (A, E, lid) in pairs])
+    return arr, len(pairs), pairs[0][0].shape[0], pairs[0][0].device
+
+
+def _workspace(nbytes, dev, ws):
+    if ws is not None:
+        if ws.numel() * ws.element_size() < nbytes:
+            raise ValueError("workspace too small")
+        return ws
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=dev)
+
+
+def dprc_norm_hutch_workspace(pairs, k, side=SIDE_OUT):
+    arr, nl, _, _ = _layers(pairs)
+    return lib().dprc_norm_hutch_workspace(arr, nl, k, side)
+
+
+def dprc_norm_hutch(pairs, k, seed, side=SIDE_OUT, probe=PROBE_RADEMACHER, n2=None, n2_layers=None,
+                    accumulate=False, ws=None):
+    """Hutchinson estimates summed over layers: returns n2 [B] (fp32).  pairs = [(A, E, layer_id), ...]."""
+    arr, nl, B, dev = _layers(pairs)
+    if n2 is None:
+        n2 = torch.zeros(B, dtype=torch.float32, device=dev)
+    need = lib().dprc_norm_hutch_workspace(arr, nl, k, side)
+    ws = _workspace(need, dev, ws)
+    _check(lib().dprc_norm_hutch(arr, nl, k, probe, seed, side, n2.data_ptr(),
+                                 n2_layers.data_ptr() if n2_layers is not None else None,
+                                 int(bool(accumulate)), ws.data_ptr(), need, _stream(dev)))
+    return n2
+
+
+def dprc_norm_hutchpp_workspace(pairs, s, r, side=SIDE_OUT):
+    arr, nl, _, _ = _layers(pairs)
+    return lib().dprc_norm_hutchpp_workspace(arr, nl, s, r, side)
+
+
+def dprc_norm_hutchpp(pairs, s, r, seed, side=SIDE_OUT, n2=None, n2_layers=None, accumulate=False, ws=None):
+    """Hutch++ estimates summed over layers: returns n2 [B] (fp32)."""
+    arr, nl, B, dev = _layers(pairs)
+    if n2 is None:
+        n2 = torch.zeros(B, dtype=torch.float32, device=dev)
+    need = lib().dprc_norm_hutchpp_workspace(arr, nl, s, r, side)
+    ws = _workspace(need, dev, ws)
+    _check(lib().dprc_norm_hutchpp(arr, nl, s, r, seed, side, n2.data_ptr(),
+                                   n2_layers.data_ptr() if n2_layers is not None else None,
+                                   int(bool(accumulate)), ws.data_ptr(), need, _stream(dev)))
+    return n2
+
+
+def dprc_clip_scale(n2, C, c=None):
+    if c is None:
+        c = torch.empty_like(n2)
+    _check(lib().dprc_clip_scale(n2.data_ptr(), n2.numel(), float(C), c.data_ptr(), _stream(n2.device)))
+    return c
+
+
+def dprc_clip_accumulate_workspace(A, E):
+    return lib().dprc_clip_accumulate_workspace(ctypes.byref(make_layer(A, E, 0)))
+
+
+def dprc_clip_accumulate(A, E, c, grad=None, accumulate=False, ws=None):
+    """grad [d, p] (fp32) (=|+=) sum_i c_i A_i^T E_i."""
+    L = make_layer(A, E, 0)
+    if grad is None:
+        grad = torch.empty(A.shape[2], E.shape[2], dtype=torch.float32, device=A.device)
+    if grad.stride(1) != 1:
+        raise ValueError("grad must have contiguous rows")
+    need = lib().dprc_clip_accumulate_workspace(ctypes.byref(L))
+    ws = _workspace(need, A.device, ws) if need else None
+    _check(lib().dprc_clip_accumulate(ctypes.byref(L), c.data_ptr(), grad.data_ptr(), grad.stride(0),
+                                      int(bool(accumulate)), ws.data_ptr() if ws is not None else None,
+                                      need, _stream(A.device)))
+    return grad
+
+
+def dprc_add_noise(grad, sigma, C, seed, tensor_id):
+    """grad += sigma * C * N(0, I) in place (grad contiguous fp32)."""
+    if not grad.is_contiguous() or grad.dtype != torch.float32:
+        raise ValueError("grad must be contiguous fp32")
+    _check(lib().dprc_add_noise(grad.data_ptr(), grad.numel(), float(sigma), float(C), seed, tensor_id,
+                                _stream(grad.device)))
+    return grad
+
+
+def dprc_probe_bits(probe, seed, layer_id, stream_id, m, k, device="cuda", out=None):
+    """Packed probe words [k, ceil(m/32)] (int32 view of the uint32 words)."""
+    nw = (m + 31) // 32
+    if out is None:
+        out = torch.empty(k, nw, dtype=torch.int32, device=device)
+    _check(lib().dprc_probe_bits(probe, seed, layer_id, stream_id, m, k, out.data_ptr(), _stream(out.device)))
+    return out
+
+
+def dprc_version():
+    return lib().dprc_version().decode()

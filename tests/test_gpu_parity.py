@@ -1,0 +1,233 @@
+"""GPU parity of libdprc against the CPU oracle on identical seeded inputs.
+
+Sizes span several tiles with ragged tails (token counts, widths and probe
+counts that are not multiples of the kernels' tiles).  Tolerances: probe bits
+bit-exact; squared-norm estimates 1e-3 relative; clipped gradients 2e-3
+relative Frobenius; noise 1e-5 * sigma * C absolute on the added term.
+"""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import philox
+from oracle import estimators as est
+import workloads
+
+pytestmark = pytest.mark.gpu
+
+NORM_RTOL = 1e-3
+GRAD_RTOL = 2e-3
+
+
+@pytest.fixture(scope="module")
+def D():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2605_24879_amd import dprc
+    dprc.lib()
+    return dprc
+
+
+def _draw(B, T, d, p, dtype="bf16", law="lognormal", layer=0, seed=0, **kw):
+    return workloads.draw(B, T, d, p, dtype=dtype, law=law, seed=seed, layer=layer, device="cuda", **kw)
+
+
+def _np(x):
+    return est.as_f64(x)
+
+
+def _rel(a, b):
+    a, b = np.asarray(a, dtype=np.float64), np.asarray(b, dtype=np.float64)
+    return np.abs(a - b) / np.maximum(np.abs(b), 1e-300)
+
+
+def _hadamard_words(m, k):
+    H = philox.hadamard_matrix(m, k)           # +-1
+    bits = (H < 0).astype(np.uint64).T         # [k, m]
+    nw = (m + 31) // 32
+    out = np.zeros((k, nw), dtype=np.uint64)
+    for u in range(m):
+        out[:, u // 32] |= bits[:, u] << np.uint64(u % 32)
+    return out.astype(np.uint32)
+
+
+# ---- probe bits --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed,layer,stream,m,k", [
+    (0, 0, 0, 48, 4), (0, 3, 1, 2048, 16), (12345678901234, 7, 0, 45, 3), (5, 112, 0, 128256, 2),
+    (2**64 - 1, 2**32 - 1, 2, 100, 33), (9, 1, 0, 1, 1), (9, 1, 0, 130, 1)])
+def test_probe_bits_bitexact(D, seed, layer, stream, m, k):
+    got = D.dprc_probe_bits(D.PROBE_RADEMACHER, seed, layer, stream, m, k).cpu().numpy().view(np.uint32)
+    ref = philox.rademacher_words(seed, layer, stream, m, k)
+    assert np.array_equal(got, ref)
+
+
+@pytest.mark.parametrize("m,k", [(64, 64), (48, 64), (100, 7)])
+def test_hadamard_bits_bitexact(D, m, k):
+    got = D.dprc_probe_bits(D.PROBE_HADAMARD, 0, 0, 0, m, k).cpu().numpy().view(np.uint32)
+    assert np.array_equal(got, _hadamard_words(m, k))
+
+
+# ---- Hutchinson ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("B,T,d,p,k,side", [
+    (3, 200, 300, 260, 16, 0),     # ragged tokens / widths, 3 x 3 tiles
+    (2, 130, 72, 520, 5, 1),       # side IN, odd k
+    (2, 96, 520, 72, 33, 2),       # AUTO -> IN (d > p), 3 column blocks
+    (1, 1, 8, 8, 1, 0),            # a single token
+    (2, 64, 64, 48, 4, 0),         # the tiny workload's shape in bf16
+])
+def test_hutch_parity_bf16(D, B, T, d, p, k, side):
+    A, E = _draw(B, T, d, p, layer=1)
+    n2l = torch.zeros(1, B, device="cuda")
+    n2 = D.dprc_norm_hutch([(A, E, 1)], k, 42, side=side, n2_layers=n2l)
+    ref = est.hutch_layer(_np(A), _np(E), k, 42, 1, side=side)
+    assert np.all(_rel(n2.cpu().numpy(), ref) < NORM_RTOL)
+    assert torch.equal(n2, n2l[0])
+
+
+def test_hutch_tiny_workload_fp32(D):
+    cfg = workloads.BY_NAME["tiny"]
+    A, E = workloads.layer_inputs(cfg, 0, device="cuda")
+    n2 = D.dprc_norm_hutch([(A, E, 0)], cfg["k"], 0)
+    ref = est.hutch_layer(_np(A), _np(E), cfg["k"], 0, 0)
+    assert np.all(_rel(n2.cpu().numpy(), ref) < NORM_RTOL)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("side", [0, 1])
+def test_hutch_hadamard_probes_give_exact_norm(D, dtype, side):
+    # 64 Sylvester-Hadamard columns span the sketched dimension (<= 64): estimate == ||A_i^T E_i||^2
+    A, E = _draw(2, 150, 64, 48, dtype=dtype, layer=3)
+    n2 = D.dprc_norm_hutch([(A, E, 0)], 64, 0, side=side, probe=D.PROBE_HADAMARD)
+    exact = est.exact_layer(_np(A), _np(E))
+    assert np.all(_rel(n2.cpu().numpy(), exact) < NORM_RTOL)
+
+
+def test_hutch_token_splits_and_multilayer(D):
+    # long token range -> several token splits per tile; two layers summed on top of a prior n2
+    A1, E1 = _draw(2, 3000, 256, 200, layer=0)
+    A2, E2 = _draw(2, 700, 136, 1100, layer=1)
+    n2 = torch.tensor([1.5, 2.5], device="cuda")
+    n2l = torch.zeros(2, 2, device="cuda")
+    D.dprc_norm_hutch([(A1, E1, 10), (A2, E2, 11)], 16, 7, n2=n2, n2_layers=n2l, accumulate=True)
+    r1 = est.hutch_layer(_np(A1), _np(E1), 16, 7, 10)
+    r2 = est.hutch_layer(_np(A2), _np(E2), 16, 7, 11)
+    got = n2l.cpu().numpy()
+    assert np.all(_rel(got[0], r1) < NORM_RTOL) and np.all(_rel(got[1], r2) < NORM_RTOL)
+    assert np.all(_rel(n2.cpu().numpy(), np.array([1.5, 2.5]) + r1 + r2) < NORM_RTOL)
+
+
+def test_hutch_strided_rows(D):
+    A, E = _draw(2, 100, 120, 90, layer=5, row_pad_a=8, row_pad_e=38)
+    assert A.stride(1) == 128 and E.stride(1) == 128
+    n2 = D.dprc_norm_hutch([(A, E, 2)], 8, 1)
+    ref = est.hutch_layer(_np(A), _np(E), 8, 1, 2)
+    assert np.all(_rel(n2.cpu().numpy(), ref) < NORM_RTOL)
+
+
+def test_hutch_deterministic(D):
+    A, E = _draw(2, 2048, 512, 384, layer=4)
+    a = D.dprc_norm_hutch([(A, E, 3)], 16, 9)
+    b = D.dprc_norm_hutch([(A, E, 3)], 16, 9)
+    assert torch.equal(a, b)
+
+
+# ---- Hutch++ ------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("B,T,d,p,s,r,side,dtype", [
+    (2, 300, 200, 150, 8, 12, 0, "bf16"),
+    (1, 520, 136, 300, 16, 32, 1, "bf16"),
+    (2, 64, 64, 48, 4, 4, 0, "f32"),
+])
+def test_hutchpp_parity(D, B, T, d, p, s, r, side, dtype):
+    A, E = _draw(B, T, d, p, dtype=dtype, law="student_t", layer=2)
+    n2 = D.dprc_norm_hutchpp([(A, E, 6)], s, r, 3, side=side)
+    ref = est.hutchpp_layer(_np(A), _np(E), s, r, 3, 6, side=side)
+    assert np.all(_rel(n2.cpu().numpy(), ref) < NORM_RTOL)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_hutchpp_low_rank_is_exact(D, dtype):
+    A, E = _draw(2, 12, 80, 96, dtype=dtype, layer=7)      # rank(A_i^T E_i) <= 12 <= s
+    n2 = D.dprc_norm_hutchpp([(A, E, 0)], 16, 8, 11)
+    exact = est.exact_layer(_np(A), _np(E))
+    assert np.all(_rel(n2.cpu().numpy(), exact) < NORM_RTOL)
+
+
+def test_hutchpp_without_sketch_equals_hutch(D):
+    A, E = _draw(2, 300, 100, 180, layer=8)
+    a = D.dprc_norm_hutchpp([(A, E, 4)], 0, 16, 5)
+    b = D.dprc_norm_hutch([(A, E, 4)], 16, 5)
+    assert torch.equal(a, b)
+
+
+# ---- clip factors, accumulation, noise --------------------------------------------------------
+
+def test_clip_scale_edges(D):
+    C = 2.0
+    vals = [0.0, 4.0, 16.0, 1.0, math.inf, math.nan, -1.0, 1e30, 3.9999998]
+    n2 = torch.tensor(vals, dtype=torch.float32, device="cuda")
+    c = D.dprc_clip_scale(n2, C).cpu().numpy()
+    ref = est.clip_scale(np.array(vals, dtype=np.float32).astype(np.float64), C)
+    assert np.all(np.abs(c - ref) <= 1e-6 * np.maximum(ref, 1e-30))
+
+
+@pytest.mark.parametrize("B,T,d,p,dtype", [
+    (3, 150, 200, 260, "bf16"),     # ragged tiles; per-sample scaling inside a tile
+    (2, 2000, 96, 72, "bf16"),      # few tiles -> split over samples and tokens
+    (2, 64, 64, 48, "f32"),         # the tiny workload
+])
+def test_clip_accumulate_parity(D, B, T, d, p, dtype):
+    A, E = _draw(B, T, d, p, dtype=dtype, layer=9)
+    cvals = [0.25, 0.0, 0.8][:B] if B == 3 else [0.37, 1.0]
+    c = torch.tensor(cvals, dtype=torch.float32, device="cuda")
+    g = D.dprc_clip_accumulate(A, E, c)
+    ref = est.clip_accumulate(_np(A), _np(E), np.array(cvals, dtype=np.float32).astype(np.float64))
+    err = np.linalg.norm(g.cpu().numpy() - ref) / np.linalg.norm(ref)
+    assert err < GRAD_RTOL
+    # accumulate onto an existing gradient
+    g0 = torch.full_like(g, 0.5)
+    D.dprc_clip_accumulate(A, E, c, grad=g0, accumulate=True)
+    err2 = np.linalg.norm(g0.cpu().numpy() - (ref + 0.5)) / np.linalg.norm(ref + 0.5)
+    assert err2 < GRAD_RTOL
+
+
+def test_clip_accumulate_zero_factor_drops_nonfinite_sample(D):
+    A, E = _draw(2, 100, 64, 64, layer=10)
+    A[1, 3, 5] = float("nan")
+    E[1, 7, 9] = float("inf")
+    c = torch.tensor([0.5, 0.0], device="cuda")
+    g = D.dprc_clip_accumulate(A, E, c).cpu().numpy()
+    assert np.all(np.isfinite(g))
+    ref = est.clip_accumulate(_np(A)[:1], _np(E)[:1], [0.5])
+    assert np.linalg.norm(g - ref) / np.linalg.norm(ref) < GRAD_RTOL
+
+
+def test_clip_accumulate_all_zero_factors(D):
+    A, E = _draw(2, 70, 40, 30, layer=11)
+    g = D.dprc_clip_accumulate(A, E, torch.zeros(2, device="cuda"))
+    assert torch.count_nonzero(g) == 0
+
+
+@pytest.mark.parametrize("numel,offset", [(1000, 0), (1023, 0), (7, 1)])
+def test_add_noise_parity(D, numel, offset):
+    sigma, C = 0.8, 1.0
+    base = torch.randn(numel + offset, device="cuda", generator=torch.Generator("cuda").manual_seed(1))
+    g = base[offset:].clone() if offset == 0 else base[offset:]
+    g0 = g.clone().cpu().numpy().astype(np.float64)
+    D.dprc_add_noise(g, sigma, C, 77, 5)
+    ref = est.add_noise(g0, sigma, C, 77, 5)
+    assert np.max(np.abs(g.cpu().numpy() - ref)) <= 1e-5 * sigma * C + 4e-7 * np.max(np.abs(ref))
+
+
+def test_add_noise_moments(D):
+    g = torch.zeros(1 << 22, device="cuda")
+    D.dprc_add_noise(g, 1.0, 1.0, 3, 9)
+    x = g.double()
+    n = x.numel()
+    assert abs(x.mean().item()) < 5 / math.sqrt(n)
+    assert abs(x.var().item() - 1.0) < 5 * math.sqrt(2.0 / n)

@@ -1,0 +1,108 @@
+"""Host-side checks of libdprc that need no GPU: the library loads, exports every
+entry point declared in include/dprc.h, and rejects bad arguments before it
+enqueues anything (so these calls never reach a kernel)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2605_24879_amd import dprc
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dprc.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(dprc.LIB_PATH), reason="libdprc.so not built")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dprc_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert len(names) >= 11
+    L = dprc.lib()
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(dprc.EXPORTS)
+
+
+def test_version_and_status_strings():
+    assert "gfx950" in dprc.dprc_version()
+    L = dprc.lib()
+    for code in range(5):
+        assert L.dprc_status_string(code).decode().startswith("DPRC_")
+
+
+def _fake_layer(**kw):
+    # device pointers are never dereferenced on the host; these calls fail validation first
+    base = dict(A=0x10000, E=0x20000, B=2, T=64, d=64, p=48, lda=64, lde=48, dtype=dprc.BF16, layer_id=0)
+    base.update(kw)
+    return dprc.Layer(base["A"], base["E"], base["B"], base["T"], base["d"], base["p"], base["lda"],
+                      base["lde"], base["dtype"], base["layer_id"])
+
+
+def _hutch(layer, k=4, ws_bytes=0, ws=0x30000, n2=0x40000, side=0, probe=0, nl=1):
+    L = dprc.lib()
+    arr = (dprc.Layer * 1)(layer)
+    return L.dprc_norm_hutch(arr, nl, k, probe, 0, side, n2, None, 0, ws, ws_bytes, None)
+
+
+def test_hutch_argument_validation():
+    L = dprc.lib()
+    assert L.dprc_norm_hutch(None, 1, 4, 0, 0, 0, 0x40000, None, 0, 0x30000, 1 << 30, None) == 1
+    assert _hutch(_fake_layer(), nl=0, ws_bytes=1 << 30) == 1
+    assert _hutch(_fake_layer(B=0), ws_bytes=1 << 30) == 1
+    assert _hutch(_fake_layer(T=-1), ws_bytes=1 << 30) == 1
+    assert _hutch(_fake_layer(lda=32), ws_bytes=1 << 30) == 1
+    assert _hutch(_fake_layer(dtype=7), ws_bytes=1 << 30) == 1
+    assert _hutch(_fake_layer(A=0), ws_bytes=1 << 30) == 1
+    assert _hutch(_fake_layer(), k=0, ws_bytes=1 << 30) == 1
+    assert _hutch(_fake_layer(), k=257, ws_bytes=1 << 30) == 1
+    assert _hutch(_fake_layer(), n2=0, ws_bytes=1 << 30) == 1
+    assert _hutch(_fake_layer(), side=5, ws_bytes=1 << 30) == 1
+    assert _hutch(_fake_layer(), probe=9, ws_bytes=1 << 30) == 1
+    # element alignment (any row stride is accepted; 16-byte aligned rows take the vector path)
+    assert _hutch(_fake_layer(A=0x10001), ws_bytes=1 << 30) == 2
+    assert _hutch(_fake_layer(E=0x20003), ws_bytes=1 << 30) == 2
+    assert _hutch(_fake_layer(dtype=dprc.F32, A=0x10002), ws_bytes=1 << 30) == 2
+    # workspace
+    need = L.dprc_norm_hutch_workspace((dprc.Layer * 1)(_fake_layer()), 1, 4, 0)
+    assert need > 0
+    assert _hutch(_fake_layer(), ws_bytes=need - 1) == 3
+    assert _hutch(_fake_layer(), ws=0, ws_bytes=need) == 1
+    assert _hutch(_fake_layer(), ws=0x30010, ws_bytes=need) == 1        # not 256-byte aligned
+
+
+def test_hutchpp_and_accumulate_validation():
+    L = dprc.lib()
+    arr = (dprc.Layer * 1)(_fake_layer())
+    assert L.dprc_norm_hutchpp_workspace(arr, 1, 16, 32, 0) > 0
+    assert L.dprc_norm_hutchpp(arr, 1, 65, 4, 0, 0, 0x40000, None, 0, 0x30000, 1 << 30, None) == 1
+    assert L.dprc_norm_hutchpp(arr, 1, 4, 0, 0, 0, 0x40000, None, 0, 0x30000, 1 << 30, None) == 1
+    assert L.dprc_norm_hutchpp(arr, 1, 49, 4, 0, 0, 0x40000, None, 0, 0x30000, 1 << 30, None) == 1  # s > p
+    assert L.dprc_norm_hutchpp(arr, 1, 4, 4, 0, 0, 0x40000, None, 0, 0x30000, 0, None) == 3
+    lay = _fake_layer()
+    assert L.dprc_clip_accumulate(ctypes.byref(lay), None, 0x50000, 48, 0, None, 0, None) == 1
+    assert L.dprc_clip_accumulate(ctypes.byref(lay), 0x60000, 0x50000, 47, 0, None, 0, None) == 1
+
+
+def test_clip_noise_bits_validation():
+    L = dprc.lib()
+    assert L.dprc_clip_scale(0x1000, 4, 0.0, 0x2000, None) == 1
+    assert L.dprc_clip_scale(0x1000, 4, float("inf"), 0x2000, None) == 1
+    assert L.dprc_clip_scale(None, 4, 1.0, 0x2000, None) == 1
+    assert L.dprc_clip_scale(0x1000, 0, 1.0, 0x2000, None) == 1
+    assert L.dprc_add_noise(0x1000, -1, 0.8, 1.0, 0, 0, None) == 1
+    assert L.dprc_add_noise(0x1000, 10, -0.1, 1.0, 0, 0, None) == 1
+    assert L.dprc_add_noise(0x1000, 10, float("nan"), 1.0, 0, 0, None) == 1
+    assert L.dprc_add_noise(0x1000, 10, 0.8, 0.0, 0, 0, None) == 1
+    assert L.dprc_add_noise(0x1002, 10, 0.8, 1.0, 0, 0, None) == 2
+    assert L.dprc_add_noise(None, 0, 0.8, 1.0, 0, 0, None) == 0          # empty: nothing to do
+    assert L.dprc_probe_bits(0, 0, 0, 0, 0, 4, 0x1000, None) == 1
+    assert L.dprc_probe_bits(0, 0, 0, 0, 32, 0, 0x1000, None) == 1
+    assert L.dprc_probe_bits(3, 0, 0, 0, 32, 4, 0x1000, None) == 1

@@ -290,3 +290,22 @@ def test_workload_generators_are_seeded_and_shaped():
     assert len(workloads.CONFIGS) == 5
     assert workloads.algorithmic_norm_bytes(workloads.BY_NAME["q_proj"]) == 67_108_864
     assert workloads.algorithmic_norm_bytes(workloads.BY_NAME["stack"]) == 54_710_501_376
+
+
+# ---- projected-order variants used for sampled full-size checks ----------------------
+
+@pytest.mark.parametrize("side", [est.SIDE_OUT, est.SIDE_IN])
+def test_projected_order_matches_explicit(side):
+    A, E = _rng_inputs(2, 30, 11, 17, seed=14)
+    m = 17 if side == est.SIDE_OUT else 11
+    Z = philox.rademacher_matrix(2, 5, 0, m, 6)
+    ref = est.hutch_layer(A, E, 6, 2, 5, side=side)
+    for i in range(2):
+        assert abs(est.hutch_sample_projected(A[i], E[i], Z, side) - ref[i]) <= 1e-12 * ref[i]
+    ZS = philox.rademacher_matrix(2, 5, 1, m, 4)
+    ZP = philox.rademacher_matrix(2, 5, 0, m, 5)
+    refpp = est.hutchpp_layer(A, E, 4, 5, 2, 5, side=side)
+    for i in range(2):
+        assert abs(est.hutchpp_sample_projected(A[i], E[i], ZS, ZP, side) - refpp[i]) <= 1e-10 * refpp[i]
+    c = np.array([0.5, 0.25])
+    assert np.allclose(est.clip_accumulate_rows(A, E, c, [1, 4]), est.clip_accumulate(A, E, c)[[1, 4]])
