@@ -1,0 +1,312 @@
+#!/usr/bin/env python3
+"""Throughput of randomized per-sample norm estimation (DP-SGD-RC) on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload q_proj|tiny|mlp|decoder|stack]
+
+One step is one pass of the workload's hot path over one batch already
+resident in HBM: the norm estimates of every layer (Hutchinson, or Hutch++ for
+``decoder``) summed per sample, the clip factors, and -- where the workload
+has them -- the clipped accumulation of every layer and the Gaussian noise.
+The default workload is one Llama-3.2-1B q_proj-shaped layer (B=4, T=2048,
+d=p=2048, bf16, k=16 Rademacher probes, clip C=1).  Inputs are synthetic
+(seeded) and several copies are rotated so that the 256 MB Infinity Cache
+does not serve a step from a previous step's reads.
+
+Prints one JSON line.  ``roofline`` covers the kernel that takes the most time
+in the step, timed with HIP events around each launch on the launch stream;
+``extra.accumulate`` times the clipped-accumulation GEMM on an mlp-shaped
+layer against the bf16 matrix-core peak; ``cpu_baseline`` is the CPU oracle
+timed on a bounded sample of the same workload.
+"""
+
+import argparse
+import ctypes
+import json
+import math
+import os
+import sys
+import time
+
+HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0       # MI355X dense bf16 matrix cores
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="q_proj")
+    ap.add_argument("--rotate-bytes", type=float, default=1.2e9,
+                    help="total bytes of rotated input copies (defeats the 256 MB Infinity Cache)")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU oracle sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extra", action="store_true", help="skip the accumulation-GEMM measurement")
+    return ap.parse_args()
+
+
+class Hip:
+    """HIP events through the runtime the process already uses."""
+
+    def __init__(self):
+        self.lib = ctypes.CDLL("libamdhip64.so")
+        self.lib.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        self.lib.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+        self.lib.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+    def events(self, n):
+        arr = (ctypes.c_void_p * n)()
+        for j in range(n):
+            e = ctypes.c_void_p()
+            if self.lib.hipEventCreate(ctypes.byref(e)) != 0:
+                raise RuntimeError("hipEventCreate failed")
+            arr[j] = e
+        return arr
+
+    def elapsed_ms(self, a, b):
+        self.lib.hipEventSynchronize(b)
+        t = ctypes.c_float()
+        if self.lib.hipEventElapsedTime(ctypes.byref(t), a, b) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return float(t.value)
+
+    def destroy(self, arr):
+        for e in arr:
+            self.lib.hipEventDestroy(e)
+
+
+def make_inputs(cfg, torch, workloads, copies):
+    sets = []
+    for c in range(copies):
+        layers = []
+        for li in range(len(cfg["layers"])):
+            A, E = workloads.layer_inputs(cfg, li, device="cuda", seed=c)
+            layers.append((A, E, li))
+        sets.append(layers)
+    return sets
+
+
+def step_fn(cfg, D, torch, ws_norm, grads):
+    C = cfg["C"]
+
+    def step(layers, n2, c):
+        if cfg["estimator"] == "hutch":
+            D.dprc_norm_hutch(layers, cfg["k"], 0, n2=n2, ws=ws_norm)
+        else:
+            D.dprc_norm_hutchpp(layers, cfg["s"], cfg["r"], 0, n2=n2, ws=ws_norm)
+        D.dprc_clip_scale(n2, C, c=c)
+        if cfg["accumulate"]:
+            for (A, E, li), g in zip(layers, grads):
+                D.dprc_clip_accumulate(A, E, c, grad=g)
+                if cfg["noise_sigma"] is not None:
+                    D.dprc_add_noise(g, cfg["noise_sigma"], C, 0, li)
+    return step
+
+
+def trace_kernels(hip, D, fn, reps, capacity=4096):
+    """Run fn() reps times with every library launch bracketed by events; per-kind launch durations."""
+    import torch
+    events = hip.events(2 * capacity)
+    kinds = (ctypes.c_int32 * capacity)()
+    count = ctypes.c_int32(0)
+    D.dprc_trace_launches(ctypes.cast(events, ctypes.c_void_p), ctypes.cast(kinds, ctypes.c_void_p), capacity,
+                          ctypes.cast(ctypes.pointer(count), ctypes.c_void_p))
+    try:
+        for _ in range(reps):
+            fn()
+        torch.cuda.synchronize()
+    finally:
+        D.dprc_trace_launches(None, None, 0, None)
+    out = []
+    for j in range(count.value):
+        out.append((D.KERNEL_NAMES.get(kinds[j], str(kinds[j])), hip.elapsed_ms(events[2 * j], events[2 * j + 1])))
+    hip.destroy(events)
+    return out
+
+
+def kernel_bytes_per_step(cfg):
+    """Algorithmic HBM bytes per step for the streaming kernels (inputs read once per launch)."""
+    elem = 4 if cfg["dtype"] == "f32" else 2
+    proj = tok = 0
+    for (_, d, p) in cfg["layers"]:
+        B, T = cfg["B"], cfg["T"]
+        m, n = p, d          # sketched side "out"
+        if cfg["estimator"] == "hutch":
+            proj += B * T * m * elem
+            tok += B * T * n * elem
+        else:                # three passes; pass 2 swaps the roles
+            proj += B * T * (2 * m + n) * elem
+            tok += B * T * (2 * n + m) * elem
+    return {"project": proj, "token_reduce": tok}
+
+
+def cpu_baseline(cfg, sets, budget_s):
+    """The oracle (fp64 numpy, explicit per-sample gradients) on a bounded sample of the workload."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+    from oracle import estimators as est
+    from oracle import philox
+    layers = sets[0]
+    B, T = cfg["B"], cfg["T"]
+    done_tokens = 0
+    pairs = []
+    t0 = time.perf_counter()
+    for (A, E, li) in layers:
+        _, d, p = cfg["layers"][li]
+        for i in range(B):
+            Ai = A[i].float().cpu().numpy().astype(np.float64)
+            Ei = E[i].float().cpu().numpy().astype(np.float64)
+            if cfg["estimator"] == "hutch":
+                Z = philox.rademacher_matrix(0, li, 0, p, cfg["k"])
+                est.hutch_layer(Ai[None], Ei[None], cfg["k"], 0, li, Z=Z)
+            else:
+                est.hutchpp_layer(Ai[None], Ei[None], cfg["s"], cfg["r"], 0, li)
+            done_tokens += T
+            pairs.append(f"{cfg['layers'][li][0]}[{i}]")
+            if time.perf_counter() - t0 > budget_s:
+                break
+        if time.perf_counter() - t0 > budget_s:
+            break
+    dt = time.perf_counter() - t0
+    info = threadpool_info()
+    threads = max([x.get("num_threads", 1) for x in info] or [1])
+    # the oracle's norm stage over all layers: tokens/s per layer-sample pass, scaled to whole-step tokens
+    layer_tokens = B * T * len(cfg["layers"])
+    return {"value": done_tokens / dt * (B * T) / layer_tokens, "unit": "tokens/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"fp64 explicit per-sample gradients + Hutchinson for {len(pairs)} (layer, sample) pairs "
+                      f"({', '.join(pairs[:6])}{'...' if len(pairs) > 6 else ''}) in {dt:.1f} s; "
+                      f"blas={','.join(sorted(set(x.get('internal_api', '?') for x in info))) or 'unknown'}, "
+                      f"os.cpu_count={os.cpu_count()}, affinity={len(os.sched_getaffinity(0))}"}
+
+
+def accumulate_extra(D, torch, workloads, hip, steps):
+    """Clipped accumulation GEMM on one mlp gate layer (d=2048, p=8192, B=2, T=8192)."""
+    cfg = workloads.BY_NAME["mlp"]
+    A, E = workloads.layer_inputs(cfg, 0, device="cuda")
+    c = torch.tensor([0.37, 0.81], device="cuda")
+    g = torch.empty(A.shape[2], E.shape[2], device="cuda")
+    for _ in range(3):
+        D.dprc_clip_accumulate(A, E, c, grad=g)
+    recs = trace_kernels(hip, D, lambda: D.dprc_clip_accumulate(A, E, c, grad=g), steps)
+    t = [ms for (k, ms) in recs if k == "accumulate"]
+    avg_ms = sum(t) / len(t)
+    flops = 2.0 * cfg["B"] * cfg["T"] * A.shape[2] * E.shape[2]
+    tf = flops / (avg_ms * 1e-3) / 1e12
+    return {"workload": "mlp.gate B=2 T=8192 d=2048 p=8192", "kernel": "accumulate",
+            "bound": "mfma", "achieved": round(tf, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(tf / BF16_PEAK_TFLOPS, 4), "avg_launch_us": round(avg_ms * 1e3, 2),
+            "flops_per_launch": flops}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (this library has no "
+              f"multi-GPU path).", file=sys.stderr)
+        sys.exit(2)
+    sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+    import torch
+    import workloads
+    from paper_2605_24879_amd import dprc as D
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    D.lib()
+    cfg = workloads.BY_NAME[args.workload]
+    B, T = cfg["B"], cfg["T"]
+    elem = 4 if cfg["dtype"] == "f32" else 2
+    in_bytes = sum(B * T * (d + p) * elem for (_, d, p) in cfg["layers"])
+    copies = max(1, min(32, math.ceil(args.rotate_bytes / in_bytes))) if in_bytes < 256e6 else 1
+    print(f"[bench] workload={cfg['name']} layers={len(cfg['layers'])} input={in_bytes/1e9:.3f} GB "
+          f"copies={copies}", file=sys.stderr, flush=True)
+    sets = make_inputs(cfg, torch, workloads, copies)
+    pairs0 = sets[0]
+    if cfg["estimator"] == "hutch":
+        ws_n = torch.empty(max(1, D.dprc_norm_hutch_workspace(pairs0, cfg["k"])), dtype=torch.uint8, device="cuda")
+    else:
+        ws_n = torch.empty(max(1, D.dprc_norm_hutchpp_workspace(pairs0, cfg["s"], cfg["r"])), dtype=torch.uint8,
+                           device="cuda")
+    grads = [torch.empty(d, p, device="cuda") for (_, d, p) in cfg["layers"]] if cfg["accumulate"] else []
+    n2 = torch.zeros(B, device="cuda")
+    c = torch.zeros(B, device="cuda")
+    step = step_fn(cfg, D, torch, ws_n, grads)
+
+    for w in range(args.warmup):
+        step(sets[w % copies], n2, c)
+    torch.cuda.synchronize()
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    t_start.record()
+    for s in range(args.steps):
+        step(sets[s % copies], n2, c)
+    t_end.record()
+    torch.cuda.synchronize()
+    ms_per_step = t_start.elapsed_time(t_end) / args.steps
+    print(f"[bench] timed {args.steps} steps: {ms_per_step*1e3:.2f} us/step", file=sys.stderr, flush=True)
+
+    # per-kernel durations over the same number of steps, with the launch hook on
+    hip = Hip()
+    it = iter(range(10 ** 9))
+    recs = trace_kernels(hip, D, lambda: step(sets[next(it) % copies], n2, c), args.steps)
+    per_kind = {}
+    for k, ms in recs:
+        tot, cnt = per_kind.get(k, (0.0, 0))
+        per_kind[k] = (tot + ms, cnt + 1)
+    dom = max(per_kind, key=lambda k: per_kind[k][0])
+    kb = kernel_bytes_per_step(cfg)
+    tot_ms, cnt = per_kind[dom]
+    launches_per_step = cnt / args.steps
+    if dom in kb:
+        bytes_per_launch = kb[dom] / launches_per_step
+        achieved = kb[dom] * args.steps / (tot_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None, "kernel": dom,
+                "bytes_per_launch": int(bytes_per_launch), "avg_launch_us": round(tot_ms / cnt * 1e3, 2)}
+    elif dom == "accumulate":
+        flops = sum(2 * B * T * d * p for (_, d, p) in cfg["layers"])
+        tf = flops * args.steps / (tot_ms * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(tf, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(tf / BF16_PEAK_TFLOPS, 4), "traffic": None, "kernel": dom,
+                "flops_per_launch": int(flops / launches_per_step), "avg_launch_us": round(tot_ms / cnt * 1e3, 2)}
+    else:
+        roof = {"bound": "hbm", "achieved": None, "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": None,
+                "traffic": None, "kernel": dom}
+    norm_bytes = workloads.algorithmic_norm_bytes(cfg)
+    norm_ms = sum(per_kind.get(k, (0.0, 0))[0] for k in ("project", "token_reduce", "qr", "hutchpp_final",
+                                                          "project_f32", "token_reduce_f32", "sample_sq",
+                                                          "probe_bits", "token_splits", "sample_sum")) / args.steps
+    kernels = {k: {"launches_per_step": v[1] / args.steps, "avg_launch_us": round(v[0] / v[1] * 1e3, 2),
+                   "us_per_step": round(v[0] / args.steps * 1e3, 2)} for k, v in sorted(per_kind.items())}
+    extra = {"norm_kernels_us_per_step": round(norm_ms * 1e3, 2),
+             "norm_hbm_gbps_kernels": round(norm_bytes / (norm_ms * 1e-3) / 1e9, 1) if norm_ms else None,
+             "step_hbm_gbps": round(norm_bytes / (ms_per_step * 1e-3) / 1e9, 1),
+             "step_hbm_frac": round(norm_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+             "kernels": kernels, "input_copies_rotated": copies}
+    if not args.no_extra:
+        extra["accumulate"] = accumulate_extra(D, torch, workloads, hip, max(5, args.steps // 5))
+    rec = {"metric": "per-sample norm-estimation tokens/s + HBM GB/s (% peak), Llama-3.2-1B shapes",
+           "value": round(B * T / (ms_per_step * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5),
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": cfg["dtype"],
+           "data": "synthetic (seeded; Llama-3.2-1B layer shapes)",
+           "config": workloads.describe(cfg) | {"C": cfg["C"], "steps_include": step_parts(cfg)},
+           "roofline": roof, "extra": extra}
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
+        rec["cpu_baseline"] = cpu_baseline(cfg, sets, args.cpu_seconds)
+    print(json.dumps(rec), flush=True)
+
+
+def step_parts(cfg):
+    parts = ["norm-" + cfg["estimator"], "clip_scale"]
+    if cfg["accumulate"]:
+        parts.append("clip_accumulate")
+    if cfg["noise_sigma"] is not None:
+        parts.append("add_noise")
+    return parts
+
+
+if __name__ == "__main__":
+    main()

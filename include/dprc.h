@@ -27,9 +27,11 @@
  *     failed check returns a non-zero dprc_status and enqueues nothing.  A
  *     failed launch returns DPRC_ERROR_HIP.  No C++ exception crosses the ABI.
  *   - Tensors are row-major with token rows: element (i, t, j) of A is at
- *     A + (i*T + t)*lda + j.  bf16 inputs need 16-byte aligned base pointers
- *     and strides that are multiples of 8 elements; fp32 inputs need 4-byte
- *     alignment.  Otherwise DPRC_ERROR_NOT_SUPPORTED.
+ *     A + (i*T + t)*lda + j.  Pointers must be aligned to their element size
+ *     (else DPRC_ERROR_NOT_SUPPORTED).  bf16 rows that start on 16-byte
+ *     boundaries (16-byte aligned base, stride a multiple of 8) with a width
+ *     that is a multiple of 8 take 16-byte loads; other layouts are correct
+ *     but slower (element loads).
  *
  * Probes: +-1 (Rademacher) entries from Philox4x32-10 (Salmon et al., SC'11)
  * keyed by (seed, layer_id, stream), shared by all samples of a layer and
@@ -144,6 +146,35 @@ dprc_status dprc_add_noise(float* grad, int64_t numel, float sigma, float C, uin
 dprc_status dprc_probe_bits(dprc_probe probe, uint64_t seed, uint32_t layer_id,
                             uint32_t stream_id, int64_t m, int32_t k, uint32_t* out,
                             hipStream_t stream);
+
+/* ---- per-launch timing (diagnostics, for profilers and benchmarks) ------------
+ * While `events` is non-NULL, every kernel that a dprc call enqueues from THIS
+ * host thread is bracketed by hipEventRecord on that call's stream: launch j
+ * (counted from this call) records events[2j] before and events[2j+1] after,
+ * kinds[j] (if kinds is non-NULL) receives its dprc_kernel_kind, and the host
+ * integer *count is advanced; recording stops once *count reaches `capacity`
+ * (the events array must hold 2*capacity created events).  *count is reset
+ * to 0 here.  events == NULL switches the hook off.  The state is per host
+ * thread and holds the caller's pointers until switched off. */
+typedef enum {
+  DPRC_KERNEL_PROJECT = 1,            /* Y = X Z (bf16 matrix cores)          */
+  DPRC_KERNEL_TOKEN_REDUCE = 2,       /* X'^T Y, estimate or store            */
+  DPRC_KERNEL_QR = 3,                 /* Hutch++ Householder QR               */
+  DPRC_KERNEL_HUTCHPP_FINAL = 4,      /* Hutch++ V = W_P - U Q^T P, estimate  */
+  DPRC_KERNEL_CLIP_SCALE = 5,
+  DPRC_KERNEL_ACCUMULATE = 6,         /* clipped accumulation GEMM            */
+  DPRC_KERNEL_SPLITK_REDUCE = 7,
+  DPRC_KERNEL_NOISE = 8,
+  DPRC_KERNEL_PROBE_BITS = 9,
+  DPRC_KERNEL_PROJECT_F32 = 10,
+  DPRC_KERNEL_TOKEN_REDUCE_F32 = 11,
+  DPRC_KERNEL_SAMPLE_SQ = 12,
+  DPRC_KERNEL_ACCUMULATE_F32 = 13,
+  DPRC_KERNEL_TOKEN_SPLITS = 14,      /* sum of token splits per tile          */
+  DPRC_KERNEL_SAMPLE_SUM = 15         /* per-sample sum of tile squares         */
+} dprc_kernel_kind;
+dprc_status dprc_trace_launches(hipEvent_t* events, int32_t* kinds, int32_t capacity,
+                                int32_t* count);
 
 const char* dprc_status_string(dprc_status status);
 const char* dprc_version(void);

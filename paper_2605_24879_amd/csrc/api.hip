@@ -133,19 +133,43 @@ TokPlan tok_plan(int64_t B, int64_t T, int64_t n) {
 
 struct TokBufs {
   float* part;
-  float* tilesq;
-  uint32_t* cnt;  // [B*ntiles] tile counters, then [B] sample counters
+  double* tilesq;
 };
 
 TokBufs take_tok(Arena& ar, int64_t B, const TokPlan& tp, int ncols_pad) {
   TokBufs b;
   b.part = tp.S > 1 ? ar.take<float>((size_t)B * tp.ntiles * tp.S * ncols_pad * kTile) : nullptr;
-  b.tilesq = ar.take<float>((size_t)B * tp.ntiles);
-  b.cnt = ar.take<uint32_t>((size_t)B * tp.ntiles + B);
+  b.tilesq = ar.take<double>((size_t)B * tp.ntiles);
   return b;
 }
 
 dprc_status hip_status(hipError_t e) { return e == hipSuccess ? DPRC_SUCCESS : DPRC_ERROR_HIP; }
+
+// Per-launch timing for diagnostics (dprc_trace_launches): host-thread state only.
+struct Trace {
+  hipEvent_t* events = nullptr;
+  int32_t* kinds = nullptr;
+  int32_t capacity = 0;
+  int32_t* count = nullptr;
+};
+thread_local Trace g_trace;
+
+template <class F>
+hipError_t traced(int kind, hipStream_t st, F&& launch) {
+  Trace& t = g_trace;
+  const bool on = t.events && t.count && *t.count < t.capacity;
+  if (on) {
+    hipError_t e = hipEventRecord(t.events[2 * *t.count], st);
+    if (e != hipSuccess) return e;
+  }
+  hipError_t e = launch();
+  if (on && e == hipSuccess) {
+    e = hipEventRecord(t.events[2 * *t.count + 1], st);
+    if (t.kinds) t.kinds[*t.count] = kind;
+    ++*t.count;
+  }
+  return e;
+}
 
 // ---- one projection + token-reduction pass (bf16) --------------------------------------------
 struct PassSpec {
@@ -186,9 +210,9 @@ dprc_status run_pass(const PassSpec& ps, int64_t B, int64_t T, uint32_t k0, uint
   pa.probe_kind = ps.probe_kind; pa.key0 = k0; pa.key1 = k1; pa.layer_id = layer; pa.stream_id = ps.stream_id;
   pa.words_per_chunk = words_per_chunk(ps.m, ps.nz);
   pa.Yt = Yt; pa.yt_ld = B * tp.T_pad;
-  pa.zero_ptr = tb.cnt; pa.zero_count = (int32_t)(B * tp.ntiles + B);
+  pa.zero_ptr = nullptr; pa.zero_count = 0;
   pa.vec = rows16(ps.X, ps.ldx);
-  hipError_t e = launch_project(pa, rows_per_wg(B * tp.T_pad, ncols_pad), st);
+  hipError_t e = traced(DPRC_KERNEL_PROJECT, st, [&] { return launch_project(pa, rows_per_wg(B * tp.T_pad, ncols_pad), st); });
   if (e != hipSuccess) return DPRC_ERROR_HIP;
 
   TokredArgs ta;
@@ -197,12 +221,19 @@ dprc_status run_pass(const PassSpec& ps, int64_t B, int64_t T, uint32_t k0, uint
   ta.Yt = Yt; ta.yt_ld = B * tp.T_pad; ta.T_pad = tp.T_pad; ta.ncols = ncols; ta.ncols_pad = ncols_pad;
   ta.ntiles = tp.ntiles; ta.S = tp.S; ta.stages_per_split = tp.sps;
   ta.mode = ps.mode;
-  ta.part = tb.part; ta.cnt_tile = tb.cnt; ta.tilesq = tb.tilesq; ta.cnt_sample = tb.cnt + B * tp.ntiles;
+  ta.part = tb.part; ta.tilesq = tb.tilesq;
   ta.scale = ps.scale; ta.n2 = ps.n2; ta.n2_layer = ps.n2_layer; ta.accumulate = ps.accumulate;
   ta.M = ps.M; ta.m_ld = ps.m_ld; ta.m_ss = (int64_t)ncols * ps.m_ld;
   ta.Mhi = ps.Mhi; ta.Mlo = ps.Mlo; ta.mh_ld = ps.mh_ld; ta.mh_ss = (int64_t)ncols * ps.mh_ld;
   ta.vec = rows16(ps.Xo, ps.ldo);
-  return hip_status(launch_tokred(ta, st));
+  e = traced(DPRC_KERNEL_TOKEN_REDUCE, st, [&] { return launch_tokred(ta, st); });
+  if (e != hipSuccess) return DPRC_ERROR_HIP;
+  if (tp.S > 1) {
+    e = traced(DPRC_KERNEL_TOKEN_SPLITS, st, [&] { return launch_tokred_splits(ta, st); });
+    if (e != hipSuccess) return DPRC_ERROR_HIP;
+  }
+  if (ps.mode == 0) return hip_status(traced(DPRC_KERNEL_SAMPLE_SUM, st, [&] { return launch_tokred_sample(ta, st); }));
+  return DPRC_SUCCESS;
 }
 
 size_t pass_ws_bytes(int64_t B, int64_t T, int64_t n, int ncols) {
@@ -234,16 +265,16 @@ dprc_status hutch_layer(const View& v, int32_t k, int probe, uint32_t k0, uint32
   uint32_t* zb = ar.take<uint32_t>((size_t)k * ceil_div(v.m, 32));
   float* Y = ar.take<float>((size_t)v.B * v.T * k);
   float* M = ar.take<float>((size_t)v.B * k * v.n);
-  hipError_t e = launch_probe_bits(probe, k0, k1, v.layer_id, 0, v.m, k, zb, st);
+  hipError_t e = traced(DPRC_KERNEL_PROBE_BITS, st, [&] { return launch_probe_bits(probe, k0, k1, v.layer_id, 0, v.m, k, zb, st); });
   if (e != hipSuccess) return DPRC_ERROR_HIP;
   ProjectF32Args pa{(const float*)v.X, v.ldx, v.T * v.ldx, (int32_t)v.B, (int32_t)v.T, (int32_t)v.m,
                     0, k, k, nullptr, 0, 0, zb, Y};
-  if ((e = launch_project_f32(pa, st)) != hipSuccess) return DPRC_ERROR_HIP;
+  if ((e = traced(DPRC_KERNEL_PROJECT_F32, st, [&] { return launch_project_f32(pa, st); })) != hipSuccess) return DPRC_ERROR_HIP;
   TokredF32Args ta{(const float*)v.Xo, v.ldo, v.T * v.ldo, (int32_t)v.B, (int32_t)v.T, (int32_t)v.n, Y, k,
                    M, v.n, (int64_t)k * v.n};
-  if ((e = launch_tokred_f32(ta, st)) != hipSuccess) return DPRC_ERROR_HIP;
-  return hip_status(launch_sample_sq(M, v.n, (int64_t)k * v.n, (int32_t)v.B, k, (int32_t)v.n,
-                                     1.0f / (float)k, n2, n2_layer, accumulate, st));
+  if ((e = traced(DPRC_KERNEL_TOKEN_REDUCE_F32, st, [&] { return launch_tokred_f32(ta, st); })) != hipSuccess) return DPRC_ERROR_HIP;
+  return hip_status(traced(DPRC_KERNEL_SAMPLE_SQ, st, [&] { return launch_sample_sq(M, v.n, (int64_t)k * v.n, (int32_t)v.B, k, (int32_t)v.n,
+                                     1.0f / (float)k, n2, n2_layer, accumulate, st); }));
 }
 
 // ---- Hutch++ -------------------------------------------------------------------------------------
@@ -325,8 +356,8 @@ dprc_status hutchpp_layer(const View& v, int32_t s, int32_t r, uint32_t k0, uint
     p2.mode = 1; p2.M = b.OS; p2.m_ld = v.m;
     if ((stt = run_pass(p2, B, T, k0, k1, v.layer_id, b.pass_ws, st)) != DPRC_SUCCESS) return stt;
     // Q = orth(O S)
-    e = launch_qr(b.OS, v.m, (int64_t)s * v.m, (int32_t)B, (int32_t)v.m, s, b.qrwork, b.Q, v.m,
-                  (int64_t)s * v.m, b.Qhi, b.Qlo, b.ld_q, (int64_t)s * b.ld_q, st);
+    e = traced(DPRC_KERNEL_QR, st, [&] { return launch_qr(b.OS, v.m, (int64_t)s * v.m, (int32_t)B, (int32_t)v.m, s, b.qrwork, b.Q, v.m,
+                  (int64_t)s * v.m, b.Qhi, b.Qlo, b.ld_q, (int64_t)s * b.ld_q, st); });
     if (e != hipSuccess) return DPRC_ERROR_HIP;
     // pass 3: [U | W_P] = Xo^T (X [Q | P])
     PassSpec p3{};
@@ -339,34 +370,34 @@ dprc_status hutchpp_layer(const View& v, int32_t s, int32_t r, uint32_t k0, uint
     const float* X = (const float*)v.X;
     const float* Xo = (const float*)v.Xo;
     if (s > 0) {
-      if ((e = launch_probe_bits(0, k0, k1, v.layer_id, 1, v.m, s, b.zb, st)) != hipSuccess) return DPRC_ERROR_HIP;
+      if ((e = traced(DPRC_KERNEL_PROBE_BITS, st, [&] { return launch_probe_bits(0, k0, k1, v.layer_id, 1, v.m, s, b.zb, st); })) != hipSuccess) return DPRC_ERROR_HIP;
       ProjectF32Args a1{X, v.ldx, T * v.ldx, (int32_t)B, (int32_t)T, (int32_t)v.m, 0, s, s, nullptr, 0, 0, b.zb, b.Y32};
-      if ((e = launch_project_f32(a1, st)) != hipSuccess) return DPRC_ERROR_HIP;
+      if ((e = traced(DPRC_KERNEL_PROJECT_F32, st, [&] { return launch_project_f32(a1, st); })) != hipSuccess) return DPRC_ERROR_HIP;
       TokredF32Args t1{Xo, v.ldo, T * v.ldo, (int32_t)B, (int32_t)T, (int32_t)v.n, b.Y32, s, b.WS32, v.n, (int64_t)s * v.n};
-      if ((e = launch_tokred_f32(t1, st)) != hipSuccess) return DPRC_ERROR_HIP;
+      if ((e = traced(DPRC_KERNEL_TOKEN_REDUCE_F32, st, [&] { return launch_tokred_f32(t1, st); })) != hipSuccess) return DPRC_ERROR_HIP;
       ProjectF32Args a2{Xo, v.ldo, T * v.ldo, (int32_t)B, (int32_t)T, (int32_t)v.n, s, 0, s, b.WS32, v.n,
                         (int64_t)s * v.n, nullptr, b.Y32};
-      if ((e = launch_project_f32(a2, st)) != hipSuccess) return DPRC_ERROR_HIP;
+      if ((e = traced(DPRC_KERNEL_PROJECT_F32, st, [&] { return launch_project_f32(a2, st); })) != hipSuccess) return DPRC_ERROR_HIP;
       TokredF32Args t2{X, v.ldx, T * v.ldx, (int32_t)B, (int32_t)T, (int32_t)v.m, b.Y32, s, b.OS, v.m, (int64_t)s * v.m};
-      if ((e = launch_tokred_f32(t2, st)) != hipSuccess) return DPRC_ERROR_HIP;
-      e = launch_qr(b.OS, v.m, (int64_t)s * v.m, (int32_t)B, (int32_t)v.m, s, b.qrwork, b.Q, v.m,
-                    (int64_t)s * v.m, nullptr, nullptr, 0, 0, st);
+      if ((e = traced(DPRC_KERNEL_TOKEN_REDUCE_F32, st, [&] { return launch_tokred_f32(t2, st); })) != hipSuccess) return DPRC_ERROR_HIP;
+      e = traced(DPRC_KERNEL_QR, st, [&] { return launch_qr(b.OS, v.m, (int64_t)s * v.m, (int32_t)B, (int32_t)v.m, s, b.qrwork, b.Q, v.m,
+                    (int64_t)s * v.m, nullptr, nullptr, 0, 0, st); });
       if (e != hipSuccess) return DPRC_ERROR_HIP;
     }
-    if ((e = launch_probe_bits(0, k0, k1, v.layer_id, 0, v.m, r, b.zb, st)) != hipSuccess) return DPRC_ERROR_HIP;
+    if ((e = traced(DPRC_KERNEL_PROBE_BITS, st, [&] { return launch_probe_bits(0, k0, k1, v.layer_id, 0, v.m, r, b.zb, st); })) != hipSuccess) return DPRC_ERROR_HIP;
     ProjectF32Args a3{X, v.ldx, T * v.ldx, (int32_t)B, (int32_t)T, (int32_t)v.m, s, r, s + r, b.Q, v.m,
                       (int64_t)s * v.m, b.zb, b.Y32};
-    if ((e = launch_project_f32(a3, st)) != hipSuccess) return DPRC_ERROR_HIP;
+    if ((e = traced(DPRC_KERNEL_PROJECT_F32, st, [&] { return launch_project_f32(a3, st); })) != hipSuccess) return DPRC_ERROR_HIP;
     TokredF32Args t3{Xo, v.ldo, T * v.ldo, (int32_t)B, (int32_t)T, (int32_t)v.n, b.Y32, s + r, b.UW, v.n,
                      (int64_t)(s + r) * v.n};
-    if ((e = launch_tokred_f32(t3, st)) != hipSuccess) return DPRC_ERROR_HIP;
+    if ((e = traced(DPRC_KERNEL_TOKEN_REDUCE_F32, st, [&] { return launch_tokred_f32(t3, st); })) != hipSuccess) return DPRC_ERROR_HIP;
     if (s == 0)
-      return hip_status(launch_sample_sq(b.UW, v.n, (int64_t)r * v.n, (int32_t)B, r, (int32_t)v.n,
-                                         1.0f / (float)r, n2, n2_layer, accumulate, st));
+      return hip_status(traced(DPRC_KERNEL_SAMPLE_SQ, st, [&] { return launch_sample_sq(b.UW, v.n, (int64_t)r * v.n, (int32_t)B, r, (int32_t)v.n,
+                                         1.0f / (float)r, n2, n2_layer, accumulate, st); }));
   }
-  return hip_status(launch_hutchpp_final(b.UW, v.n, (int64_t)(s + r) * v.n, b.Q, v.m, (int64_t)s * v.m,
+  return hip_status(traced(DPRC_KERNEL_HUTCHPP_FINAL, st, [&] { return launch_hutchpp_final(b.UW, v.n, (int64_t)(s + r) * v.n, b.Q, v.m, (int64_t)s * v.m,
                                          (int32_t)B, (int32_t)v.n, (int32_t)v.m, s, r, k0, k1, v.layer_id,
-                                         n2, n2_layer, accumulate, st));
+                                         n2, n2_layer, accumulate, st); }));
 }
 
 // ---- clipped accumulation ----------------------------------------------------------------------------
@@ -401,6 +432,16 @@ const char* dprc_status_string(dprc_status s) {
 }
 
 const char* dprc_version(void) { return "dprc 0.1.0 (gfx950)"; }
+
+dprc_status dprc_trace_launches(hipEvent_t* events, int32_t* kinds, int32_t capacity, int32_t* count) {
+  if (events && (capacity < 0 || !count)) return DPRC_ERROR_INVALID_VALUE;
+  g_trace.events = events;
+  g_trace.kinds = kinds;
+  g_trace.capacity = events ? capacity : 0;
+  g_trace.count = events ? count : nullptr;
+  if (count) *count = 0;
+  return DPRC_SUCCESS;
+}
 
 size_t dprc_norm_hutch_workspace(const dprc_layer* layers, int32_t num_layers, int32_t k, dprc_side side) {
   if (check_layers(layers, num_layers, side) != DPRC_SUCCESS || k < 1 || k > 256) return 0;
@@ -467,7 +508,7 @@ dprc_status dprc_norm_hutchpp(const dprc_layer* layers, int32_t num_layers, int3
 
 dprc_status dprc_clip_scale(const float* n2, int64_t B, float C, float* c, hipStream_t stream) {
   if (!n2 || !c || B < 1 || !(C > 0.f) || std::isinf(C)) return DPRC_ERROR_INVALID_VALUE;
-  return hip_status(launch_clip_scale(n2, B, C, c, stream));
+  return hip_status(traced(DPRC_KERNEL_CLIP_SCALE, stream, [&] { return launch_clip_scale(n2, B, C, c, stream); }));
 }
 
 size_t dprc_clip_accumulate_workspace(const dprc_layer* L) {
@@ -488,9 +529,9 @@ dprc_status dprc_clip_accumulate(const dprc_layer* L, const float* c, float* gra
   if (ws_bytes < need) return DPRC_ERROR_WORKSPACE_TOO_SMALL;
   if (need && (!ws || !aligned(ws, kAlign))) return DPRC_ERROR_INVALID_VALUE;
   if (L->dtype == DPRC_F32)
-    return hip_status(launch_gemm_f32((const float*)L->A, L->lda, L->T * L->lda, (const float*)L->E, L->lde,
+    return hip_status(traced(DPRC_KERNEL_ACCUMULATE_F32, stream, [&] { return launch_gemm_f32((const float*)L->A, L->lda, L->T * L->lda, (const float*)L->E, L->lde,
                                       L->T * L->lde, (int32_t)L->B, (int32_t)L->T, (int32_t)L->d, (int32_t)L->p, c,
-                                      grad, ldg, accumulate, stream));
+                                      grad, ldg, accumulate, stream); }));
   const GemmPlan g = gemm_plan(*L);
   GemmArgs a;
   a.A = (const uint16_t*)L->A; a.lda = L->lda; a.a_ss = L->T * L->lda;
@@ -501,9 +542,9 @@ dprc_status dprc_clip_accumulate(const dprc_layer* L, const float* c, float* gra
   a.part = (float*)ws;
   a.vec_a = rows16(L->A, L->lda);
   a.vec_e = rows16(L->E, L->lde);
-  hipError_t e = launch_gemm(a, stream);
+  hipError_t e = traced(DPRC_KERNEL_ACCUMULATE, stream, [&] { return launch_gemm(a, stream); });
   if (e != hipSuccess) return DPRC_ERROR_HIP;
-  if (g.S > 1) return hip_status(launch_splitk_reduce(a.part, g.S, a.d, a.p, grad, ldg, accumulate, stream));
+  if (g.S > 1) return hip_status(traced(DPRC_KERNEL_SPLITK_REDUCE, stream, [&] { return launch_splitk_reduce(a.part, g.S, a.d, a.p, grad, ldg, accumulate, stream); }));
   return DPRC_SUCCESS;
 }
 
@@ -515,7 +556,7 @@ dprc_status dprc_add_noise(float* grad, int64_t numel, float sigma, float C, uin
   if (numel == 0) return DPRC_SUCCESS;
   uint32_t k0, k1;
   key_of(seed, k0, k1);
-  return hip_status(launch_noise(grad, numel, sigma * C, k0, k1, tensor_id, stream));
+  return hip_status(traced(DPRC_KERNEL_NOISE, stream, [&] { return launch_noise(grad, numel, sigma * C, k0, k1, tensor_id, stream); }));
 }
 
 dprc_status dprc_probe_bits(dprc_probe probe, uint64_t seed, uint32_t layer_id, uint32_t stream_id, int64_t m,
@@ -524,7 +565,7 @@ dprc_status dprc_probe_bits(dprc_probe probe, uint64_t seed, uint32_t layer_id, 
   if (probe != DPRC_PROBE_RADEMACHER && probe != DPRC_PROBE_HADAMARD) return DPRC_ERROR_INVALID_VALUE;
   uint32_t k0, k1;
   key_of(seed, k0, k1);
-  return hip_status(launch_probe_bits((int)probe, k0, k1, layer_id, stream_id, m, k, out, stream));
+  return hip_status(traced(DPRC_KERNEL_PROBE_BITS, stream, [&] { return launch_probe_bits((int)probe, k0, k1, layer_id, stream_id, m, k, out, stream); }));
 }
 
 }  // extern "C"

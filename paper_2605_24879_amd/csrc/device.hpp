@@ -94,15 +94,33 @@ __device__ __forceinline__ uint4 signs_to_bf16x8(uint32_t byte) {
   return r;
 }
 
-// Eight consecutive bf16 of a token row starting at column u (u a multiple of 8),
-// zero past `lim`; 16-byte load when the row is 16-byte aligned, element loads otherwise.
-__device__ __forceinline__ uint4 load_bf16x8(const uint16_t* row, int64_t u, int64_t lim, bool vec) {
-  if (u >= lim) return uint4{0, 0, 0, 0};
-  if (vec && u + 8 <= lim) return *reinterpret_cast<const uint4*>(row + u);
+// Loads of 8 consecutive bf16 of a token row.  The fast form is one 16-byte
+// load with no branch: callers pass a pointer that is valid and 16-byte aligned
+// even when the lane is masked (a clamped address) and the value is zeroed by a
+// select, so all loads of a stage stay in flight together.  The element form
+// serves rows that are not 16-byte aligned or widths that are not a multiple
+// of 8 (the host picks the form per launch).
+__device__ __forceinline__ uint4 load8_sel(const uint16_t* p, bool ok) {
+  const uint4 v = *reinterpret_cast<const uint4*>(p);
+  return ok ? v : uint4{0, 0, 0, 0};
+}
+
+__device__ __forceinline__ uint4 load8_elem(const uint16_t* row, int64_t u, int64_t lim, bool ok) {
   uint32_t h[8];
 #pragma unroll
-  for (int j = 0; j < 8; ++j) h[j] = (u + j < lim) ? (uint32_t)row[u + j] : 0u;
+  for (int j = 0; j < 8; ++j) h[j] = (ok && u + j < lim) ? (uint32_t)row[u + j] : 0u;
   return uint4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
+}
+
+template <bool FAST>
+__device__ __forceinline__ uint4 load_bf16x8(const uint16_t* row, int64_t u, int64_t lim, bool row_ok,
+                                             const uint16_t* safe) {
+  if constexpr (FAST) {
+    const bool ok = row_ok && u < lim;          // lim % 8 == 0: u < lim implies u + 8 <= lim
+    return load8_sel(ok ? row + u : safe, ok);
+  } else {
+    return load8_elem(row, u, lim, row_ok);
+  }
 }
 
 // ---- matrix cores and LDS ------------------------------------------------------------

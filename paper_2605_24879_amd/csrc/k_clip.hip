@@ -36,6 +36,7 @@ hipError_t launch_clip_scale(const float* n2, int64_t B, float C, float* c, hipS
 constexpr int kGT = 128;                   // tile edge
 constexpr int kGLd = kGT + 8;              // padded LDS row
 
+template <bool FAST>
 __global__ __launch_bounds__(kBlock) void gemm_kernel(GemmArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t la[2][kStage * kGLd];
   __shared__ __attribute__((aligned(16))) uint16_t le[2][kStage * kGLd];
@@ -61,8 +62,10 @@ __global__ __launch_bounds__(kBlock) void gemm_kernel(GemmArgs a) {
     for (int q = 0; q < 4; ++q) {
       const int64_t t = tok0 + lr0 + 16 * q;
       const bool ok = t < a.T;
-      ga[q] = ok ? load_bf16x8(a.A + (int64_t)i * a.a_ss + t * a.lda, ja, a.d, a.vec_a) : uint4{0, 0, 0, 0};
-      ge[q] = ok ? load_bf16x8(a.E + (int64_t)i * a.e_ss + t * a.lde, je, a.p, a.vec_e) : uint4{0, 0, 0, 0};
+      const uint16_t* as = a.A + (int64_t)i * a.a_ss;
+      const uint16_t* es = a.E + (int64_t)i * a.e_ss;
+      ga[q] = load_bf16x8<FAST>(as + (ok ? t : 0) * a.lda, ja, a.d, ok, as);
+      ge[q] = load_bf16x8<FAST>(es + (ok ? t : 0) * a.lde, je, a.p, ok, es);
     }
   };
   auto swrite = [&](int buf) {
@@ -155,7 +158,10 @@ __global__ __launch_bounds__(kBlock) void gemm_kernel(GemmArgs a) {
 
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t st) {
   dim3 grid((unsigned)ceil_div(a.p, kGT), (unsigned)ceil_div(a.d, kGT), (unsigned)a.S);
-  hipLaunchKernelGGL(gemm_kernel, grid, dim3(kBlock), 0, st, a);
+  if (a.vec_a && a.vec_e && a.d % 8 == 0 && a.p % 8 == 0)
+    hipLaunchKernelGGL(gemm_kernel<true>, grid, dim3(kBlock), 0, st, a);
+  else
+    hipLaunchKernelGGL(gemm_kernel<false>, grid, dim3(kBlock), 0, st, a);
   return hipGetLastError();
 }
 

@@ -17,7 +17,7 @@
 
 namespace dprc {
 
-template <int RB, int NB, bool DENSE>
+template <int RB, int NB, bool DENSE, bool FAST>
 __global__ __launch_bounds__(kBlock) void project_kernel(ProjectArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint32_t smem[];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
@@ -71,31 +71,49 @@ __global__ __launch_bounds__(kBlock) void project_kernel(ProjectArgs a) {
     }
     const int64_t rem = a.m - uc;
     const int nsub = (int)min((int64_t)(wpc >> 1), (rem + 63) >> 6);
-    for (int q = wv; q < nsub; q += 4) {
-      const int64_t u0 = uc + 64 * (int64_t)q;
-      uint4 av[RB][2];
+    // U sub-chunks per batch: all their loads are issued before the first MFMA
+    constexpr int U = RB == 1 ? 8 : (RB == 2 ? 4 : 2);
+    for (int qb = wv; qb < nsub; qb += 4 * U) {
+      uint4 av[U][RB][2];
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb)
+      for (int uu = 0; uu < U; ++uu) {
+        const int q = qb + 4 * uu;
+        const int64_t u0 = uc + 64 * (int64_t)(q < nsub ? q : qb);
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) av[rb][ks] = rowok[rb] ? load_bf16x8(rowp[rb], u0 + 32 * ks + 8 * g, a.m, a.vec) : uint4{0, 0, 0, 0};
+        for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
+          for (int ks = 0; ks < 2; ++ks)
+            av[uu][rb][ks] = load_bf16x8<FAST>(rowp[rb], u0 + 32 * ks + 8 * g, a.m, rowok[rb] && q < nsub, xs);
+      }
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-          const int c = 16 * nb + l16;
-          uint4 bh = uint4{0, 0, 0, 0}, bl = uint4{0, 0, 0, 0};
-          if (DENSE && c < a.nd) {
-            const int64_t off = (int64_t)c * a.ld_r + u0 + 32 * ks + 8 * g;
-            bh = *reinterpret_cast<const uint4*>(rhi + off);
-            bl = *reinterpret_cast<const uint4*>(rlo + off);
-          } else if (c - a.nd < a.nz) {
-            const uint32_t word = zw[(c - a.nd) * wpc + 2 * q + ks];
-            bh = signs_to_bf16x8((word >> (8 * g)) & 0xFFu);
-          }
+      for (int uu = 0; uu < U; ++uu) {
+        const int q = qb + 4 * uu;
+        if (q >= nsub) break;                      // wave-uniform
+        const int64_t u0 = uc + 64 * (int64_t)q;
 #pragma unroll
-          for (int rb = 0; rb < RB; ++rb) {
-            acc[rb][nb] = mfma16x16x32(av[rb][ks], bh, acc[rb][nb]);
-            if (DENSE) acc[rb][nb] = mfma16x16x32(av[rb][ks], bl, acc[rb][nb]);
+        for (int ks = 0; ks < 2; ++ks) {
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) {
+            const int c = 16 * nb + l16;
+            // select, not branch: every lane issues the same loads
+            const int cz = c - a.nd;
+            const bool isz = cz >= 0 && cz < a.nz;
+            const uint32_t word = a.nz > 0 ? zw[(isz ? cz : 0) * wpc + 2 * q + ks] : 0u;
+            const uint4 zb = signs_to_bf16x8((word >> (8 * g)) & 0xFFu);
+            uint4 bh = isz ? zb : uint4{0, 0, 0, 0}, bl = uint4{0, 0, 0, 0};
+            if (DENSE) {
+              const bool isd = c < a.nd;
+              const int64_t off = (int64_t)(isd ? c : 0) * a.ld_r + u0 + 32 * ks + 8 * g;
+              const uint4 dh = *reinterpret_cast<const uint4*>(rhi + off);
+              const uint4 dl = *reinterpret_cast<const uint4*>(rlo + off);
+              bh = isd ? dh : bh;
+              bl = isd ? dl : bl;
+            }
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb) {
+              acc[rb][nb] = mfma16x16x32(av[uu][rb][ks], bh, acc[rb][nb]);
+              if (DENSE) acc[rb][nb] = mfma16x16x32(av[uu][rb][ks], bl, acc[rb][nb]);
+            }
           }
         }
       }
@@ -134,10 +152,15 @@ static hipError_t launch_rb_nb(const ProjectArgs& a, hipStream_t st) {
   const size_t rbytes = (size_t)4 * 16 * RB * (16 * NB + 4) * 4;
   const size_t lds = zbytes + rbytes;
   dim3 grid((unsigned)(a.T_pad / (16 * RB)), (unsigned)a.B);
-  if (a.nd > 0)
-    hipLaunchKernelGGL((project_kernel<RB, NB, true>), grid, dim3(kBlock), lds, st, a);
+  const bool fast = a.vec && a.m % 8 == 0;
+  if (a.nd > 0 && fast)
+    hipLaunchKernelGGL((project_kernel<RB, NB, true, true>), grid, dim3(kBlock), lds, st, a);
+  else if (a.nd > 0)
+    hipLaunchKernelGGL((project_kernel<RB, NB, true, false>), grid, dim3(kBlock), lds, st, a);
+  else if (fast)
+    hipLaunchKernelGGL((project_kernel<RB, NB, false, true>), grid, dim3(kBlock), lds, st, a);
   else
-    hipLaunchKernelGGL((project_kernel<RB, NB, false>), grid, dim3(kBlock), lds, st, a);
+    hipLaunchKernelGGL((project_kernel<RB, NB, false, false>), grid, dim3(kBlock), lds, st, a);
   return hipGetLastError();
 }
 

@@ -35,29 +35,6 @@ __device__ __forceinline__ double block_sum_d(double v, double* red4) {
   return (red4[0] + red4[1]) + (red4[2] + red4[3]);
 }
 
-// Per-tile squared norm is ready (block-uniform value v): record it; the last
-// tile of the sample turns the tile values into the estimate.
-__device__ void finish_tile(const TokredArgs& a, int i, int tile, double v, double* dred,
-                            int* flag) {
-  const int tid = threadIdx.x;
-  if (tid == 0) {
-    a.tilesq[(int64_t)i * a.ntiles + tile] = (float)v;
-    __threadfence();
-    *flag = (atomicAdd(&a.cnt_sample[i], 1u) == (uint32_t)(a.ntiles - 1));
-  }
-  __syncthreads();
-  if (!*flag) return;
-  __threadfence();
-  double t = 0.0;
-  for (int k = tid; k < a.ntiles; k += kBlock) t += (double)a.tilesq[(int64_t)i * a.ntiles + k];
-  t = block_sum_d(t, dred);
-  if (tid == 0) {
-    const float est = (float)(t * (double)a.scale);
-    a.n2[i] = (a.accumulate ? a.n2[i] : 0.f) + est;
-    if (a.n2_layer) a.n2_layer[i] = est;
-  }
-}
-
 __device__ __forceinline__ void store4(const TokredArgs& a, int i, int c, int j, const float v[4]) {
   if (c >= a.ncols) return;
   if (a.M) {
@@ -79,11 +56,10 @@ __device__ __forceinline__ void store4(const TokredArgs& a, int i, int c, int j,
   }
 }
 
-template <int NB>
+template <int NB, bool FAST>
 __global__ __launch_bounds__(kBlock) void tokred_kernel(TokredArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t lds[2][kStage * kLdsLd];
   __shared__ double dred[4];
-  __shared__ int flag;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int g = lane >> 4, l16 = lane & 15, r4 = l16 >> 2, c4 = lane & 3;
   const int i = blockIdx.y;
@@ -103,7 +79,7 @@ __global__ __launch_bounds__(kBlock) void tokred_kernel(TokredArgs a) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int64_t t = tok0 + lr0 + 16 * q;
-      gv[q] = (t < te) ? load_bf16x8(xs + t * a.ldx, jc, a.n, a.vec) : uint4{0, 0, 0, 0};
+      gv[q] = load_bf16x8<FAST>(xs + (t < te ? t : 0) * a.ldx, jc, a.n, t < te, xs);
     }
   };
   auto swrite = [&](int buf) {
@@ -163,6 +139,7 @@ __global__ __launch_bounds__(kBlock) void tokred_kernel(TokredArgs a) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) w[x][nb][q] = acc[x][0][nb][q] + acc[x][1][nb][q];
 
+  const int64_t tslot = (int64_t)i * a.ntiles + tile;
   if (a.S == 1) {
     if (a.mode == 0) {
       double sq = 0.0;
@@ -173,7 +150,7 @@ __global__ __launch_bounds__(kBlock) void tokred_kernel(TokredArgs a) {
 #pragma unroll
           for (int q = 0; q < 4; ++q) sq += (double)(w[x][nb][q] * w[x][nb][q]);
       sq = block_sum_d(sq, dred);
-      finish_tile(a, i, tile, sq, dred, &flag);
+      if (tid == 0) a.tilesq[tslot] = sq;
     } else {
 #pragma unroll
       for (int x = 0; x < 2; ++x)
@@ -182,9 +159,7 @@ __global__ __launch_bounds__(kBlock) void tokred_kernel(TokredArgs a) {
     }
     return;
   }
-
-  // token splits: publish the partial tile, the last workgroup of the tile sums them in order
-  const int64_t tslot = (int64_t)i * a.ntiles + tile;
+  // token splits: publish the partial tile; the finish kernel sums the splits in order
   float* mypart = a.part + (tslot * a.S + s) * (int64_t)a.ncols_pad * kTile;
 #pragma unroll
   for (int x = 0; x < 2; ++x)
@@ -193,12 +168,14 @@ __global__ __launch_bounds__(kBlock) void tokred_kernel(TokredArgs a) {
       float* dst = mypart + (int64_t)(16 * nb + l16) * kTile + 16 * (2 * wv + x) + 4 * g;
       *reinterpret_cast<float4*>(dst) = float4{w[x][nb][0], w[x][nb][1], w[x][nb][2], w[x][nb][3]};
     }
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) flag = (atomicAdd(&a.cnt_tile[tslot], 1u) == (uint32_t)(a.S - 1));
-  __syncthreads();
-  if (!flag) return;
-  __threadfence();
+}
+
+// Sum of the token splits of one tile, in split order: its squared norm (mode 0)
+// or the stored tile (mode 1).
+__global__ __launch_bounds__(kBlock) void tokred_splits_kernel(TokredArgs a) {
+  __shared__ double dred[4];
+  const int tid = threadIdx.x, tile = blockIdx.x, i = blockIdx.y;
+  const int64_t tslot = (int64_t)i * a.ntiles + tile;
   const float* tp = a.part + tslot * a.S * (int64_t)a.ncols_pad * kTile;
   double sq = 0.0;
   for (int gi = tid; gi < a.ncols_pad * (kTile / 4); gi += kBlock) {
@@ -212,29 +189,60 @@ __global__ __launch_bounds__(kBlock) void tokred_kernel(TokredArgs a) {
       if (c < a.ncols)
         for (int q = 0; q < 4; ++q) sq += (double)(v[q] * v[q]);
     } else {
-      store4(a, i, c, j0 + j4, v);
+      store4(a, i, c, tile * kTile + j4, v);
     }
   }
   if (a.mode == 0) {
     sq = block_sum_d(sq, dred);
-    finish_tile(a, i, tile, sq, dred, &flag);
+    if (tid == 0) a.tilesq[tslot] = sq;
   }
+}
+
+// estimate_i = scale * sum over tiles (in tile order), into n2 and the per-layer copy
+__global__ __launch_bounds__(kBlock) void tokred_sample_kernel(TokredArgs a) {
+  __shared__ double dred[4];
+  const int i = blockIdx.x;
+  double t = 0.0;
+  for (int k = threadIdx.x; k < a.ntiles; k += kBlock) t += a.tilesq[(int64_t)i * a.ntiles + k];
+  t = block_sum_d(t, dred);
+  if (threadIdx.x == 0) {
+    const float est = (float)(t * (double)a.scale);
+    a.n2[i] = (a.accumulate ? a.n2[i] : 0.f) + est;
+    if (a.n2_layer) a.n2_layer[i] = est;
+  }
+}
+
+hipError_t launch_tokred_splits(const TokredArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL(tokred_splits_kernel, dim3((unsigned)a.ntiles, (unsigned)a.B), dim3(kBlock), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_tokred_sample(const TokredArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL(tokred_sample_kernel, dim3((unsigned)a.B), dim3(kBlock), 0, st, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_tokred(const TokredArgs& a, hipStream_t st) {
   dim3 grid((unsigned)(a.ntiles * a.S), (unsigned)a.B);
+  const bool fast = a.vec && a.n % 8 == 0;
+#define DPRC_TOKRED_CASE(NB)                                                                   \
+  case NB:                                                                                     \
+    if (fast) hipLaunchKernelGGL((tokred_kernel<NB, true>), grid, dim3(kBlock), 0, st, a);     \
+    else hipLaunchKernelGGL((tokred_kernel<NB, false>), grid, dim3(kBlock), 0, st, a);         \
+    break;
   switch (a.ncols_pad / 16) {
-    case 1: hipLaunchKernelGGL(tokred_kernel<1>, grid, dim3(kBlock), 0, st, a); break;
-    case 2: hipLaunchKernelGGL(tokred_kernel<2>, grid, dim3(kBlock), 0, st, a); break;
-    case 3: hipLaunchKernelGGL(tokred_kernel<3>, grid, dim3(kBlock), 0, st, a); break;
-    case 4: hipLaunchKernelGGL(tokred_kernel<4>, grid, dim3(kBlock), 0, st, a); break;
-    case 5: hipLaunchKernelGGL(tokred_kernel<5>, grid, dim3(kBlock), 0, st, a); break;
-    case 6: hipLaunchKernelGGL(tokred_kernel<6>, grid, dim3(kBlock), 0, st, a); break;
-    case 8: hipLaunchKernelGGL(tokred_kernel<8>, grid, dim3(kBlock), 0, st, a); break;
-    case 12: hipLaunchKernelGGL(tokred_kernel<12>, grid, dim3(kBlock), 0, st, a); break;
-    case 16: hipLaunchKernelGGL(tokred_kernel<16>, grid, dim3(kBlock), 0, st, a); break;
+    DPRC_TOKRED_CASE(1)
+    DPRC_TOKRED_CASE(2)
+    DPRC_TOKRED_CASE(3)
+    DPRC_TOKRED_CASE(4)
+    DPRC_TOKRED_CASE(5)
+    DPRC_TOKRED_CASE(6)
+    DPRC_TOKRED_CASE(8)
+    DPRC_TOKRED_CASE(12)
+    DPRC_TOKRED_CASE(16)
     default: return hipErrorInvalidValue;
   }
+#undef DPRC_TOKRED_CASE
   return hipGetLastError();
 }
 

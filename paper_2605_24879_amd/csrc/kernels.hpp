@@ -52,9 +52,7 @@ struct TokredArgs {
   int32_t ntiles, S, stages_per_split;
   int32_t mode;
   float* part;            // [B][ntiles][S][ncols_pad][kTile] (S > 1)
-  uint32_t* cnt_tile;     // [B][ntiles]
-  float* tilesq;          // [B][ntiles]
-  uint32_t* cnt_sample;   // [B]
+  double* tilesq;         // [B][ntiles] (mode 0)
   float scale;            // estimate = scale * ||M_i||^2
   float* n2;
   float* n2_layer;
@@ -110,6 +108,8 @@ hipError_t launch_probe_bits(int probe_kind, uint32_t key0, uint32_t key1, uint3
 hipError_t launch_fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t st);
 hipError_t launch_project(const ProjectArgs& a, int rows_per_wg, hipStream_t st);
 hipError_t launch_tokred(const TokredArgs& a, hipStream_t st);
+hipError_t launch_tokred_splits(const TokredArgs& a, hipStream_t st);   // S > 1
+hipError_t launch_tokred_sample(const TokredArgs& a, hipStream_t st);   // mode 0
 hipError_t launch_project_f32(const ProjectF32Args& a, hipStream_t st);
 hipError_t launch_tokred_f32(const TokredF32Args& a, hipStream_t st);
 // n2 (=|+=) scale * sum_{c<ncols, j<n} M[i][c][j]^2 (+ optional per-layer copy)

@@ -25,7 +25,7 @@ STREAM_PROBE, STREAM_SKETCH, STREAM_NOISE = 0, 1, 2
 EXPORTS = ["dprc_norm_hutch_workspace", "dprc_norm_hutch", "dprc_norm_hutchpp_workspace",
            "dprc_norm_hutchpp", "dprc_clip_scale", "dprc_clip_accumulate_workspace",
            "dprc_clip_accumulate", "dprc_add_noise", "dprc_probe_bits", "dprc_status_string",
-           "dprc_version"]
+           "dprc_version", "dprc_trace_launches"]
 
 
 class Layer(ctypes.Structure):
@@ -61,6 +61,7 @@ def lib():
             "dprc_probe_bits": (ctypes.c_int, [ctypes.c_int, U64, U32, U32, I64, I32, P, P]),
             "dprc_status_string": (ctypes.c_char_p, [ctypes.c_int]),
             "dprc_version": (ctypes.c_char_p, []),
+            "dprc_trace_launches": (ctypes.c_int, [P, P, I32, P]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -202,3 +203,14 @@ def dprc_probe_bits(probe, seed, layer_id, stream_id, m, k, device="cuda", out=N
 
 def dprc_version():
     return lib().dprc_version().decode()
+
+
+KERNEL_NAMES = {1: "project", 2: "token_reduce", 3: "qr", 4: "hutchpp_final", 5: "clip_scale",
+                6: "accumulate", 7: "splitk_reduce", 8: "noise", 9: "probe_bits", 10: "project_f32",
+                11: "token_reduce_f32", 12: "sample_sq", 13: "accumulate_f32",
+                14: "token_splits", 15: "sample_sum"}
+
+
+def dprc_trace_launches(events_ptr, kinds_ptr, capacity, count_ptr):
+    """Switch the per-launch event hook on (events_ptr = hipEvent_t array) or off (None)."""
+    _check(lib().dprc_trace_launches(events_ptr, kinds_ptr, capacity, count_ptr))
