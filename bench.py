@@ -42,6 +42,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true", help="skip the accumulation-GEMM measurement")
+    ap.add_argument("--graph", action="store_true",
+                    help="replay a captured HIP graph per step instead of launching from the host")
     return ap.parse_args()
 
 
@@ -87,7 +89,7 @@ def make_inputs(cfg, torch, workloads, copies):
     return sets
 
 
-def step_fn(cfg, D, torch, ws_norm, grads):
+def step_fn(cfg, D, torch, ws_norm, grads, ws_acc):
     C = cfg["C"]
 
     def step(layers, n2, c):
@@ -98,7 +100,7 @@ def step_fn(cfg, D, torch, ws_norm, grads):
         D.dprc_clip_scale(n2, C, c=c)
         if cfg["accumulate"]:
             for (A, E, li), g in zip(layers, grads):
-                D.dprc_clip_accumulate(A, E, c, grad=g)
+                D.dprc_clip_accumulate(A, E, c, grad=g, ws=ws_acc)
                 if cfg["noise_sigma"] is not None:
                     D.dprc_add_noise(g, cfg["noise_sigma"], C, 0, li)
     return step
@@ -231,20 +233,38 @@ def main():
     grads = [torch.empty(d, p, device="cuda") for (_, d, p) in cfg["layers"]] if cfg["accumulate"] else []
     n2 = torch.zeros(B, device="cuda")
     c = torch.zeros(B, device="cuda")
-    step = step_fn(cfg, D, torch, ws_n, grads)
+    ws_acc = None
+    if cfg["accumulate"]:
+        need = max(D.dprc_clip_accumulate_workspace(A, E) for (A, E, _) in pairs0)
+        ws_acc = torch.empty(max(1, need), dtype=torch.uint8, device="cuda")
+    step = step_fn(cfg, D, torch, ws_n, grads, ws_acc)
 
-    for w in range(args.warmup):
+    for w in range(max(args.warmup, 1)):
         step(sets[w % copies], n2, c)
     torch.cuda.synchronize()
+    run = lambda s: step(sets[s % copies], n2, c)
+    if args.graph:
+        # one captured graph per input copy; the library enqueues on torch's capture stream
+        graphs = []
+        for ci in range(copies):
+            gr = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gr):
+                step(sets[ci], n2, c)
+            graphs.append(gr)
+        for w in range(args.warmup):
+            graphs[w % copies].replay()
+        torch.cuda.synchronize()
+        run = lambda s: graphs[s % copies].replay()
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     t_start.record()
     for s in range(args.steps):
-        step(sets[s % copies], n2, c)
+        run(s)
     t_end.record()
     torch.cuda.synchronize()
     ms_per_step = t_start.elapsed_time(t_end) / args.steps
-    print(f"[bench] timed {args.steps} steps: {ms_per_step*1e3:.2f} us/step", file=sys.stderr, flush=True)
+    print(f"[bench] timed {args.steps} steps ({'graph replay' if args.graph else 'eager'}): "
+          f"{ms_per_step*1e3:.2f} us/step", file=sys.stderr, flush=True)
 
     # per-kernel durations over the same number of steps, with the launch hook on
     hip = Hip()
@@ -291,7 +311,8 @@ def main():
            "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5),
            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": cfg["dtype"],
            "data": "synthetic (seeded; Llama-3.2-1B layer shapes)",
-           "config": workloads.describe(cfg) | {"C": cfg["C"], "steps_include": step_parts(cfg)},
+           "config": workloads.describe(cfg) | {"C": cfg["C"], "steps_include": step_parts(cfg),
+                                                "launch": "hip_graph_replay" if args.graph else "eager"},
            "roofline": roof, "extra": extra}
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
