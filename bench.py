@@ -296,7 +296,8 @@ def main():
     norm_bytes = workloads.algorithmic_norm_bytes(cfg)
     norm_ms = sum(per_kind.get(k, (0.0, 0))[0] for k in ("project", "token_reduce", "qr", "hutchpp_final",
                                                           "project_f32", "token_reduce_f32", "sample_sq",
-                                                          "probe_bits", "token_splits", "sample_sum")) / args.steps
+                                                          "probe_bits", "token_splits", "sample_sum", "qr_combine", "qr_expand",
+                                                          "hutchpp_sum")) / args.steps
     kernels = {k: {"launches_per_step": v[1] / args.steps, "avg_launch_us": round(v[0] / v[1] * 1e3, 2),
                    "us_per_step": round(v[0] / args.steps * 1e3, 2)} for k, v in sorted(per_kind.items())}
     extra = {"norm_kernels_us_per_step": round(norm_ms * 1e3, 2),

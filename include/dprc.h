@@ -106,7 +106,7 @@ dprc_status dprc_norm_hutch(const dprc_layer* layers, int32_t num_layers, int32_
  * With M_i = X'_i^T X_i (m probed columns): sketch O S = M_i^T (M_i S) with s
  * sketch probes (stream 1), Q = orthonormal basis of its columns (Householder
  * QR), U = M_i Q, V = M_i P - U (Q^T P) with r residual probes P (stream 0),
- * estimate ||U||_F^2 + ||V||_F^2 / r.  s in [0, 64], r in [1, 256],
+ * estimate ||U||_F^2 + ||V||_F^2 / r.  s in [0, 32], r in [1, 256],
  * s + r <= 256, s <= the sketched dimension.  s = 0 gives Hutchinson with r
  * probes.  Outputs as for dprc_norm_hutch. */
 size_t dprc_norm_hutchpp_workspace(const dprc_layer* layers, int32_t num_layers, int32_t s,
@@ -171,7 +171,10 @@ typedef enum {
   DPRC_KERNEL_SAMPLE_SQ = 12,
   DPRC_KERNEL_ACCUMULATE_F32 = 13,
   DPRC_KERNEL_TOKEN_SPLITS = 14,      /* sum of token splits per tile          */
-  DPRC_KERNEL_SAMPLE_SUM = 15         /* per-sample sum of tile squares         */
+  DPRC_KERNEL_SAMPLE_SUM = 15,        /* per-sample sum of tile squares         */
+  DPRC_KERNEL_QR_COMBINE = 16,        /* QR of the stacked block R factors      */
+  DPRC_KERNEL_QR_EXPAND = 17,         /* rows of Q, and Q^T P per row block     */
+  DPRC_KERNEL_HUTCHPP_SUM = 18        /* per-sample Hutch++ estimate            */
 } dprc_kernel_kind;
 dprc_status dprc_trace_launches(hipEvent_t* events, int32_t* kinds, int32_t capacity,
                                 int32_t* count);

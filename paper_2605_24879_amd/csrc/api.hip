@@ -282,7 +282,8 @@ struct PPBufs {
   uint16_t *WShi, *WSlo; int64_t ld_ws;   // pass-1 result, dense operand of pass 2 (bf16)
   float* WS32;                             // same, fp32 path
   float* OS;                               // [B][s][m]
-  double* qrwork;                          // [B][2][s][m]
+  QrArgs qr;                               // QR scratch (s > 0)
+  FinalArgs fin;                           // finalize scratch (s > 0)
   float* Q;                                // [B][s][m]
   uint16_t *Qhi, *Qlo; int64_t ld_q;       // bf16 path
   float* UW;                               // [B][s+r][n]
@@ -307,9 +308,17 @@ size_t hutchpp_layout(const View& v, int32_t s, int32_t r, void* ws, PPBufs* out
       b.WS32 = ar.take<float>((size_t)B * s * v.n);
     }
     b.OS = ar.take<float>((size_t)B * s * v.m);
-    b.qrwork = ar.take<double>((size_t)B * 2 * s * v.m);
     b.Q = ar.take<float>((size_t)B * s * v.m);
     b.UW = ar.take<float>((size_t)B * (s + r) * v.n);
+    const QrPlan qp = qr_plan(v.m, s);
+    b.qr.B = (int32_t)B; b.qr.m = (int32_t)v.m; b.qr.s = s; b.qr.r = r; b.qr.R = qp.R; b.qr.nblk = qp.nblk;
+    b.qr.V = ar.take<double>((size_t)B * qp.nblk * s * qp.R);
+    b.qr.tau = ar.take<double>((size_t)B * qp.nblk * s);
+    b.qr.Rst = ar.take<double>((size_t)B * s * qp.nblk * s);
+    b.qr.Q2 = ar.take<double>((size_t)B * s * qp.nblk * s);
+    b.qr.Cpart = ar.take<double>((size_t)B * qp.nblk * s * r);
+    b.fin.nchunk = final_chunks(v.n);
+    b.fin.Fpart = ar.take<double>((size_t)B * b.fin.nchunk * 2);
   }
   if (v.dtype == DPRC_BF16) {
     b.pass_ws = ar.base ? ar.base + ((ar.off + kAlign - 1) / kAlign) * kAlign : nullptr;
@@ -324,6 +333,19 @@ size_t hutchpp_layout(const View& v, int32_t s, int32_t r, void* ws, PPBufs* out
   }
   if (out) *out = b;
   return ar.off;
+}
+
+// Q = orth(O S) (three TSQR launches), with C = Q^T P formed alongside.
+dprc_status run_qr(PPBufs& b, const View& v, uint32_t k0, uint32_t k1, bool bf16_out, hipStream_t st) {
+  QrArgs& q = b.qr;
+  q.OS = b.OS; q.os_ld = v.m; q.os_ss = (int64_t)q.s * v.m;
+  q.key0 = k0; q.key1 = k1; q.layer = v.layer_id;
+  q.Q = b.Q; q.q_ld = v.m; q.q_ss = (int64_t)q.s * v.m;
+  q.Qhi = bf16_out ? b.Qhi : nullptr; q.Qlo = bf16_out ? b.Qlo : nullptr;
+  q.qh_ld = bf16_out ? b.ld_q : 0; q.qh_ss = (int64_t)q.s * q.qh_ld;
+  if (traced(DPRC_KERNEL_QR, st, [&] { return launch_qr_blocks(q, st); }) != hipSuccess) return DPRC_ERROR_HIP;
+  if (traced(DPRC_KERNEL_QR_COMBINE, st, [&] { return launch_qr_combine(q, st); }) != hipSuccess) return DPRC_ERROR_HIP;
+  return hip_status(traced(DPRC_KERNEL_QR_EXPAND, st, [&] { return launch_qr_expand(q, st); }));
 }
 
 dprc_status hutchpp_layer(const View& v, int32_t s, int32_t r, uint32_t k0, uint32_t k1, float* n2,
@@ -355,10 +377,8 @@ dprc_status hutchpp_layer(const View& v, int32_t s, int32_t r, uint32_t k0, uint
     p2.nd = s; p2.Rhi = b.WShi; p2.Rlo = b.WSlo; p2.ld_r = b.ld_ws;
     p2.mode = 1; p2.M = b.OS; p2.m_ld = v.m;
     if ((stt = run_pass(p2, B, T, k0, k1, v.layer_id, b.pass_ws, st)) != DPRC_SUCCESS) return stt;
-    // Q = orth(O S)
-    e = traced(DPRC_KERNEL_QR, st, [&] { return launch_qr(b.OS, v.m, (int64_t)s * v.m, (int32_t)B, (int32_t)v.m, s, b.qrwork, b.Q, v.m,
-                  (int64_t)s * v.m, b.Qhi, b.Qlo, b.ld_q, (int64_t)s * b.ld_q, st); });
-    if (e != hipSuccess) return DPRC_ERROR_HIP;
+    // Q = orth(O S) and C = Q^T P
+    if ((stt = run_qr(b, v, k0, k1, true, st)) != DPRC_SUCCESS) return stt;
     // pass 3: [U | W_P] = Xo^T (X [Q | P])
     PassSpec p3{};
     p3.X = X; p3.ldx = v.ldx; p3.m = v.m; p3.Xo = Xo; p3.ldo = v.ldo; p3.n = v.n;
@@ -380,9 +400,8 @@ dprc_status hutchpp_layer(const View& v, int32_t s, int32_t r, uint32_t k0, uint
       if ((e = traced(DPRC_KERNEL_PROJECT_F32, st, [&] { return launch_project_f32(a2, st); })) != hipSuccess) return DPRC_ERROR_HIP;
       TokredF32Args t2{X, v.ldx, T * v.ldx, (int32_t)B, (int32_t)T, (int32_t)v.m, b.Y32, s, b.OS, v.m, (int64_t)s * v.m};
       if ((e = traced(DPRC_KERNEL_TOKEN_REDUCE_F32, st, [&] { return launch_tokred_f32(t2, st); })) != hipSuccess) return DPRC_ERROR_HIP;
-      e = traced(DPRC_KERNEL_QR, st, [&] { return launch_qr(b.OS, v.m, (int64_t)s * v.m, (int32_t)B, (int32_t)v.m, s, b.qrwork, b.Q, v.m,
-                    (int64_t)s * v.m, nullptr, nullptr, 0, 0, st); });
-      if (e != hipSuccess) return DPRC_ERROR_HIP;
+      const dprc_status sq = run_qr(b, v, k0, k1, false, st);
+      if (sq != DPRC_SUCCESS) return sq;
     }
     if ((e = traced(DPRC_KERNEL_PROBE_BITS, st, [&] { return launch_probe_bits(0, k0, k1, v.layer_id, 0, v.m, r, b.zb, st); })) != hipSuccess) return DPRC_ERROR_HIP;
     ProjectF32Args a3{X, v.ldx, T * v.ldx, (int32_t)B, (int32_t)T, (int32_t)v.m, s, r, s + r, b.Q, v.m,
@@ -395,9 +414,13 @@ dprc_status hutchpp_layer(const View& v, int32_t s, int32_t r, uint32_t k0, uint
       return hip_status(traced(DPRC_KERNEL_SAMPLE_SQ, st, [&] { return launch_sample_sq(b.UW, v.n, (int64_t)r * v.n, (int32_t)B, r, (int32_t)v.n,
                                          1.0f / (float)r, n2, n2_layer, accumulate, st); }));
   }
-  return hip_status(traced(DPRC_KERNEL_HUTCHPP_FINAL, st, [&] { return launch_hutchpp_final(b.UW, v.n, (int64_t)(s + r) * v.n, b.Q, v.m, (int64_t)s * v.m,
-                                         (int32_t)B, (int32_t)v.n, (int32_t)v.m, s, r, k0, k1, v.layer_id,
-                                         n2, n2_layer, accumulate, st); }));
+  FinalArgs fa = b.fin;
+  fa.UW = b.UW; fa.uw_ld = v.n; fa.uw_ss = (int64_t)(s + r) * v.n;
+  fa.B = (int32_t)B; fa.n = (int32_t)v.n; fa.s = s; fa.r = r; fa.nblk = b.qr.nblk;
+  fa.Cpart = b.qr.Cpart; fa.n2 = n2; fa.n2_layer = n2_layer; fa.accumulate = accumulate;
+  if ((e = traced(DPRC_KERNEL_HUTCHPP_FINAL, st, [&] { return launch_hpp_rows(fa, st); })) != hipSuccess)
+    return DPRC_ERROR_HIP;
+  return hip_status(traced(DPRC_KERNEL_HUTCHPP_SUM, st, [&] { return launch_hpp_sum(fa, st); }));
 }
 
 // ---- clipped accumulation ----------------------------------------------------------------------------
@@ -474,7 +497,7 @@ dprc_status dprc_norm_hutch(const dprc_layer* layers, int32_t num_layers, int32_
 size_t dprc_norm_hutchpp_workspace(const dprc_layer* layers, int32_t num_layers, int32_t s, int32_t r,
                                    dprc_side side) {
   if (check_layers(layers, num_layers, side) != DPRC_SUCCESS) return 0;
-  if (s < 0 || s > 64 || r < 1 || r > 256 || s + r > 256) return 0;
+  if (s < 0 || s > 32 || r < 1 || r > 256 || s + r > 256) return 0;
   size_t need = 0;
   for (int32_t l = 0; l < num_layers; ++l) {
     const View v = view_of(layers[l], side);
@@ -489,7 +512,7 @@ dprc_status dprc_norm_hutchpp(const dprc_layer* layers, int32_t num_layers, int3
                               size_t ws_bytes, hipStream_t stream) {
   dprc_status st = check_layers(layers, num_layers, side);
   if (st != DPRC_SUCCESS) return st;
-  if (s < 0 || s > 64 || r < 1 || r > 256 || s + r > 256 || !n2) return DPRC_ERROR_INVALID_VALUE;
+  if (s < 0 || s > 32 || r < 1 || r > 256 || s + r > 256 || !n2) return DPRC_ERROR_INVALID_VALUE;
   for (int32_t l = 0; l < num_layers; ++l)
     if (s > view_of(layers[l], side).m) return DPRC_ERROR_INVALID_VALUE;
   const size_t need = dprc_norm_hutchpp_workspace(layers, num_layers, s, r, side);

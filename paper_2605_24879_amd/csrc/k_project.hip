@@ -101,7 +101,7 @@ __global__ __launch_bounds__(kBlock) void project_kernel(ProjectArgs a) {
             const uint32_t word = a.nz > 0 ? zw[(isz ? cz : 0) * wpc + 2 * q + ks] : 0u;
             const uint4 zb = signs_to_bf16x8((word >> (8 * g)) & 0xFFu);
             uint4 bh = isz ? zb : uint4{0, 0, 0, 0}, bl = uint4{0, 0, 0, 0};
-            if (DENSE) {
+            if (DENSE && 16 * nb < a.nd) {   // uniform: only column blocks that hold dense columns load them
               const bool isd = c < a.nd;
               const int64_t off = (int64_t)(isd ? c : 0) * a.ld_r + u0 + 32 * ks + 8 * g;
               const uint4 dh = *reinterpret_cast<const uint4*>(rhi + off);

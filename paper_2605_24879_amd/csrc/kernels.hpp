@@ -102,6 +102,42 @@ struct TokredF32Args {
   int64_t m_ld, m_ss;
 };
 
+// Tall-skinny QR of O S (m x s per sample) and C = Q^T P (Hutch++).
+struct QrArgs {
+  const float* OS;        // OS[i*os_ss + c*os_ld + j]
+  int64_t os_ld, os_ss;
+  int32_t B, m, s, r;
+  int32_t R, nblk;        // rows per block, blocks
+  double* V;              // [B][nblk][s][R] block reflectors
+  double* tau;            // [B][nblk][s]
+  double* Rst;            // [B][s][nblk*s] stacked R factors, then their reflectors
+  double* Q2;             // [B][s][nblk*s]
+  double* Cpart;          // [B][nblk][s][r]
+  uint32_t key0, key1, layer;
+  float* Q;               // Q[i*q_ss + c*q_ld + j] (may be null)
+  int64_t q_ld, q_ss;
+  uint16_t* Qhi;          // bf16 hi/lo pairs, zero for rows m .. qh_ld-1 (may be null)
+  uint16_t* Qlo;
+  int64_t qh_ld, qh_ss;
+};
+struct QrPlan {
+  int32_t R, nblk;
+};
+QrPlan qr_plan(int64_t m, int s);
+
+// Hutch++ estimate from U | W_P (UW[i*uw_ss + c*uw_ld + j], c < s + r) and C.
+struct FinalArgs {
+  const float* UW;
+  int64_t uw_ld, uw_ss;
+  int32_t B, n, s, r, nblk, nchunk;
+  const double* Cpart;    // [B][nblk][s][r]
+  double* Fpart;          // [B][nchunk][2]
+  float* n2;
+  float* n2_layer;
+  int32_t accumulate;
+};
+int32_t final_chunks(int64_t n);
+
 hipError_t launch_probe_bits(int probe_kind, uint32_t key0, uint32_t key1, uint32_t layer,
                              uint32_t stream_id, int64_t m, int32_t k, uint32_t* out,
                              hipStream_t st);
@@ -116,14 +152,11 @@ hipError_t launch_tokred_f32(const TokredF32Args& a, hipStream_t st);
 hipError_t launch_sample_sq(const float* M, int64_t m_ld, int64_t m_ss, int32_t B, int32_t ncols,
                             int32_t n, float scale, float* n2, float* n2_layer, int accumulate,
                             hipStream_t st);
-hipError_t launch_qr(const float* OS, int64_t os_ld, int64_t os_ss, int32_t B, int32_t m,
-                     int32_t s, double* work, float* Q, int64_t q_ld, int64_t q_ss, uint16_t* Qhi,
-                     uint16_t* Qlo, int64_t qh_ld, int64_t qh_ss, hipStream_t st);
-hipError_t launch_hutchpp_final(const float* UW, int64_t uw_ld, int64_t uw_ss, const float* Q,
-                                int64_t q_ld, int64_t q_ss, int32_t B, int32_t n, int32_t m,
-                                int32_t s, int32_t r, uint32_t key0, uint32_t key1,
-                                uint32_t layer, float* n2, float* n2_layer, int accumulate,
-                                hipStream_t st);
+hipError_t launch_qr_blocks(const QrArgs& a, hipStream_t st);
+hipError_t launch_qr_combine(const QrArgs& a, hipStream_t st);
+hipError_t launch_qr_expand(const QrArgs& a, hipStream_t st);
+hipError_t launch_hpp_rows(const FinalArgs& a, hipStream_t st);
+hipError_t launch_hpp_sum(const FinalArgs& a, hipStream_t st);
 hipError_t launch_clip_scale(const float* n2, int64_t B, float C, float* c, hipStream_t st);
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t st);
 hipError_t launch_gemm_f32(const float* A, int64_t lda, int64_t a_ss, const float* E, int64_t lde,

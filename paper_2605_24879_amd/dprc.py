@@ -208,7 +208,7 @@ def dprc_version():
 KERNEL_NAMES = {1: "project", 2: "token_reduce", 3: "qr", 4: "hutchpp_final", 5: "clip_scale",
                 6: "accumulate", 7: "splitk_reduce", 8: "noise", 9: "probe_bits", 10: "project_f32",
                 11: "token_reduce_f32", 12: "sample_sq", 13: "accumulate_f32",
-                14: "token_splits", 15: "sample_sum"}
+                14: "token_splits", 15: "sample_sum", 16: "qr_combine", 17: "qr_expand", 18: "hutchpp_sum"}
 
 
 def dprc_trace_launches(events_ptr, kinds_ptr, capacity, count_ptr):

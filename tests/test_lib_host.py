@@ -82,7 +82,7 @@ def test_hutchpp_and_accumulate_validation():
     L = dprc.lib()
     arr = (dprc.Layer * 1)(_fake_layer())
     assert L.dprc_norm_hutchpp_workspace(arr, 1, 16, 32, 0) > 0
-    assert L.dprc_norm_hutchpp(arr, 1, 65, 4, 0, 0, 0x40000, None, 0, 0x30000, 1 << 30, None) == 1
+    assert L.dprc_norm_hutchpp(arr, 1, 33, 4, 0, 0, 0x40000, None, 0, 0x30000, 1 << 30, None) == 1
     assert L.dprc_norm_hutchpp(arr, 1, 4, 0, 0, 0, 0x40000, None, 0, 0x30000, 1 << 30, None) == 1
     assert L.dprc_norm_hutchpp(arr, 1, 49, 4, 0, 0, 0x40000, None, 0, 0x30000, 1 << 30, None) == 1  # s > p
     assert L.dprc_norm_hutchpp(arr, 1, 4, 4, 0, 0, 0x40000, None, 0, 0x30000, 0, None) == 3
