@@ -149,8 +149,9 @@ dprc_status dprc_probe_bits(dprc_probe probe, uint64_t seed, uint32_t layer_id,
 
 /* ---- per-launch timing (diagnostics, for profilers and benchmarks) ------------
  * While `events` is non-NULL, every kernel that a dprc call enqueues from THIS
- * host thread is bracketed by hipEventRecord on that call's stream: launch j
- * (counted from this call) records events[2j] before and events[2j+1] after,
+ * host thread is launched with hipExtLaunchKernelGGL and start/stop events that
+ * the dispatch itself stamps (no extra packets): launch j (counted from this
+ * call) uses events[2j] (start) and events[2j+1] (stop),
  * kinds[j] (if kinds is non-NULL) receives its dprc_kernel_kind, and the host
  * integer *count is advanced; recording stops once *count reaches `capacity`
  * (the events array must hold 2*capacity created events).  *count is reset

@@ -153,18 +153,17 @@ struct Trace {
   int32_t* count = nullptr;
 };
 thread_local Trace g_trace;
+thread_local LaunchEvents g_next_events;
 
+// The start/stop events ride on the launch itself (hipExtLaunchKernelGGL in DPRC_LAUNCH).
 template <class F>
-hipError_t traced(int kind, hipStream_t st, F&& launch) {
+hipError_t traced(int kind, hipStream_t, F&& launch) {
   Trace& t = g_trace;
   const bool on = t.events && t.count && *t.count < t.capacity;
-  if (on) {
-    hipError_t e = hipEventRecord(t.events[2 * *t.count], st);
-    if (e != hipSuccess) return e;
-  }
-  hipError_t e = launch();
+  if (on) g_next_events = LaunchEvents{t.events[2 * *t.count], t.events[2 * *t.count + 1]};
+  const hipError_t e = launch();
+  g_next_events = LaunchEvents{};
   if (on && e == hipSuccess) {
-    e = hipEventRecord(t.events[2 * *t.count + 1], st);
     if (t.kinds) t.kinds[*t.count] = kind;
     ++*t.count;
   }
@@ -440,6 +439,10 @@ GemmPlan gemm_plan(const dprc_layer& L) {
 }
 
 }  // namespace
+
+namespace dprc {
+LaunchEvents& next_launch_events() { return g_next_events; }
+}  // namespace dprc
 
 extern "C" {
 

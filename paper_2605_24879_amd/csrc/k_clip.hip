@@ -19,7 +19,7 @@ __global__ void clip_scale_kernel(const float* n2, int64_t B, float C, float* c)
 }
 
 hipError_t launch_clip_scale(const float* n2, int64_t B, float C, float* c, hipStream_t st) {
-  hipLaunchKernelGGL(clip_scale_kernel, dim3((unsigned)ceil_div(B, 256)), dim3(256), 0, st, n2, B, C, c);
+  DPRC_LAUNCH(clip_scale_kernel, dim3((unsigned)ceil_div(B, 256)), dim3(256), 0, st, n2, B, C, c);
   return hipGetLastError();
 }
 
@@ -159,9 +159,9 @@ __global__ __launch_bounds__(kBlock) void gemm_kernel(GemmArgs a) {
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t st) {
   dim3 grid((unsigned)ceil_div(a.p, kGT), (unsigned)ceil_div(a.d, kGT), (unsigned)a.S);
   if (a.vec_a && a.vec_e && a.d % 8 == 0 && a.p % 8 == 0)
-    hipLaunchKernelGGL(gemm_kernel<true>, grid, dim3(kBlock), 0, st, a);
+    DPRC_LAUNCH(gemm_kernel<true>, grid, dim3(kBlock), 0, st, a);
   else
-    hipLaunchKernelGGL(gemm_kernel<false>, grid, dim3(kBlock), 0, st, a);
+    DPRC_LAUNCH(gemm_kernel<false>, grid, dim3(kBlock), 0, st, a);
   return hipGetLastError();
 }
 
@@ -182,7 +182,7 @@ hipError_t launch_splitk_reduce(const float* part, int32_t S, int32_t d, int32_t
                                 int64_t ldo, int accumulate, hipStream_t st) {
   const int64_t total = (int64_t)d * p;
   const unsigned blocks = (unsigned)std::min<int64_t>(8192, ceil_div(total, 256));
-  hipLaunchKernelGGL(splitk_reduce_kernel, dim3(blocks), dim3(256), 0, st, part, S, d, p, out, ldo, accumulate);
+  DPRC_LAUNCH(splitk_reduce_kernel, dim3(blocks), dim3(256), 0, st, part, S, d, p, out, ldo, accumulate);
   return hipGetLastError();
 }
 
@@ -211,7 +211,7 @@ hipError_t launch_gemm_f32(const float* A, int64_t lda, int64_t a_ss, const floa
                            const float* c, float* out, int64_t ldo, int accumulate,
                            hipStream_t st) {
   const int64_t total = (int64_t)d * p;
-  hipLaunchKernelGGL(gemm_f32_kernel, dim3((unsigned)ceil_div(total, 256)), dim3(256), 0, st, A, lda,
+  DPRC_LAUNCH(gemm_f32_kernel, dim3((unsigned)ceil_div(total, 256)), dim3(256), 0, st, A, lda,
                      a_ss, E, lde, e_ss, B, T, d, p, c, out, ldo, accumulate);
   return hipGetLastError();
 }
@@ -258,7 +258,7 @@ hipError_t launch_noise(float* g, int64_t numel, float scale, uint32_t key0, uin
                         uint32_t tensor_id, hipStream_t st) {
   const int64_t nq = (numel + 3) / 4;
   const unsigned blocks = (unsigned)std::min<int64_t>(16384, ceil_div(nq, 256));
-  hipLaunchKernelGGL(noise_kernel, dim3(blocks), dim3(256), 0, st, g, numel, scale, key0, key1, tensor_id);
+  DPRC_LAUNCH(noise_kernel, dim3(blocks), dim3(256), 0, st, g, numel, scale, key0, key1, tensor_id);
   return hipGetLastError();
 }
 

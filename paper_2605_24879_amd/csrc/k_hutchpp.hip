@@ -260,7 +260,7 @@ static size_t qr_lds_expand(const QrArgs& a) {
 }
 
 hipError_t launch_qr_blocks(const QrArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(qr_blocks_kernel, dim3((unsigned)a.nblk, (unsigned)a.B), dim3(kQrThreads),
+  DPRC_LAUNCH(qr_blocks_kernel, dim3((unsigned)a.nblk, (unsigned)a.B), dim3(kQrThreads),
                      (size_t)a.s * a.R * 8, st, a);
   return hipGetLastError();
 }
@@ -268,12 +268,12 @@ hipError_t launch_qr_blocks(const QrArgs& a, hipStream_t st) {
 hipError_t launch_qr_combine(const QrArgs& a, hipStream_t st) {
   const size_t bytes = (size_t)2 * a.s * a.nblk * a.s * 8;
   const int in_lds = bytes <= 96 * 1024;
-  hipLaunchKernelGGL(qr_combine_kernel, dim3((unsigned)a.B), dim3(kQrThreads), in_lds ? bytes : 0, st, a, in_lds);
+  DPRC_LAUNCH(qr_combine_kernel, dim3((unsigned)a.B), dim3(kQrThreads), in_lds ? bytes : 0, st, a, in_lds);
   return hipGetLastError();
 }
 
 hipError_t launch_qr_expand(const QrArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(qr_expand_kernel, dim3((unsigned)a.nblk, (unsigned)a.B), dim3(kQrThreads), qr_lds_expand(a),
+  DPRC_LAUNCH(qr_expand_kernel, dim3((unsigned)a.nblk, (unsigned)a.B), dim3(kQrThreads), qr_lds_expand(a),
                      st, a);
   return hipGetLastError();
 }
@@ -336,13 +336,13 @@ __global__ __launch_bounds__(kQrThreads) void hpp_sum_kernel(FinalArgs a) {
 }
 
 hipError_t launch_hpp_rows(const FinalArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(hpp_rows_kernel, dim3((unsigned)a.nchunk, (unsigned)a.B), dim3(kFinRows),
+  DPRC_LAUNCH(hpp_rows_kernel, dim3((unsigned)a.nchunk, (unsigned)a.B), dim3(kFinRows),
                      (size_t)a.s * a.r * 4, st, a);
   return hipGetLastError();
 }
 
 hipError_t launch_hpp_sum(const FinalArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(hpp_sum_kernel, dim3((unsigned)a.B), dim3(kQrThreads), 0, st, a);
+  DPRC_LAUNCH(hpp_sum_kernel, dim3((unsigned)a.B), dim3(kQrThreads), 0, st, a);
   return hipGetLastError();
 }
 

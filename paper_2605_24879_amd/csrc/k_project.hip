@@ -154,13 +154,13 @@ static hipError_t launch_rb_nb(const ProjectArgs& a, hipStream_t st) {
   dim3 grid((unsigned)(a.T_pad / (16 * RB)), (unsigned)a.B);
   const bool fast = a.vec && a.m % 8 == 0;
   if (a.nd > 0 && fast)
-    hipLaunchKernelGGL((project_kernel<RB, NB, true, true>), grid, dim3(kBlock), lds, st, a);
+    DPRC_LAUNCH((project_kernel<RB, NB, true, true>), grid, dim3(kBlock), lds, st, a);
   else if (a.nd > 0)
-    hipLaunchKernelGGL((project_kernel<RB, NB, true, false>), grid, dim3(kBlock), lds, st, a);
+    DPRC_LAUNCH((project_kernel<RB, NB, true, false>), grid, dim3(kBlock), lds, st, a);
   else if (fast)
-    hipLaunchKernelGGL((project_kernel<RB, NB, false, true>), grid, dim3(kBlock), lds, st, a);
+    DPRC_LAUNCH((project_kernel<RB, NB, false, true>), grid, dim3(kBlock), lds, st, a);
   else
-    hipLaunchKernelGGL((project_kernel<RB, NB, false, false>), grid, dim3(kBlock), lds, st, a);
+    DPRC_LAUNCH((project_kernel<RB, NB, false, false>), grid, dim3(kBlock), lds, st, a);
   return hipGetLastError();
 }
 
@@ -219,7 +219,7 @@ hipError_t launch_probe_bits(int kind, uint32_t key0, uint32_t key1, uint32_t la
   const int64_t nblk = ((m + 31) / 32 + 3) / 4;
   const int64_t total = nblk * k;
   if (total == 0) return hipSuccess;
-  hipLaunchKernelGGL(probe_bits_kernel, dim3((unsigned)ceil_div(total, 256)), dim3(256), 0, st,
+  DPRC_LAUNCH(probe_bits_kernel, dim3((unsigned)ceil_div(total, 256)), dim3(256), 0, st,
                      kind, key0, key1, layer, stream_id, m, k, out);
   return hipGetLastError();
 }
@@ -233,7 +233,7 @@ __global__ void fill_u32_kernel(uint32_t* p, int64_t n, uint32_t v) {
 hipError_t launch_fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t st) {
   if (n <= 0) return hipSuccess;
   const unsigned blocks = (unsigned)std::min<int64_t>(1024, ceil_div(n, 256));
-  hipLaunchKernelGGL(fill_u32_kernel, dim3(blocks), dim3(256), 0, st, p, n, v);
+  DPRC_LAUNCH(fill_u32_kernel, dim3(blocks), dim3(256), 0, st, p, n, v);
   return hipGetLastError();
 }
 
@@ -264,7 +264,7 @@ __global__ void project_f32_kernel(ProjectF32Args a) {
 
 hipError_t launch_project_f32(const ProjectF32Args& a, hipStream_t st) {
   const int64_t total = (int64_t)a.B * a.T * a.ncols;
-  hipLaunchKernelGGL(project_f32_kernel, dim3((unsigned)ceil_div(total, 256)), dim3(256), 0, st, a);
+  DPRC_LAUNCH(project_f32_kernel, dim3((unsigned)ceil_div(total, 256)), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 

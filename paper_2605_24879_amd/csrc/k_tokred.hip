@@ -213,12 +213,12 @@ __global__ __launch_bounds__(kBlock) void tokred_sample_kernel(TokredArgs a) {
 }
 
 hipError_t launch_tokred_splits(const TokredArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(tokred_splits_kernel, dim3((unsigned)a.ntiles, (unsigned)a.B), dim3(kBlock), 0, st, a);
+  DPRC_LAUNCH(tokred_splits_kernel, dim3((unsigned)a.ntiles, (unsigned)a.B), dim3(kBlock), 0, st, a);
   return hipGetLastError();
 }
 
 hipError_t launch_tokred_sample(const TokredArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(tokred_sample_kernel, dim3((unsigned)a.B), dim3(kBlock), 0, st, a);
+  DPRC_LAUNCH(tokred_sample_kernel, dim3((unsigned)a.B), dim3(kBlock), 0, st, a);
   return hipGetLastError();
 }
 
@@ -227,8 +227,8 @@ hipError_t launch_tokred(const TokredArgs& a, hipStream_t st) {
   const bool fast = a.vec && a.n % 8 == 0;
 #define DPRC_TOKRED_CASE(NB)                                                                   \
   case NB:                                                                                     \
-    if (fast) hipLaunchKernelGGL((tokred_kernel<NB, true>), grid, dim3(kBlock), 0, st, a);     \
-    else hipLaunchKernelGGL((tokred_kernel<NB, false>), grid, dim3(kBlock), 0, st, a);         \
+    if (fast) DPRC_LAUNCH((tokred_kernel<NB, true>), grid, dim3(kBlock), 0, st, a);     \
+    else DPRC_LAUNCH((tokred_kernel<NB, false>), grid, dim3(kBlock), 0, st, a);         \
     break;
   switch (a.ncols_pad / 16) {
     DPRC_TOKRED_CASE(1)
@@ -263,7 +263,7 @@ __global__ void tokred_f32_kernel(TokredF32Args a) {
 
 hipError_t launch_tokred_f32(const TokredF32Args& a, hipStream_t st) {
   const int64_t total = (int64_t)a.B * a.n * a.ncols;
-  hipLaunchKernelGGL(tokred_f32_kernel, dim3((unsigned)ceil_div(total, 256)), dim3(256), 0, st, a);
+  DPRC_LAUNCH(tokred_f32_kernel, dim3((unsigned)ceil_div(total, 256)), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 
@@ -289,7 +289,7 @@ __global__ __launch_bounds__(kBlock) void sample_sq_kernel(const float* M, int64
 hipError_t launch_sample_sq(const float* M, int64_t m_ld, int64_t m_ss, int32_t B, int32_t ncols,
                             int32_t n, float scale, float* n2, float* n2_layer, int accumulate,
                             hipStream_t st) {
-  hipLaunchKernelGGL(sample_sq_kernel, dim3(B), dim3(kBlock), 0, st, M, m_ld, m_ss, ncols, n, scale,
+  DPRC_LAUNCH(sample_sq_kernel, dim3(B), dim3(kBlock), 0, st, M, m_ld, m_ss, ncols, n, scale,
                      n2, n2_layer, accumulate);
   return hipGetLastError();
 }

@@ -2,10 +2,29 @@
 // the library).  Every launch wrapper enqueues on the given stream and returns
 // hipGetLastError().
 #pragma once
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 namespace dprc {
+
+// Start/stop events for the next launch on this host thread, set by the
+// launch-trace hook of the C ABI (null otherwise).  With events, the kernel is
+// launched through hipExtLaunchKernelGGL, which stamps them from the dispatch
+// itself (no extra packets, so no timing overhead is added to the kernel).
+struct LaunchEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+LaunchEvents& next_launch_events();
+
+#define DPRC_LAUNCH(kernel, grid, block, lds, st, ...)                                            \
+  do {                                                                                             \
+    ::dprc::LaunchEvents& ev_ = ::dprc::next_launch_events();                                      \
+    if (ev_.start)                                                                                 \
+      hipExtLaunchKernelGGL(kernel, grid, block, lds, st, ev_.start, ev_.stop, 0u, __VA_ARGS__);   \
+    else                                                                                           \
+      hipLaunchKernelGGL(kernel, grid, block, lds, st, __VA_ARGS__);                               \
+  } while (0)
 
 constexpr int kWave = 64;
 constexpr int kBlock = 256;        // threads per workgroup of the streaming kernels
