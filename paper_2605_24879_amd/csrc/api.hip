@@ -423,20 +423,7 @@ dprc_status hutchpp_layer(const View& v, int32_t s, int32_t r, uint32_t k0, uint
 }
 
 // ---- clipped accumulation ----------------------------------------------------------------------------
-struct GemmPlan {
-  int32_t S, sps, spl;
-};
-GemmPlan gemm_plan(const dprc_layer& L) {
-  GemmPlan g;
-  g.sps = (int32_t)ceil_div(L.T, kStage);
-  const int64_t total = L.B * g.sps;
-  const int64_t tiles = ceil_div(L.d, 128) * ceil_div(L.p, 128);
-  int64_t S = 1;
-  if (tiles < 256) S = std::min<int64_t>(ceil_div(512, tiles), std::max<int64_t>(1, total / 8));
-  g.spl = (int32_t)ceil_div(total, S);
-  g.S = (int32_t)ceil_div(total, g.spl);
-  return g;
-}
+GemmPlan gemm_plan(const dprc_layer& L) { return gemm_plan_v2(L.B, L.T, L.d, L.p); }
 
 }  // namespace
 

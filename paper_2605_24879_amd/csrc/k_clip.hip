@@ -23,148 +23,6 @@ hipError_t launch_clip_scale(const float* n2, int64_t B, float C, float* c, hipS
   return hipGetLastError();
 }
 
-// ---- grad = sum_i c_i A_i^T E_i on bf16 matrix cores ---------------------------------------
-// Workgroup tile 128 (d) x 128 (p), four waves of 64 x 64; the contraction runs
-// over tokens, sample by sample.  Both operands are token-major, so 64-token
-// tiles of A and E are staged in LDS and read back token-contiguous with the
-// LDS transpose read.  The per-sample factor is applied to the fp32
-// accumulator: before the first stage of sample i the accumulator is rescaled
-// by c_prev / c_i, and by the last c at the end, so the result is
-// sum_i c_i (A_i^T E_i) with no bf16 rounding of c_i * E.  Samples with c_i = 0
-// are skipped.  Splits over the (sample, stage) list write fp32 partials that
-// a second kernel sums in a fixed order.
-constexpr int kGT = 128;                   // tile edge
-constexpr int kGLd = kGT + 8;              // padded LDS row
-
-template <bool FAST>
-__global__ __launch_bounds__(kBlock) void gemm_kernel(GemmArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t la[2][kStage * kGLd];
-  __shared__ __attribute__((aligned(16))) uint16_t le[2][kStage * kGLd];
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  const int g = lane >> 4, l16 = lane & 15, r4 = l16 >> 2, c4 = lane & 3;
-  const int wm = wv >> 1, wn = wv & 1;
-  const int p0 = blockIdx.x * kGT, d0 = blockIdx.y * kGT, split = blockIdx.z;
-  const int sps = a.stages_per_sample;
-  const int gs_begin = split * a.stages_per_split;
-  const int gs_end = min(a.B * sps, gs_begin + a.stages_per_split);
-  const int lr0 = tid >> 4, lc = (tid & 15) * 8;
-  const int64_t ja = (int64_t)d0 + lc, je = (int64_t)p0 + lc;
-
-  auto next_valid = [&](int gs) {
-    while (gs < gs_end && a.c[gs / sps] == 0.f) gs = (gs / sps + 1) * sps;
-    return gs;
-  };
-  uint4 ga[4], ge[4];
-  auto gload = [&](int gs) {
-    const int i = gs / sps;
-    const int64_t tok0 = (int64_t)(gs - i * sps) * kStage;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int64_t t = tok0 + lr0 + 16 * q;
-      const bool ok = t < a.T;
-      const uint16_t* as = a.A + (int64_t)i * a.a_ss;
-      const uint16_t* es = a.E + (int64_t)i * a.e_ss;
-      ga[q] = load_bf16x8<FAST>(as + (ok ? t : 0) * a.lda, ja, a.d, ok, as);
-      ge[q] = load_bf16x8<FAST>(es + (ok ? t : 0) * a.lde, je, a.p, ok, es);
-    }
-  };
-  auto swrite = [&](int buf) {
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      *reinterpret_cast<uint4*>(&la[buf][(lr0 + 16 * q) * kGLd + lc]) = ga[q];
-      *reinterpret_cast<uint4*>(&le[buf][(lr0 + 16 * q) * kGLd + lc]) = ge[q];
-    }
-  };
-
-  f32x4_t acc[4][4];
-#pragma unroll
-  for (int x = 0; x < 4; ++x)
-#pragma unroll
-    for (int y = 0; y < 4; ++y) acc[x][y] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-
-  int gs = next_valid(gs_begin);
-  if (gs < gs_end) {
-    gload(gs);
-    swrite(0);
-  }
-  __syncthreads();
-  int buf = 0, cur_i = -1;
-  float cur_c = 0.f;
-  while (gs < gs_end) {
-    const int gnext = next_valid(gs + 1);
-    if (gnext < gs_end) gload(gnext);
-    const int si = gs / sps;
-    if (si != cur_i) {
-      const float ci = a.c[si];
-      if (cur_i >= 0) {
-        const float ratio = cur_c / ci;
-#pragma unroll
-        for (int x = 0; x < 4; ++x)
-#pragma unroll
-          for (int y = 0; y < 4; ++y) acc[x][y] *= ratio;
-      }
-      cur_c = ci;
-      cur_i = si;
-    }
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      uint4 av[4], bv[4];
-#pragma unroll
-      for (int x = 0; x < 4; ++x) {
-        const uint16_t* pa = &la[buf][(32 * ks + 8 * g + r4) * kGLd + 16 * (4 * wm + x) + 4 * c4];
-        av[x] = make_u4(lds_read_tr16(pa), lds_read_tr16(pa + 4 * kGLd));
-        const uint16_t* pe = &le[buf][(32 * ks + 8 * g + r4) * kGLd + 16 * (4 * wn + x) + 4 * c4];
-        bv[x] = make_u4(lds_read_tr16(pe), lds_read_tr16(pe + 4 * kGLd));
-      }
-#pragma unroll
-      for (int x = 0; x < 4; ++x)
-#pragma unroll
-        for (int y = 0; y < 4; ++y) acc[x][y] = mfma16x16x32(av[x], bv[y], acc[x][y]);
-    }
-    if (gnext < gs_end) swrite(buf ^ 1);
-    __syncthreads();
-    buf ^= 1;
-    gs = gnext;
-  }
-
-  // epilogue: lane holds rows d0 + 16*(4wm+x) + 4g + q, column p0 + 16*(4wn+y) + l16
-  float* dst;
-  int64_t ld;
-  bool direct = a.S == 1;
-  if (direct) {
-    dst = a.out;
-    ld = a.ldo;
-  } else {
-    dst = a.part + (int64_t)split * a.d * a.p;
-    ld = a.p;
-  }
-#pragma unroll
-  for (int x = 0; x < 4; ++x)
-#pragma unroll
-    for (int y = 0; y < 4; ++y) {
-      const int col = p0 + 16 * (4 * wn + y) + l16;
-      if (col >= a.p) continue;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int row = d0 + 16 * (4 * wm + x) + 4 * g + q;
-        if (row >= a.d) continue;
-        const float v = acc[x][y][q] * cur_c;
-        float* o = dst + (int64_t)row * ld + col;
-        if (direct && a.accumulate) *o += v;
-        else *o = v;
-      }
-    }
-}
-
-hipError_t launch_gemm(const GemmArgs& a, hipStream_t st) {
-  dim3 grid((unsigned)ceil_div(a.p, kGT), (unsigned)ceil_div(a.d, kGT), (unsigned)a.S);
-  if (a.vec_a && a.vec_e && a.d % 8 == 0 && a.p % 8 == 0)
-    DPRC_LAUNCH(gemm_kernel<true>, grid, dim3(kBlock), 0, st, a);
-  else
-    DPRC_LAUNCH(gemm_kernel<false>, grid, dim3(kBlock), 0, st, a);
-  return hipGetLastError();
-}
-
 __global__ void splitk_reduce_kernel(const float* part, int32_t S, int32_t d, int32_t p, float* out,
                                      int64_t ldo, int accumulate) {
   const int64_t total = (int64_t)d * p;

@@ -98,6 +98,10 @@ struct GemmArgs {
   float* part;            // [S][d][p] (S > 1)
   int32_t vec_a, vec_e;   // token rows 16-byte aligned
 };
+struct GemmPlan {
+  int32_t S, sps, spl, tiles;   // splits, slabs per sample, slabs per split, output tiles
+};
+GemmPlan gemm_plan_v2(int64_t B, int64_t T, int64_t d, int64_t p);
 
 // fp32 (SIMT) variants, used for fp32 inputs.
 struct ProjectF32Args {
