@@ -25,7 +25,7 @@ typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16_t;
 
 constexpr int kGM = 256;            // tile rows (d) and columns (p)
 constexpr int kGK = 32;             // tokens per slab
-constexpr int kGLd = kGM + 16;      // LDS row: 544 bytes, 4 consecutive rows start 32 bytes apart mod 128
+constexpr int kGLd = kGM + 32;      // LDS row: 576 bytes; the 4 rows x 2 column groups of a 32-lane transpose read hit distinct 32-byte bank groups
 constexpr int kGThreads = 512;      // 8 waves
 
 __device__ __forceinline__ f32x16_t mfma32x32x16(const uint4& a, const uint4& b, f32x16_t c) {
@@ -57,29 +57,44 @@ __global__ __launch_bounds__(kGThreads, 1) void gemm_kernel(GemmArgs a) {
   const int lr = tid >> 5, lc = (tid & 31) * 8;             // loads: rows lr + 16q, 8 columns at lc
   const int64_t ja = (int64_t)d0 + lc, je = (int64_t)p0 + lc;
 
-  auto next_valid = [&](int gs) {
-    while (gs < gs_end && a.c[gs / sps] == 0.f) gs = (gs / sps + 1) * sps;
-    return gs;
+  // position in the (sample, slab) list, advanced without divisions; samples with c_i = 0 are skipped
+  struct Pos {
+    int i, st, gs;
+  };
+  auto skip_zero = [&](Pos q) {
+    while (q.gs < gs_end && a.c[q.i] == 0.f) {
+      q.gs += sps - q.st;
+      q.i += 1;
+      q.st = 0;
+    }
+    return q;
+  };
+  auto advance = [&](Pos q) {
+    q.gs += 1;
+    if (++q.st == sps) {
+      q.st = 0;
+      q.i += 1;
+    }
+    return skip_zero(q);
   };
   uint4 ga[2], ge[2];
-  auto gload = [&](int gs) {
-    const int i = gs / sps;
-    const int64_t tok0 = (int64_t)(gs - i * sps) * kGK;
-    const uint16_t* as = a.A + (int64_t)i * a.a_ss;
-    const uint16_t* es = a.E + (int64_t)i * a.e_ss;
+  auto gload = [&](const Pos& q) {
+    const int64_t tok0 = (int64_t)q.st * kGK;
+    const uint16_t* as = a.A + (int64_t)q.i * a.a_ss;
+    const uint16_t* es = a.E + (int64_t)q.i * a.e_ss;
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      const int64_t t = tok0 + lr + 16 * q;
+    for (int r = 0; r < 2; ++r) {
+      const int64_t t = tok0 + lr + 16 * r;
       const bool ok = t < a.T;
-      ga[q] = load_bf16x8<FAST>(as + (ok ? t : 0) * a.lda, ja, a.d, ok, as);
-      ge[q] = load_bf16x8<FAST>(es + (ok ? t : 0) * a.lde, je, a.p, ok, es);
+      ga[r] = load_bf16x8<FAST>(as + (ok ? t : 0) * a.lda, ja, a.d, ok, as);
+      ge[r] = load_bf16x8<FAST>(es + (ok ? t : 0) * a.lde, je, a.p, ok, es);
     }
   };
   auto swrite = [&](int buf) {
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      *reinterpret_cast<uint4*>(&la[buf][(lr + 16 * q) * kGLd + lc]) = ga[q];
-      *reinterpret_cast<uint4*>(&le[buf][(lr + 16 * q) * kGLd + lc]) = ge[q];
+    for (int r = 0; r < 2; ++r) {
+      *reinterpret_cast<uint4*>(&la[buf][(lr + 16 * r) * kGLd + lc]) = ga[r];
+      *reinterpret_cast<uint4*>(&le[buf][(lr + 16 * r) * kGLd + lc]) = ge[r];
     }
   };
 
@@ -91,22 +106,21 @@ __global__ __launch_bounds__(kGThreads, 1) void gemm_kernel(GemmArgs a) {
 #pragma unroll
       for (int q = 0; q < 16; ++q) acc[x][y][q] = 0.f;
 
-  int gs = next_valid(gs_begin);
-  if (gs < gs_end) {
-    gload(gs);
+  Pos cur = skip_zero(Pos{gs_begin / sps, gs_begin % sps, gs_begin});
+  if (cur.gs < gs_end) {
+    gload(cur);
     swrite(0);
   }
-  int gnext = gs < gs_end ? next_valid(gs + 1) : gs_end;
-  if (gnext < gs_end) gload(gnext);
+  Pos nxt = cur.gs < gs_end ? advance(cur) : cur;
+  if (nxt.gs < gs_end) gload(nxt);
   __syncthreads();
   int buf = 0, cur_i = -1;
   float cur_c = 0.f;
   // the lane's transpose-read offsets: rows 8*(g/2) + r4 (+4), columns 16*(g%2) + 4*c4
   const int tr_row = 8 * (g >> 1) + r4, tr_col = 16 * (g & 1) + 4 * c4;
-  while (gs < gs_end) {
-    const int si = gs / sps;
-    if (si != cur_i) {
-      const float ci = a.c[si];
+  while (cur.gs < gs_end) {
+    if (cur.i != cur_i) {
+      const float ci = a.c[cur.i];
       if (cur_i >= 0) {
         const float ratio = cur_c / ci;
 #pragma unroll
@@ -115,7 +129,7 @@ __global__ __launch_bounds__(kGThreads, 1) void gemm_kernel(GemmArgs a) {
           for (int y = 0; y < 2; ++y) acc[x][y] *= ratio;
       }
       cur_c = ci;
-      cur_i = si;
+      cur_i = cur.i;
     }
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
@@ -135,13 +149,13 @@ __global__ __launch_bounds__(kGThreads, 1) void gemm_kernel(GemmArgs a) {
 #pragma unroll
         for (int y = 0; y < 2; ++y) acc[x][y] = mfma32x32x16(av[x], bv[y], acc[x][y]);
     }
-    const int gafter = gnext < gs_end ? next_valid(gnext + 1) : gs_end;
-    if (gnext < gs_end) swrite(buf ^ 1);
-    if (gafter < gs_end) gload(gafter);
+    const Pos after = nxt.gs < gs_end ? advance(nxt) : nxt;
+    if (nxt.gs < gs_end) swrite(buf ^ 1);
+    if (after.gs < gs_end) gload(after);
     __syncthreads();
     buf ^= 1;
-    gs = gnext;
-    gnext = gafter;
+    cur = nxt;
+    nxt = after;
   }
 
   // epilogue: lane holds rows 8*(q/4) + 4*(lane/32) + q%4 and column lane%32 of each 32 x 32 block

@@ -25,8 +25,8 @@ __global__ __launch_bounds__(kBlock) void project_kernel(ProjectArgs a) {
   const int i = blockIdx.y;
   const int t0 = blockIdx.x * 16 * RB;
   const int wpc = a.words_per_chunk;
-  uint32_t* zw = smem;                                            // [nz][wpc]
-  float* red = reinterpret_cast<float*>(smem + (a.nz > 0 ? a.nz * wpc : 0));
+  uint32_t* zw = smem;                                            // [nz][wpc + 1]
+  float* red = reinterpret_cast<float*>(smem + (a.nz > 0 ? a.nz * (wpc + 1) : 0));
   constexpr int RS = 16 * NB + 4;                                 // padded row of a reduction slot
 
   if (a.zero_ptr != nullptr && blockIdx.x == 0 && blockIdx.y == 0)
@@ -64,7 +64,7 @@ __global__ __launch_bounds__(kBlock) void project_kernel(ProjectArgs a) {
         else
           v = u32x4{hadamard_word(w0, c), hadamard_word(w0 + 1, c), hadamard_word(w0 + 2, c),
                     hadamard_word(w0 + 3, c)};
-        uint32_t* dst = zw + c * wpc + 4 * b;
+        uint32_t* dst = zw + c * (wpc + 1) + 4 * b;     // odd row stride: 16 lanes of 16 columns hit 16 banks
         dst[0] = v.x; dst[1] = v.y; dst[2] = v.z; dst[3] = v.w;
       }
       __syncthreads();
@@ -98,7 +98,7 @@ __global__ __launch_bounds__(kBlock) void project_kernel(ProjectArgs a) {
             // select, not branch: every lane issues the same loads
             const int cz = c - a.nd;
             const bool isz = cz >= 0 && cz < a.nz;
-            const uint32_t word = a.nz > 0 ? zw[(isz ? cz : 0) * wpc + 2 * q + ks] : 0u;
+            const uint32_t word = a.nz > 0 ? zw[(isz ? cz : 0) * (wpc + 1) + 2 * q + ks] : 0u;
             const uint4 zb = signs_to_bf16x8((word >> (8 * g)) & 0xFFu);
             uint4 bh = isz ? zb : uint4{0, 0, 0, 0}, bl = uint4{0, 0, 0, 0};
             if (DENSE && 16 * nb < a.nd) {   // uniform: only column blocks that hold dense columns load them
@@ -148,7 +148,7 @@ __global__ __launch_bounds__(kBlock) void project_kernel(ProjectArgs a) {
 
 template <int RB, int NB>
 static hipError_t launch_rb_nb(const ProjectArgs& a, hipStream_t st) {
-  const size_t zbytes = a.nz > 0 ? (size_t)a.nz * a.words_per_chunk * 4 : 0;
+  const size_t zbytes = a.nz > 0 ? (size_t)a.nz * (a.words_per_chunk + 1) * 4 : 0;
   const size_t rbytes = (size_t)4 * 16 * RB * (16 * NB + 4) * 4;
   const size_t lds = zbytes + rbytes;
   dim3 grid((unsigned)(a.T_pad / (16 * RB)), (unsigned)a.B);

@@ -85,7 +85,7 @@ __global__ __launch_bounds__(kBlock) void tokred_kernel(TokredArgs a) {
   auto swrite = [&](int buf) {
 #pragma unroll
     for (int q = 0; q < 4; ++q)
-      *reinterpret_cast<uint4*>(&lds[buf][(lr0 + 16 * q) * kLdsLd + lc]) = gv[q];
+      *reinterpret_cast<uint4*>(&lds[buf][(lr0 + 16 * q) * kLdsLd + lds_swz(lr0 + 16 * q, lc)]) = gv[q];
   };
 
   f32x4_t acc[2][2][NB];
@@ -118,7 +118,8 @@ __global__ __launch_bounds__(kBlock) void tokred_kernel(TokredArgs a) {
 #pragma unroll
       for (int x = 0; x < 2; ++x) {
         const int mb = 2 * wv + x;
-        const uint16_t* p = &lds[buf][(32 * ks + 8 * g + r4) * kLdsLd + 16 * mb + 4 * c4];
+        // rows 32ks + 8g + r4 (+4) all have bit 3 equal to g & 1
+        const uint16_t* p = &lds[buf][(32 * ks + 8 * g + r4) * kLdsLd + ((16 * mb + 4 * c4) ^ ((g & 1) << 6))];
         const uint4 av = make_u4(lds_read_tr16(p), lds_read_tr16(p + 4 * kLdsLd));
 #pragma unroll
         for (int h = 0; h < 2; ++h)

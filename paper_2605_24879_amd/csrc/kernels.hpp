@@ -30,7 +30,12 @@ constexpr int kWave = 64;
 constexpr int kBlock = 256;        // threads per workgroup of the streaming kernels
 constexpr int kStage = 64;         // tokens per pipeline stage of the token reduction
 constexpr int kTile = 128;         // result rows per token-reduction workgroup
-constexpr int kLdsLd = kTile + 8;  // padded LDS row (elements) of a staged 64 x 128 bf16 tile
+// Padded LDS row (elements) of a staged 64 x 128 bf16 tile: 288 bytes, so the four
+// rows of one 16-lane transpose read start 32 bytes apart; rows with bit 3 set are
+// stored with their 64-column halves swapped, so the rows 8 apart that neighbouring
+// lane groups read land in the other half of the banks.
+constexpr int kLdsLd = kTile + 16;
+__host__ __device__ constexpr int lds_swz(int row, int col) { return col ^ (((row >> 3) & 1) << 6); }
 
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
