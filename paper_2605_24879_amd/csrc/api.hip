@@ -102,16 +102,16 @@ int pad_cols(int ncols) {
 int rows_per_wg(int64_t rows, int ncols_pad) {
   const int nb = ncols_pad / 16;
   int rb = 1;
-  if (rows >= 64 * 1024) rb = 4;
-  else if (rows >= 32 * 1024) rb = 2;
+  if (rows >= 32 * 1024) rb = 2;
   while (rb > 1 && rb * nb > 8) rb >>= 1;
   return 16 * rb;
 }
 
 int words_per_chunk(int64_t m, int nz) {
-  const int64_t all = round_up(ceil_div(m, 32), 4);
+  // whole 512-column stages of the projection kernel per chunk
+  const int64_t all = round_up(ceil_div(m, 32), 16);
   if (nz <= 0) return (int)all;
-  return (int)std::min<int64_t>(all, std::max(4, (8192 / nz) & ~3));
+  return (int)std::min<int64_t>(all, std::max(16, (8192 / nz) & ~15));
 }
 
 // Token-reduction geometry for one (operand width n, columns) pass.

@@ -112,6 +112,36 @@ __device__ __forceinline__ uint4 load8_elem(const uint16_t* row, int64_t u, int6
   return uint4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
 }
 
+// Raw buffer resource over [base, base + bytes): a load at a byte offset at or
+// beyond `bytes` returns zero without touching memory (hardware range check), so
+// masked lanes need no branch, only an out-of-range offset.  bytes < 2^31; base
+// and bytes are wave-uniform (the resource lives in scalar registers; reading the
+// byte count through readfirstlane keeps a value that the compiler computed in a
+// vector register from turning every load into a loop over lanes).
+constexpr uint32_t kOobOffset = 0x80000000u;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0,
+                                           (int)__builtin_amdgcn_readfirstlane(bytes), 0x00020000);
+}
+__device__ __forceinline__ uint4 buffer_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
+}
+
+// The 8 bf16 values +-1 of one byte of probe signs (bit set -> -1) as a 16x16x32
+// B operand fragment.  `P` holds the byte in bits 0..7 of both 16-bit halves
+// (bits 8..15 of each half are ignored); `mask` = 0x80008000 and `one` =
+// 0x3F803F80 for a probe column, both 0 for a column that takes zeros.  Dword j
+// gets bit 2j into the sign of its low bf16 and bit 2j+1 into the sign of its high
+// bf16: a packed 16-bit shift left moves both into bit 15 of their halves.
+typedef unsigned short u16x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t shl16x2(uint32_t v, unsigned short lo, unsigned short hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_bit_cast(u16x2_t, v) << u16x2_t{lo, hi});
+}
+__device__ __forceinline__ uint4 expand_signs(uint32_t P, uint32_t mask, uint32_t one) {
+  return uint4{(shl16x2(P, 15, 14) & mask) | one, (shl16x2(P, 13, 12) & mask) | one,
+               (shl16x2(P, 11, 10) & mask) | one, (shl16x2(P, 9, 8) & mask) | one};
+}
+
 template <bool FAST>
 __device__ __forceinline__ uint4 load_bf16x8(const uint16_t* row, int64_t u, int64_t lim, bool row_ok,
                                              const uint16_t* safe) {
@@ -135,6 +165,12 @@ __device__ __forceinline__ uint2 lds_read_tr16(const uint16_t* p) {
 }
 
 __device__ __forceinline__ uint4 make_u4(uint2 a, uint2 b) { return uint4{a.x, a.y, b.x, b.y}; }
+
+// component-wise select (a select of whole vectors can end up as a select of
+// their stack addresses)
+__device__ __forceinline__ uint4 select4(bool c, const uint4& a, const uint4& b) {
+  return uint4{c ? a.x : b.x, c ? a.y : b.y, c ? a.z : b.z, c ? a.w : b.w};
+}
 
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll

@@ -61,7 +61,7 @@ __global__ __launch_bounds__(kGThreads, 1) void gemm_kernel(GemmArgs a) {
   struct Pos {
     int i, st, gs;
   };
-  auto skip_zero = [&](Pos q) {
+  auto skip_zero = [&](Pos q) __attribute__((always_inline)) {
     while (q.gs < gs_end && a.c[q.i] == 0.f) {
       q.gs += sps - q.st;
       q.i += 1;
@@ -69,7 +69,7 @@ __global__ __launch_bounds__(kGThreads, 1) void gemm_kernel(GemmArgs a) {
     }
     return q;
   };
-  auto advance = [&](Pos q) {
+  auto advance = [&](Pos q) __attribute__((always_inline)) {
     q.gs += 1;
     if (++q.st == sps) {
       q.st = 0;
@@ -78,7 +78,7 @@ __global__ __launch_bounds__(kGThreads, 1) void gemm_kernel(GemmArgs a) {
     return skip_zero(q);
   };
   uint4 ga[2], ge[2];
-  auto gload = [&](const Pos& q) {
+  auto gload = [&](const Pos& q) __attribute__((always_inline)) {
     const int64_t tok0 = (int64_t)q.st * kGK;
     const uint16_t* as = a.A + (int64_t)q.i * a.a_ss;
     const uint16_t* es = a.E + (int64_t)q.i * a.e_ss;
@@ -90,7 +90,7 @@ __global__ __launch_bounds__(kGThreads, 1) void gemm_kernel(GemmArgs a) {
       ge[r] = load_bf16x8<FAST>(es + (ok ? t : 0) * a.lde, je, a.p, ok, es);
     }
   };
-  auto swrite = [&](int buf) {
+  auto swrite = [&](int buf) __attribute__((always_inline)) {
 #pragma unroll
     for (int r = 0; r < 2; ++r) {
       *reinterpret_cast<uint4*>(&la[buf][(lr + 16 * r) * kGLd + lc]) = ga[r];

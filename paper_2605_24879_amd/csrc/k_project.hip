@@ -1,57 +1,167 @@
 // Row projection Y = X R (the E_i Z step of the Hutchinson estimator, Algorithm 2;
 // also the X' W_S and X [Q | P] steps of Hutch++), bf16 matrix cores.
 //
-// A workgroup owns 16*RB token rows of one sample and the whole width m; its
-// four waves split m into interleaved 64-column sub-chunks (one 128-byte line
-// per token row), so every load is a coalesced 16-byte read of a token row and
-// X is read from HBM exactly once.  The +-1 probe columns are generated from
-// Philox into LDS per workgroup (the probe matrix never exists in HBM) and
-// expanded to bf16 in registers; +-1 is exact in bf16 and bf16 x bf16 products
-// are exact in fp32, so Y is the fp32 sum of exact terms.  Dense columns
-// (Hutch++) arrive pre-split into bf16 hi + lo and take two MFMAs.  The four
-// partial Y tiles are summed in LDS and written as bf16 hi/lo pairs in the
-// token-contiguous layout that the token-reduction kernel consumes directly.
+// A workgroup owns 16*RB token rows of one sample and the whole width m, walked
+// in stages of 512 columns; in each stage every wave owns a 128-column slice.
+// A wave reads its slice four token rows at a time (each row a whole 256-byte
+// run, so every load instruction covers full cache lines), keeps P stages in
+// flight in registers, and passes each stage through a private LDS tile (XOR
+// swizzled, no bank conflicts on either side) to get the MFMA operand layout:
+// 16 token rows x 8 consecutive columns per lane.  X is read from HBM exactly
+// once.  The +-1 probe columns are generated from Philox into LDS per workgroup
+// (the probe matrix never exists in HBM) and expanded to bf16 in registers;
+// +-1 is exact in bf16 and bf16 x bf16 products are exact in fp32, so Y is the
+// fp32 sum of exact terms.  Dense columns (Hutch++) arrive pre-split into bf16
+// hi + lo and take two MFMAs.  The four waves' partial Y tiles are summed in
+// LDS and written as bf16 hi/lo pairs in the token-contiguous layout that the
+// token-reduction kernel consumes directly.
 #include <algorithm>
 #include "device.hpp"
 #include "kernels.hpp"
 
 namespace dprc {
 
+constexpr int kProjSlice = 128;                 // columns per wave per stage
+constexpr int kProjStage = 4 * kProjSlice;      // columns per stage
+
+// Orders a wave's LDS accesses around a hand-off between its lanes (LDS
+// operations of one wave execute in issue order; this keeps the compiler from
+// moving them across).
+__device__ __forceinline__ void wave_lds_fence() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+template <int V>
+struct PInt {
+  static constexpr int value = V;
+};
+
 template <int RB, int NB, bool DENSE, bool FAST>
 __global__ __launch_bounds__(kBlock) void project_kernel(ProjectArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint32_t smem[];
+  constexpr int P = RB == 1 ? 4 : 2;            // stages in flight per wave
+  constexpr int NL = 4 * RB;                    // loads per lane per stage
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int g = lane >> 4, l16 = lane & 15;
   const int i = blockIdx.y;
   const int t0 = blockIdx.x * 16 * RB;
-  const int wpc = a.words_per_chunk;
+  const int wpc = a.words_per_chunk;            // a multiple of 16: chunks are whole stages
   uint32_t* zw = smem;                                            // [nz][wpc + 1]
-  float* red = reinterpret_cast<float*>(smem + (a.nz > 0 ? a.nz * (wpc + 1) : 0));
+  uint32_t* region = smem + (a.nz > 0 ? a.nz * (wpc + 1) : 0);
+  // X tiles [4 waves][16 RB rows][128 columns], later the reduction slots
+  uint16_t* xt = reinterpret_cast<uint16_t*>(region) + wv * (16 * RB * kProjSlice);
+  float* red = reinterpret_cast<float*>(region);
   constexpr int RS = 16 * NB + 4;                                 // padded row of a reduction slot
 
   if (a.zero_ptr != nullptr && blockIdx.x == 0 && blockIdx.y == 0)
     for (int idx = tid; idx < a.zero_count; idx += kBlock) a.zero_ptr[idx] = 0u;
 
+  // loads: lane -> row 4j + lane/16 of the tile (j = load index), 16-byte piece
+  // p = (lane%16) ^ row of its slice, stored at LDS slot lane%16
   const uint16_t* xs = a.X + (int64_t)i * a.x_ss;
-  const uint16_t* rowp[RB];
-  bool rowok[RB];
+  const int vrows = max(0, min(16 * RB, a.T - t0));
+  const __amdgpu_buffer_rsrc_t xr = buffer_rsrc(xs + (int64_t)t0 * a.ldx, (uint32_t)(vrows * a.ldx * 2));
+  const int lrow = lane >> 4, lslot = lane & 15;
+  const uint16_t* rowp[NL];
+  uint32_t roff[NL];
+  int lpiece[NL];
 #pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    const int t = t0 + 16 * rb + l16;
-    rowok[rb] = t < a.T;
-    rowp[rb] = xs + (int64_t)(rowok[rb] ? t : 0) * a.ldx;
+  for (int j = 0; j < NL; ++j) {
+    const int rr = 4 * j + lrow;
+    lpiece[j] = lslot ^ (rr & 15);
+    roff[j] = (uint32_t)(rr * a.ldx) * 2u;
+    const int t = t0 + rr;
+    rowp[j] = xs + (int64_t)(t < a.T ? t : 0) * a.ldx;
   }
+
   f32x4_t acc[RB][NB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) acc[rb][nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
+  // per column block: probe columns take +-1, others zero (dense columns come from R)
+  uint32_t zmask[NB], zone[NB];
+  int zrow[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    const int cz = 16 * nb + l16 - a.nd;
+    const bool isz = cz >= 0 && cz < a.nz;
+    zmask[nb] = isz ? 0x80008000u : 0u;
+    zone[nb] = isz ? 0x3F803F80u : 0u;
+    zrow[nb] = (isz ? cz : 0) * (wpc + 1);
+  }
+  const uint32_t psel = (uint32_t)g * 0x00010001u;               // byte g into both 16-bit halves
+
   const uint16_t* rhi = DENSE ? a.Rhi + (int64_t)i * a.r_ss : nullptr;
   const uint16_t* rlo = DENSE ? a.Rlo + (int64_t)i * a.r_ss : nullptr;
 
-  for (int64_t uc = 0; uc < a.m; uc += 32 * (int64_t)wpc) {
-    if (a.nz > 0) {
+  // Stage st (absolute) of this wave: columns st*512 + 128*wv .. + 127.  Stages past
+  // the chunk are issued too, out of range, so every stage has the same loads and
+  // the waits on the in-order load counter count exactly.
+  auto gload = [&](uint4 (&dst)[NL], int st, int col_end) __attribute__((always_inline)) {
+    const int c0 = st * kProjStage + kProjSlice * wv;
+#pragma unroll
+    for (int j = 0; j < NL; ++j) {
+      const int col = c0 + 8 * lpiece[j];
+      if constexpr (FAST) {
+        const bool ok = col < col_end;
+        dst[j] = buffer_load16(xr, ok ? roff[j] + 2u * (uint32_t)col : kOobOffset);
+      } else {
+        dst[j] = load8_elem(rowp[j], col, col_end, t0 + 4 * j + lrow < a.T);
+      }
+    }
+  };
+  auto to_lds = [&](const uint4 (&src)[NL]) __attribute__((always_inline)) {
+    wave_lds_fence();                              // the previous stage's reads are done
+#pragma unroll
+    for (int j = 0; j < NL; ++j)
+      *reinterpret_cast<uint4*>(&xt[(4 * j + lrow) * kProjSlice + 8 * lslot]) = src[j];
+    wave_lds_fence();
+  };
+  auto mult = [&](int st, int uc) __attribute__((always_inline)) {
+    const int c0 = st * kProjStage + kProjSlice * wv;
+    if (c0 >= a.m) return;                         // wave-uniform: slice past the width
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      const int w = (c0 - uc) / 32 + kb;           // probe word of this k-block within the chunk
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        uint4 bh = uint4{0, 0, 0, 0}, bl = uint4{0, 0, 0, 0};
+        if (a.nz > 0) {
+          const uint32_t word = zw[zrow[nb] + w];
+          bh = expand_signs(__builtin_amdgcn_perm(word, word, psel), zmask[nb], zone[nb]);
+        }
+        if (DENSE && 16 * nb < a.nd) {   // uniform: only column blocks that hold dense columns load them
+          const int c = 16 * nb + l16;
+          const bool isd = c < a.nd;
+          const int64_t off = (int64_t)(isd ? c : 0) * a.ld_r + c0 + 32 * kb + 8 * g;
+          const uint4 dh = *reinterpret_cast<const uint4*>(rhi + off);
+          const uint4 dl = *reinterpret_cast<const uint4*>(rlo + off);
+          bh = select4(isd, dh, bh);
+          bl = select4(isd, dl, bl);
+        }
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          const int r = 16 * rb + l16;
+          const uint4 av = *reinterpret_cast<const uint4*>(&xt[r * kProjSlice + 8 * ((4 * kb + g) ^ l16)]);
+          acc[rb][nb] = mfma16x16x32(av, bh, acc[rb][nb]);
+          if (DENSE) acc[rb][nb] = mfma16x16x32(av, bl, acc[rb][nb]);
+        }
+      }
+    }
+  };
+
+  for (int uc = 0; uc < a.m; uc += 32 * wpc) {
+    const int col_end = min(a.m, uc + 32 * wpc);
+    const int s0 = uc / kProjStage;
+    const int nst = (col_end - uc + kProjStage - 1) / kProjStage;
+    uint4 ring[P][NL];
+#pragma unroll
+    for (int q = 0; q < P; ++q) gload(ring[q], s0 + q, q < nst ? col_end : 0);
+    if (a.nz > 0) {                                // generated while the first stages are in flight
       __syncthreads();
       const int nblk = wpc >> 2;
       const uint32_t wbase = (uint32_t)(uc >> 5);
@@ -69,55 +179,34 @@ __global__ __launch_bounds__(kBlock) void project_kernel(ProjectArgs a) {
       }
       __syncthreads();
     }
-    const int64_t rem = a.m - uc;
-    const int nsub = (int)min((int64_t)(wpc >> 1), (rem + 63) >> 6);
-    // U sub-chunks per batch: all their loads are issued before the first MFMA
-    constexpr int U = RB == 1 ? 8 : (RB == 2 ? 4 : 2);
-    for (int qb = wv; qb < nsub; qb += 4 * U) {
-      uint4 av[U][RB][2];
-#pragma unroll
-      for (int uu = 0; uu < U; ++uu) {
-        const int q = qb + 4 * uu;
-        const int64_t u0 = uc + 64 * (int64_t)(q < nsub ? q : qb);
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-          for (int ks = 0; ks < 2; ++ks)
-            av[uu][rb][ks] = load_bf16x8<FAST>(rowp[rb], u0 + 32 * ks + 8 * g, a.m, rowok[rb] && q < nsub, xs);
+    auto step = [&](int k, auto ph) __attribute__((always_inline)) {
+      constexpr int q = decltype(ph)::value;
+      const int st = s0 + k;
+      to_lds(ring[q]);
+      gload(ring[q], st + P, k + P < nst ? col_end : 0);
+      mult(st, uc);
+    };
+    // whole groups of P stages in the loop (no early exit reaches its back edge,
+    // so the compiler's wait counting stays exact), the remainder after it
+    int k = 0;
+    if constexpr (P == 4) {
+      for (; k + 4 <= nst; k += 4) {
+        step(k, PInt<0>{});
+        step(k + 1, PInt<1>{});
+        step(k + 2, PInt<2>{});
+        step(k + 3, PInt<3>{});
       }
-#pragma unroll
-      for (int uu = 0; uu < U; ++uu) {
-        const int q = qb + 4 * uu;
-        if (q >= nsub) break;                      // wave-uniform
-        const int64_t u0 = uc + 64 * (int64_t)q;
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-#pragma unroll
-          for (int nb = 0; nb < NB; ++nb) {
-            const int c = 16 * nb + l16;
-            // select, not branch: every lane issues the same loads
-            const int cz = c - a.nd;
-            const bool isz = cz >= 0 && cz < a.nz;
-            const uint32_t word = a.nz > 0 ? zw[(isz ? cz : 0) * (wpc + 1) + 2 * q + ks] : 0u;
-            const uint4 zb = signs_to_bf16x8((word >> (8 * g)) & 0xFFu);
-            uint4 bh = isz ? zb : uint4{0, 0, 0, 0}, bl = uint4{0, 0, 0, 0};
-            if (DENSE && 16 * nb < a.nd) {   // uniform: only column blocks that hold dense columns load them
-              const bool isd = c < a.nd;
-              const int64_t off = (int64_t)(isd ? c : 0) * a.ld_r + u0 + 32 * ks + 8 * g;
-              const uint4 dh = *reinterpret_cast<const uint4*>(rhi + off);
-              const uint4 dl = *reinterpret_cast<const uint4*>(rlo + off);
-              bh = isd ? dh : bh;
-              bl = isd ? dl : bl;
-            }
-#pragma unroll
-            for (int rb = 0; rb < RB; ++rb) {
-              acc[rb][nb] = mfma16x16x32(av[uu][rb][ks], bh, acc[rb][nb]);
-              if (DENSE) acc[rb][nb] = mfma16x16x32(av[uu][rb][ks], bl, acc[rb][nb]);
-            }
-          }
-        }
+      if (k < nst) step(k, PInt<0>{});
+      if (k + 1 < nst) step(k + 1, PInt<1>{});
+      if (k + 2 < nst) step(k + 2, PInt<2>{});
+    } else {
+      for (; k + 2 <= nst; k += 2) {
+        step(k, PInt<0>{});
+        step(k + 1, PInt<1>{});
       }
+      if (k < nst) step(k, PInt<0>{});
     }
+    __syncthreads();                               // zw and the X tiles are reused
   }
 
   // sum the four waves' partial tiles
@@ -149,10 +238,12 @@ __global__ __launch_bounds__(kBlock) void project_kernel(ProjectArgs a) {
 template <int RB, int NB>
 static hipError_t launch_rb_nb(const ProjectArgs& a, hipStream_t st) {
   const size_t zbytes = a.nz > 0 ? (size_t)a.nz * (a.words_per_chunk + 1) * 4 : 0;
-  const size_t rbytes = (size_t)4 * 16 * RB * (16 * NB + 4) * 4;
+  const size_t rbytes = std::max((size_t)4 * 16 * RB * (16 * NB + 4) * 4, (size_t)4 * 16 * RB * kProjSlice * 2);
   const size_t lds = zbytes + rbytes;
+  if (a.words_per_chunk % 16 != 0) return hipErrorInvalidValue;
   dim3 grid((unsigned)(a.T_pad / (16 * RB)), (unsigned)a.B);
-  const bool fast = a.vec && a.m % 8 == 0;
+  // buffer offsets of one workgroup's rows stay below 2^31
+  const bool fast = a.vec && a.m % 8 == 0 && (int64_t)16 * RB * a.ldx * 2 < ((int64_t)1 << 31);
   if (a.nd > 0 && fast)
     DPRC_LAUNCH((project_kernel<RB, NB, true, true>), grid, dim3(kBlock), lds, st, a);
   else if (a.nd > 0)
@@ -184,7 +275,6 @@ hipError_t launch_project(const ProjectArgs& a, int rows_per_wg, hipStream_t st)
   switch (rows_per_wg) {
     case 16: return launch_rb<1>(a, st);
     case 32: return launch_rb<2>(a, st);
-    case 64: return launch_rb<4>(a, st);
     default: return hipErrorInvalidValue;
   }
 }

@@ -56,36 +56,82 @@ __device__ __forceinline__ void store4(const TokredArgs& a, int i, int c, int j,
   }
 }
 
+template <int V>
+struct Int {
+  static constexpr int value = V;
+};
+
 template <int NB, bool FAST>
 __global__ __launch_bounds__(kBlock) void tokred_kernel(TokredArgs a) {
+  // Y stages go through LDS with X (one 16-byte load per thread per 16 columns)
+  // when they are small; wider Y is read straight from global memory at use.
+  constexpr bool YLDS = NB <= 4;
+  constexpr int YLd = kStage + 8;                       // padded LDS row of one Y column (144 bytes)
   __shared__ __attribute__((aligned(16))) uint16_t lds[2][kStage * kLdsLd];
+  __shared__ __attribute__((aligned(16))) uint16_t ylds[YLDS ? 2 : 1][YLDS ? 2 * 16 * NB * YLd : 8];
   __shared__ double dred[4];
+  constexpr int P = 4;                                  // stages in flight in registers, one more in LDS
+  static_assert(P == 4, "the stage loop below is written out for four ring slots");
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int g = lane >> 4, l16 = lane & 15, r4 = l16 >> 2, c4 = lane & 3;
   const int i = blockIdx.y;
   const int tile = blockIdx.x / a.S, s = blockIdx.x - tile * a.S;
   const int j0 = tile * kTile;
-  const int64_t tb = (int64_t)s * a.stages_per_split * kStage;
-  const int64_t te = min((int64_t)a.T, tb + (int64_t)a.stages_per_split * kStage);
-  const int nst = te > tb ? (int)((te - tb + kStage - 1) / kStage) : 0;
+  const int tb = s * a.stages_per_split * kStage;
+  const int te = min(a.T, tb + a.stages_per_split * kStage);
+  const int nst = te > tb ? (te - tb + kStage - 1) / kStage : 0;
 
   const int lr0 = tid >> 4, lc = (tid & 15) * 8;
-  const int64_t jc = (int64_t)j0 + lc;
   const uint16_t* xs = a.X + (int64_t)i * a.x_ss;
+  // FAST: one buffer resource per stage (64 token rows from column j0); rows past
+  // the split and columns past n read as zero through out-of-range offsets
+  const uint32_t row_bytes = (uint32_t)a.ldx * 2u;
+  const uint32_t lane_off = j0 + lc < a.n ? (uint32_t)lr0 * row_bytes + 2u * lc : kOobOffset;
+  const uint16_t* ys = a.Yt + (int64_t)i * a.T_pad;
+  // Y stage loads: column-half ch = tid / 8 + 32 r (h = ch / ncols16, c = ch % ncols16), tokens 8 (tid % 8) ..
+  const int ych = tid >> 3, ytk = (tid & 7) * 8;
 
-  uint4 gv[4];
-  auto gload = [&](int st) {
-    const int64_t tok0 = tb + (int64_t)st * kStage;
+  struct Stage {
+    uint4 x[4];
+    uint4 y[YLDS ? NB : 1];
+  };
+  // Stages past the split (st >= nst) are issued too, with an empty range (X) or
+  // clamped to the last stage (Y): the load sequence is the same in every stage,
+  // so the waits on the in-order load counter count exactly.
+  auto gload = [&](Stage& dst, int st) __attribute__((always_inline)) {
+    if constexpr (FAST) {
+      const int t0 = tb + st * kStage;
+      const int rows = max(0, min(kStage, te - t0));
+      const __amdgpu_buffer_rsrc_t xr =
+          buffer_rsrc(xs + (int64_t)(rows > 0 ? t0 : 0) * a.ldx + j0, (uint32_t)rows * row_bytes);
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int64_t t = tok0 + lr0 + 16 * q;
-      gv[q] = load_bf16x8<FAST>(xs + (t < te ? t : 0) * a.ldx, jc, a.n, t < te, xs);
+      for (int q = 0; q < 4; ++q) dst.x[q] = buffer_load16(xr, lane_off + (uint32_t)(16 * q) * row_bytes);
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int t = tb + st * kStage + lr0 + 16 * q;
+        const bool ok = st < nst && t < te;
+        dst.x[q] = load_bf16x8<false>(xs + (int64_t)(ok ? t : 0) * a.ldx, (int64_t)j0 + lc, a.n, ok, xs);
+      }
+    }
+    if constexpr (YLDS) {
+      const int ytok = tb + min(st, nst - 1) * kStage + ytk;
+#pragma unroll
+      for (int r = 0; r < NB; ++r) {
+        const int ch = ych + 32 * r, h = ch / (16 * NB), c = ch - h * 16 * NB;
+        dst.y[r] = *reinterpret_cast<const uint4*>(ys + ((int64_t)h * a.ncols_pad + c) * a.yt_ld + ytok);
+      }
     }
   };
-  auto swrite = [&](int buf) {
+  auto swrite = [&](const Stage& src, int buf) __attribute__((always_inline)) {
 #pragma unroll
     for (int q = 0; q < 4; ++q)
-      *reinterpret_cast<uint4*>(&lds[buf][(lr0 + 16 * q) * kLdsLd + lds_swz(lr0 + 16 * q, lc)]) = gv[q];
+      *reinterpret_cast<uint4*>(&lds[buf][(lr0 + 16 * q) * kLdsLd + lds_swz(lr0 + 16 * q, lc)]) = src.x[q];
+    if constexpr (YLDS) {
+#pragma unroll
+      for (int r = 0; r < NB; ++r)
+        *reinterpret_cast<uint4*>(&ylds[buf][(ych + 32 * r) * YLd + ytk]) = src.y[r];
+    }
   };
 
   f32x4_t acc[2][2][NB];
@@ -96,25 +142,21 @@ __global__ __launch_bounds__(kBlock) void tokred_kernel(TokredArgs a) {
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) acc[x][h][nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  if (nst > 0) {
-    gload(0);
-    swrite(0);
-  }
-  __syncthreads();
-  const uint16_t* ybase = a.Yt + (int64_t)i * a.T_pad + 8 * g;
-  for (int st = 0; st < nst; ++st) {
-    const int buf = st & 1;
-    if (st + 1 < nst) gload(st + 1);
-    const int64_t ytok = tb + (int64_t)st * kStage;
+  auto mult = [&](int buf, int st) __attribute__((always_inline)) {
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
       uint4 bop[2][NB];
 #pragma unroll
       for (int h = 0; h < 2; ++h)
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
-          bop[h][nb] = *reinterpret_cast<const uint4*>(
-              ybase + ((int64_t)h * a.ncols_pad + 16 * nb + l16) * a.yt_ld + ytok + 32 * ks);
+        for (int nb = 0; nb < NB; ++nb) {
+          if constexpr (YLDS)
+            bop[h][nb] = *reinterpret_cast<const uint4*>(
+                &ylds[buf][(h * 16 * NB + 16 * nb + l16) * YLd + 32 * ks + 8 * g]);
+          else
+            bop[h][nb] = *reinterpret_cast<const uint4*>(
+                ys + ((int64_t)h * a.ncols_pad + 16 * nb + l16) * a.yt_ld + tb + st * kStage + 32 * ks + 8 * g);
+        }
 #pragma unroll
       for (int x = 0; x < 2; ++x) {
         const int mb = 2 * wv + x;
@@ -127,8 +169,33 @@ __global__ __launch_bounds__(kBlock) void tokred_kernel(TokredArgs a) {
           for (int nb = 0; nb < NB; ++nb) acc[x][h][nb] = mfma16x16x32(av, bop[h][nb], acc[x][h][nb]);
       }
     }
-    if (st + 1 < nst) swrite(buf ^ 1);
+  };
+
+  if (nst > 0) {
+    Stage ring[P];
+#pragma unroll
+    for (int q = 0; q < P; ++q) gload(ring[q], q);
+    swrite(ring[0], 0);
     __syncthreads();
+    auto step = [&](int st, auto ph) __attribute__((always_inline)) {
+      gload(ring[ph.value], st + P);               // ring[ph] held stage st, already in LDS
+      mult(ph.value & 1, st);
+      // unconditional: after the last stage it stores an unused (empty-range) stage
+      swrite(ring[(ph.value + 1) % P], (ph.value + 1) & 1);
+      __syncthreads();
+    };
+    // whole groups of P stages in the loop (no early exit reaches its back edge, so
+    // the compiler's wait counting stays exact), the remainder after it
+    int st0 = 0;
+    for (; st0 + P <= nst; st0 += P) {
+      step(st0 + 0, Int<0>{});
+      step(st0 + 1, Int<1>{});
+      step(st0 + 2, Int<2>{});
+      step(st0 + 3, Int<3>{});
+    }
+    if (st0 + 0 < nst) step(st0 + 0, Int<0>{});
+    if (st0 + 1 < nst) step(st0 + 1, Int<1>{});
+    if (st0 + 2 < nst) step(st0 + 2, Int<2>{});
   }
 
   // W = hi part + lo part; lane holds rows j0 + 16*mb + 4*g + (0..3) of column 16*nb + l16
@@ -182,8 +249,20 @@ __global__ __launch_bounds__(kBlock) void tokred_splits_kernel(TokredArgs a) {
   for (int gi = tid; gi < a.ncols_pad * (kTile / 4); gi += kBlock) {
     const int c = gi / (kTile / 4), j4 = (gi - c * (kTile / 4)) * 4;
     float v[4] = {0.f, 0.f, 0.f, 0.f};
-    for (int s2 = 0; s2 < a.S; ++s2) {
-      const float4 pv = *reinterpret_cast<const float4*>(tp + ((int64_t)s2 * a.ncols_pad + c) * kTile + j4);
+    const float* src = tp + (int64_t)c * kTile + j4;
+    const int64_t sstride = (int64_t)a.ncols_pad * kTile;
+    int s2 = 0;
+    for (; s2 + 8 <= a.S; s2 += 8) {                 // eight loads in flight, summed in split order
+      float4 pv[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) pv[u] = *reinterpret_cast<const float4*>(src + (s2 + u) * sstride);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        v[0] += pv[u].x; v[1] += pv[u].y; v[2] += pv[u].z; v[3] += pv[u].w;
+      }
+    }
+    for (; s2 < a.S; ++s2) {
+      const float4 pv = *reinterpret_cast<const float4*>(src + s2 * sstride);
       v[0] += pv.x; v[1] += pv.y; v[2] += pv.z; v[3] += pv.w;
     }
     if (a.mode == 0) {
@@ -225,7 +304,8 @@ hipError_t launch_tokred_sample(const TokredArgs& a, hipStream_t st) {
 
 hipError_t launch_tokred(const TokredArgs& a, hipStream_t st) {
   dim3 grid((unsigned)(a.ntiles * a.S), (unsigned)a.B);
-  const bool fast = a.vec && a.n % 8 == 0;
+  // buffer offsets within one 64-row stage stay below 2^31
+  const bool fast = a.vec && a.n % 8 == 0 && (int64_t)kStage * a.ldx * 2 < ((int64_t)1 << 31);
 #define DPRC_TOKRED_CASE(NB)                                                                   \
   case NB:                                                                                     \
     if (fast) DPRC_LAUNCH((tokred_kernel<NB, true>), grid, dim3(kBlock), 0, st, a);     \
