@@ -26,20 +26,25 @@ typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16_t;
 constexpr int kGM = 256;            // tile rows (d) and columns (p)
 constexpr int kGK = 32;             // tokens per slab
 constexpr int kGLd = kGM + 32;      // LDS row: 576 bytes; the 4 rows x 2 column groups of a 32-lane transpose read hit distinct 32-byte bank groups
-constexpr int kGThreads = 512;      // 8 waves
 
 __device__ __forceinline__ f32x16_t mfma32x32x16(const uint4& a, const uint4& b, f32x16_t c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b),
                                                   c, 0, 0, 0);
 }
 
-template <bool FAST>
-__global__ __launch_bounds__(kGThreads, 1) void gemm_kernel(GemmArgs a) {
+// NW = 8: waves of 128 x 64 (2 x 4 of them); NW = 4: waves of 128 x 128 (2 x 2).
+template <int NW, bool FAST>
+__global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmArgs a) {
+  constexpr int kThreads = 64 * NW;
+  constexpr int WN = NW == 8 ? 64 : 128;             // wave tile columns
+  constexpr int YB = WN / 32;                        // 32-column MFMA blocks per wave
+  constexpr int RP = kThreads / 32;                  // slab rows per load pass
+  constexpr int RQ = kGK / RP;                       // load passes per slab
   __shared__ __attribute__((aligned(16))) uint16_t la[2][kGK * kGLd];
   __shared__ __attribute__((aligned(16))) uint16_t le[2][kGK * kGLd];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int g = lane >> 4, r4 = (lane & 15) >> 2, c4 = lane & 3;
-  const int wm = wv >> 2, wn = wv & 3;               // wave tile rows wm*128, columns wn*64
+  const int wm = wv / (kGM / WN), wn = wv % (kGM / WN);   // wave tile rows wm*128, columns wn*WN
 
   // tile of this workgroup: consecutive ids of one XCD walk the smaller dimension first
   const int tm_n = (a.d + kGM - 1) / kGM, tn_n = (a.p + kGM - 1) / kGM;
@@ -54,108 +59,119 @@ __global__ __launch_bounds__(kGThreads, 1) void gemm_kernel(GemmArgs a) {
   const int sps = a.stages_per_sample;
   const int gs_begin = split * a.stages_per_split;
   const int gs_end = min(a.B * sps, gs_begin + a.stages_per_split);
-  const int lr = tid >> 5, lc = (tid & 31) * 8;             // loads: rows lr + 16q, 8 columns at lc
+  const int lr = tid >> 5, lc = (tid & 31) * 8;             // loads: rows lr + RP q, 8 columns at lc
   const int64_t ja = (int64_t)d0 + lc, je = (int64_t)p0 + lc;
 
-  // position in the (sample, slab) list, advanced without divisions; samples with c_i = 0 are skipped
-  struct Pos {
-    int i, st, gs;
-  };
-  auto skip_zero = [&](Pos q) __attribute__((always_inline)) {
-    while (q.gs < gs_end && a.c[q.i] == 0.f) {
-      q.gs += sps - q.st;
-      q.i += 1;
-      q.st = 0;
-    }
-    return q;
-  };
-  auto advance = [&](Pos q) __attribute__((always_inline)) {
-    q.gs += 1;
-    if (++q.st == sps) {
-      q.st = 0;
-      q.i += 1;
-    }
-    return skip_zero(q);
-  };
-  uint4 ga[2], ge[2];
-  auto gload = [&](const Pos& q) __attribute__((always_inline)) {
-    const int64_t tok0 = (int64_t)q.st * kGK;
-    const uint16_t* as = a.A + (int64_t)q.i * a.a_ss;
-    const uint16_t* es = a.E + (int64_t)q.i * a.e_ss;
+  uint4 ga[2][RQ], ge[2][RQ];                     // two slabs in flight
+  // FAST: per slab one buffer resource per operand over its (up to) 32 token rows,
+  // starting at the tile's first column; rows past T and columns past d / p read
+  // as zero through out-of-range offsets, and a slab past the sample's last one has
+  // an empty range.  Element loads otherwise.
+  const uint32_t arow = (uint32_t)a.lda * 2u, erow = (uint32_t)a.lde * 2u;
+  const uint32_t aoff = d0 + lc < a.d ? (uint32_t)lr * arow + 2u * lc : kOobOffset;
+  const uint32_t eoff = p0 + lc < a.p ? (uint32_t)lr * erow + 2u * lc : kOobOffset;
+  auto gload = [&](int sl, int i, int st, int st_end) __attribute__((always_inline)) {
+    const int tok0 = st * kGK;
+    const uint16_t* as = a.A + (int64_t)i * a.a_ss;
+    const uint16_t* es = a.E + (int64_t)i * a.e_ss;
+    if constexpr (FAST) {
+      const int rows = st < st_end ? min(kGK, a.T - tok0) : 0;
+      const int64_t t0 = rows > 0 ? tok0 : 0;
+      const __amdgpu_buffer_rsrc_t ar = buffer_rsrc(as + t0 * a.lda + d0, (uint32_t)rows * arow);
+      const __amdgpu_buffer_rsrc_t er = buffer_rsrc(es + t0 * a.lde + p0, (uint32_t)rows * erow);
 #pragma unroll
-    for (int r = 0; r < 2; ++r) {
-      const int64_t t = tok0 + lr + 16 * r;
-      const bool ok = t < a.T;
-      ga[r] = load_bf16x8<FAST>(as + (ok ? t : 0) * a.lda, ja, a.d, ok, as);
-      ge[r] = load_bf16x8<FAST>(es + (ok ? t : 0) * a.lde, je, a.p, ok, es);
+      for (int r = 0; r < RQ; ++r) {
+        ga[sl][r] = buffer_load16(ar, aoff + (uint32_t)(RP * r) * arow);
+        ge[sl][r] = buffer_load16(er, eoff + (uint32_t)(RP * r) * erow);
+      }
+    } else {
+#pragma unroll
+      for (int r = 0; r < RQ; ++r) {
+        const int t = tok0 + lr + RP * r;
+        const bool ok = st < st_end && t < a.T;
+        ga[sl][r] = load8_elem(as + (int64_t)(ok ? t : 0) * a.lda, ja, a.d, ok);
+        ge[sl][r] = load8_elem(es + (int64_t)(ok ? t : 0) * a.lde, je, a.p, ok);
+      }
     }
   };
-  auto swrite = [&](int buf) __attribute__((always_inline)) {
+  auto swrite = [&](int sl, int buf) __attribute__((always_inline)) {
 #pragma unroll
-    for (int r = 0; r < 2; ++r) {
-      *reinterpret_cast<uint4*>(&la[buf][(lr + 16 * r) * kGLd + lc]) = ga[r];
-      *reinterpret_cast<uint4*>(&le[buf][(lr + 16 * r) * kGLd + lc]) = ge[r];
+    for (int r = 0; r < RQ; ++r) {
+      *reinterpret_cast<uint4*>(&la[buf][(lr + RP * r) * kGLd + lc]) = ga[sl][r];
+      *reinterpret_cast<uint4*>(&le[buf][(lr + RP * r) * kGLd + lc]) = ge[sl][r];
     }
   };
 
-  f32x16_t acc[4][2];
+  f32x16_t acc[4][YB];
 #pragma unroll
   for (int x = 0; x < 4; ++x)
 #pragma unroll
-    for (int y = 0; y < 2; ++y)
+    for (int y = 0; y < YB; ++y)
 #pragma unroll
       for (int q = 0; q < 16; ++q) acc[x][y][q] = 0.f;
 
-  Pos cur = skip_zero(Pos{gs_begin / sps, gs_begin % sps, gs_begin});
-  if (cur.gs < gs_end) {
-    gload(cur);
-    swrite(0);
-  }
-  Pos nxt = cur.gs < gs_end ? advance(cur) : cur;
-  if (nxt.gs < gs_end) gload(nxt);
-  __syncthreads();
-  int buf = 0, cur_i = -1;
-  float cur_c = 0.f;
   // the lane's transpose-read offsets: rows 8*(g/2) + r4 (+4), columns 16*(g%2) + 4*c4
   const int tr_row = 8 * (g >> 1) + r4, tr_col = 16 * (g & 1) + 4 * c4;
-  while (cur.gs < gs_end) {
-    if (cur.i != cur_i) {
-      const float ci = a.c[cur.i];
-      if (cur_i >= 0) {
-        const float ratio = cur_c / ci;
-#pragma unroll
-        for (int x = 0; x < 4; ++x)
-#pragma unroll
-          for (int y = 0; y < 2; ++y) acc[x][y] *= ratio;
-      }
-      cur_c = ci;
-      cur_i = cur.i;
-    }
+  auto slab = [&](int buf) __attribute__((always_inline)) {
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
-      uint4 av[4], bv[2];
+      uint4 av[4], bv[YB];
 #pragma unroll
       for (int x = 0; x < 4; ++x) {
         const uint16_t* pa = &la[buf][(16 * ks + tr_row) * kGLd + wm * 128 + 32 * x + tr_col];
         av[x] = make_u4(lds_read_tr16(pa), lds_read_tr16(pa + 4 * kGLd));
       }
 #pragma unroll
-      for (int y = 0; y < 2; ++y) {
-        const uint16_t* pe = &le[buf][(16 * ks + tr_row) * kGLd + wn * 64 + 32 * y + tr_col];
+      for (int y = 0; y < YB; ++y) {
+        const uint16_t* pe = &le[buf][(16 * ks + tr_row) * kGLd + wn * WN + 32 * y + tr_col];
         bv[y] = make_u4(lds_read_tr16(pe), lds_read_tr16(pe + 4 * kGLd));
       }
 #pragma unroll
       for (int x = 0; x < 4; ++x)
 #pragma unroll
-        for (int y = 0; y < 2; ++y) acc[x][y] = mfma32x32x16(av[x], bv[y], acc[x][y]);
+        for (int y = 0; y < YB; ++y) acc[x][y] = mfma32x32x16(av[x], bv[y], acc[x][y]);
     }
-    const Pos after = nxt.gs < gs_end ? advance(nxt) : nxt;
-    if (nxt.gs < gs_end) swrite(buf ^ 1);
-    if (after.gs < gs_end) gload(after);
+  };
+
+  // samples of this split in order; the accumulator is rescaled between samples
+  // (outside the slab loop), samples with c_i = 0 are skipped
+  float cur_c = 0.f;
+  bool started = false;
+  const int i_first = gs_begin / sps, i_last = gs_end > gs_begin ? (gs_end - 1) / sps : i_first - 1;
+  for (int i = i_first; i <= i_last; ++i) {
+    const float ci = a.c[i];
+    if (ci == 0.f) continue;
+    const int st_lo = max(0, gs_begin - i * sps), st_hi = min(sps, gs_end - i * sps);
+    if (started) {
+      const float ratio = cur_c / ci;
+#pragma unroll
+      for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int y = 0; y < YB; ++y) acc[x][y] *= ratio;
+    }
+    started = true;
+    cur_c = ci;
+    __syncthreads();                               // the previous sample's last slab is consumed
+    // slab k sits in LDS buffer k % 2 while it is multiplied; register slot k % 2
+    // receives slab k + 2 at the start of that step and slot (k + 1) % 2 (slab
+    // k + 1, issued a step earlier) goes to the other buffer at its end.  Slabs
+    // past the sample's last load empty ranges (zeros); steps go in pairs.
+    gload(0, i, st_lo, st_hi);
+    gload(1, i, st_lo + 1, st_hi);
+    swrite(0, 0);
     __syncthreads();
-    buf ^= 1;
-    cur = nxt;
-    nxt = after;
+    for (int st = st_lo; st < st_hi; st += 2) {
+      gload(0, i, st + 2, st_hi);
+      __builtin_amdgcn_sched_barrier(0);           // keep the loads ahead of the step's MFMAs
+      slab(0);
+      swrite(1, 1);
+      __syncthreads();
+      gload(1, i, st + 3, st_hi);
+      __builtin_amdgcn_sched_barrier(0);
+      slab(1);
+      swrite(0, 0);
+      __syncthreads();
+    }
   }
 
   // epilogue: lane holds rows 8*(q/4) + 4*(lane/32) + q%4 and column lane%32 of each 32 x 32 block
@@ -172,8 +188,8 @@ __global__ __launch_bounds__(kGThreads, 1) void gemm_kernel(GemmArgs a) {
 #pragma unroll
   for (int x = 0; x < 4; ++x)
 #pragma unroll
-    for (int y = 0; y < 2; ++y) {
-      const int col = p0 + wn * 64 + 32 * y + (lane & 31);
+    for (int y = 0; y < YB; ++y) {
+      const int col = p0 + wn * WN + 32 * y + (lane & 31);
       if (col >= a.p) continue;
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
@@ -203,10 +219,13 @@ GemmPlan gemm_plan_v2(int64_t B, int64_t T, int64_t d, int64_t p) {
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t st) {
   const int tiles = (int)(ceil_div(a.d, kGM) * ceil_div(a.p, kGM));
   dim3 grid((unsigned)tiles, (unsigned)a.S);
-  if (a.vec_a && a.vec_e && a.d % 8 == 0 && a.p % 8 == 0)
-    DPRC_LAUNCH(gemm_kernel<true>, grid, dim3(kGThreads), 0, st, a);
+  constexpr int NW = 4;
+  // buffer offsets within one 32-row slab stay below 2^31
+  if (a.vec_a && a.vec_e && a.d % 8 == 0 && a.p % 8 == 0 &&
+      (int64_t)kGK * std::max(a.lda, a.lde) * 2 < ((int64_t)1 << 31))
+    DPRC_LAUNCH((gemm_kernel<NW, true>), grid, dim3(64 * NW), 0, st, a);
   else
-    DPRC_LAUNCH(gemm_kernel<false>, grid, dim3(kGThreads), 0, st, a);
+    DPRC_LAUNCH((gemm_kernel<NW, false>), grid, dim3(64 * NW), 0, st, a);
   return hipGetLastError();
 }
 
