@@ -33,7 +33,12 @@ __device__ __forceinline__ f32x16_t mfma32x32x16(const uint4& a, const uint4& b,
 }
 
 // NW = 8: waves of 128 x 64 (2 x 4 of them); NW = 4: waves of 128 x 128 (2 x 2).
-template <int NW, bool FAST>
+template <int V>
+struct GInt {
+  static constexpr int value = V;
+};
+
+template <int NW, int NS, bool FAST>
 __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmArgs a) {
   constexpr int kThreads = 64 * NW;
   constexpr int WN = NW == 8 ? 64 : 128;             // wave tile columns
@@ -62,7 +67,7 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmArgs a) {
   const int lr = tid >> 5, lc = (tid & 31) * 8;             // loads: rows lr + RP q, 8 columns at lc
   const int64_t ja = (int64_t)d0 + lc, je = (int64_t)p0 + lc;
 
-  uint4 ga[2][RQ], ge[2][RQ];                     // two slabs in flight
+  uint4 ga[NS][RQ], ge[NS][RQ];                   // slabs in flight
   // FAST: per slab one buffer resource per operand over its (up to) 32 token rows,
   // starting at the tile's first column; rows past T and columns past d / p read
   // as zero through out-of-range offsets, and a slab past the sample's last one has
@@ -152,25 +157,49 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmArgs a) {
     started = true;
     cur_c = ci;
     __syncthreads();                               // the previous sample's last slab is consumed
-    // slab k sits in LDS buffer k % 2 while it is multiplied; register slot k % 2
-    // receives slab k + 2 at the start of that step and slot (k + 1) % 2 (slab
-    // k + 1, issued a step earlier) goes to the other buffer at its end.  Slabs
-    // past the sample's last load empty ranges (zeros); steps go in pairs.
-    gload(0, i, st_lo, st_hi);
-    gload(1, i, st_lo + 1, st_hi);
+    // slab k sits in LDS buffer k % 2 while it is multiplied; register slot k % NS
+    // receives slab k + NS at the start of that step, and slot (k + 1) % NS (slab
+    // k + 1, issued NS - 1 steps earlier) goes to the other buffer at its end.
+    // Slabs past the sample's last load empty ranges (zeros).
+#pragma unroll
+    for (int q = 0; q < NS; ++q) gload(q, i, st_lo + q, st_hi);
     swrite(0, 0);
     __syncthreads();
-    for (int st = st_lo; st < st_hi; st += 2) {
-      gload(0, i, st + 2, st_hi);
+    auto step = [&](int st, auto u) __attribute__((always_inline)) {
+      constexpr int k = decltype(u)::value;      // step index modulo 2 NS
+      gload(k % NS, i, st + NS, st_hi);
       __builtin_amdgcn_sched_barrier(0);           // keep the loads ahead of the step's MFMAs
-      slab(0);
-      swrite(1, 1);
+      slab(k % 2);
+      swrite((k + 1) % NS, (k + 1) % 2);
       __syncthreads();
-      gload(1, i, st + 3, st_hi);
-      __builtin_amdgcn_sched_barrier(0);
-      slab(1);
-      swrite(0, 0);
-      __syncthreads();
+    };
+    // whole groups of 2 NS steps in the loop (no early exit reaches its back edge,
+    // so the compiler's wait counting stays exact), the remainder after it
+    int st = st_lo;
+    for (; st + 2 * NS <= st_hi; st += 2 * NS) {
+      step(st, GInt<0>{});
+      step(st + 1, GInt<1>{});
+      step(st + 2, GInt<2>{});
+      step(st + 3, GInt<3>{});
+      if constexpr (NS > 2) {
+        step(st + 4, GInt<4>{});
+        step(st + 5, GInt<5>{});
+      }
+      if constexpr (NS > 3) {
+        step(st + 6, GInt<6>{});
+        step(st + 7, GInt<7>{});
+      }
+    }
+    if (st < st_hi) step(st, GInt<0>{});
+    if (st + 1 < st_hi) step(st + 1, GInt<1>{});
+    if (st + 2 < st_hi) step(st + 2, GInt<2>{});
+    if constexpr (NS > 2) {
+      if (st + 3 < st_hi) step(st + 3, GInt<3>{});
+      if (st + 4 < st_hi) step(st + 4, GInt<4>{});
+    }
+    if constexpr (NS > 3) {
+      if (st + 5 < st_hi) step(st + 5, GInt<5>{});
+      if (st + 6 < st_hi) step(st + 6, GInt<6>{});
     }
   }
 
@@ -219,13 +248,13 @@ GemmPlan gemm_plan_v2(int64_t B, int64_t T, int64_t d, int64_t p) {
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t st) {
   const int tiles = (int)(ceil_div(a.d, kGM) * ceil_div(a.p, kGM));
   dim3 grid((unsigned)tiles, (unsigned)a.S);
-  constexpr int NW = 4;
+  constexpr int NW = 4, NS = 2;
   // buffer offsets within one 32-row slab stay below 2^31
   if (a.vec_a && a.vec_e && a.d % 8 == 0 && a.p % 8 == 0 &&
       (int64_t)kGK * std::max(a.lda, a.lde) * 2 < ((int64_t)1 << 31))
-    DPRC_LAUNCH((gemm_kernel<NW, true>), grid, dim3(64 * NW), 0, st, a);
+    DPRC_LAUNCH((gemm_kernel<NW, NS, true>), grid, dim3(64 * NW), 0, st, a);
   else
-    DPRC_LAUNCH((gemm_kernel<NW, false>), grid, dim3(64 * NW), 0, st, a);
+    DPRC_LAUNCH((gemm_kernel<NW, NS, false>), grid, dim3(64 * NW), 0, st, a);
   return hipGetLastError();
 }
 
