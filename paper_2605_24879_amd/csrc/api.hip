@@ -101,8 +101,10 @@ int pad_cols(int ncols) {
 
 int rows_per_wg(int64_t rows, int ncols_pad) {
   const int nb = ncols_pad / 16;
+  // 32-row workgroups while that still gives 256 or more of them (fixed per-workgroup
+  // costs such as the probe generation are spread over twice the data)
   int rb = 1;
-  if (rows >= 32 * 1024) rb = 2;
+  if (rows >= 8 * 1024) rb = 2;
   while (rb > 1 && rb * nb > 8) rb >>= 1;
   return 16 * rb;
 }
@@ -124,7 +126,7 @@ TokPlan tok_plan(int64_t B, int64_t T, int64_t n) {
   p.ntiles = (int32_t)ceil_div(n, kTile);
   const int64_t stages = p.T_pad / kStage;
   const int64_t base = B * p.ntiles;
-  int64_t S = std::max<int64_t>(1, ceil_div(512, base));
+  int64_t S = std::max<int64_t>(1, ceil_div(256, base));
   S = std::min<int64_t>(S, std::max<int64_t>(1, stages / 4));  // >= 4 stages (256 tokens) per split
   p.sps = (int32_t)ceil_div(stages, S);
   p.S = (int32_t)ceil_div(stages, p.sps);
