@@ -108,7 +108,9 @@ dprc_status dprc_norm_hutch(const dprc_layer* layers, int32_t num_layers, int32_
  * QR), U = M_i Q, V = M_i P - U (Q^T P) with r residual probes P (stream 0),
  * estimate ||U||_F^2 + ||V||_F^2 / r.  s in [0, 32], r in [1, 256],
  * s + r <= 256, s <= the sketched dimension.  s = 0 gives Hutchinson with r
- * probes.  Outputs as for dprc_norm_hutch. */
+ * probes.  A sketched dimension above 2^21 rows returns DPRC_ERROR_NOT_SUPPORTED
+ * (the QR tree of 128-row blocks is at most eight levels deep).  Outputs as for
+ * dprc_norm_hutch. */
 size_t dprc_norm_hutchpp_workspace(const dprc_layer* layers, int32_t num_layers, int32_t s,
                                    int32_t r, dprc_side side);
 dprc_status dprc_norm_hutchpp(const dprc_layer* layers, int32_t num_layers, int32_t s, int32_t r,
@@ -160,7 +162,7 @@ dprc_status dprc_probe_bits(dprc_probe probe, uint64_t seed, uint32_t layer_id,
 typedef enum {
   DPRC_KERNEL_PROJECT = 1,            /* Y = X Z (bf16 matrix cores)          */
   DPRC_KERNEL_TOKEN_REDUCE = 2,       /* X'^T Y, estimate or store            */
-  DPRC_KERNEL_QR = 3,                 /* Hutch++ Householder QR               */
+  DPRC_KERNEL_QR = 3,                 /* Hutch++ QR of 128-row blocks of O S  */
   DPRC_KERNEL_HUTCHPP_FINAL = 4,      /* Hutch++ V = W_P - U Q^T P, estimate  */
   DPRC_KERNEL_CLIP_SCALE = 5,
   DPRC_KERNEL_ACCUMULATE = 6,         /* clipped accumulation GEMM            */
@@ -173,8 +175,8 @@ typedef enum {
   DPRC_KERNEL_ACCUMULATE_F32 = 13,
   DPRC_KERNEL_TOKEN_SPLITS = 14,      /* sum of token splits per tile          */
   DPRC_KERNEL_SAMPLE_SUM = 15,        /* per-sample sum of tile squares         */
-  DPRC_KERNEL_QR_COMBINE = 16,        /* QR of the stacked block R factors      */
-  DPRC_KERNEL_QR_EXPAND = 17,         /* rows of Q, and Q^T P per row block     */
+  DPRC_KERNEL_QR_COMBINE = 16,        /* QR of stacked block R factors (upper tree levels) */
+  DPRC_KERNEL_QR_EXPAND = 17,         /* rows of Q per tree level; Q^T P at the first */
   DPRC_KERNEL_HUTCHPP_SUM = 18        /* per-sample Hutch++ estimate            */
 } dprc_kernel_kind;
 dprc_status dprc_trace_launches(hipEvent_t* events, int32_t* kinds, int32_t capacity,

@@ -311,13 +311,19 @@ size_t hutchpp_layout(const View& v, int32_t s, int32_t r, void* ws, PPBufs* out
     b.OS = ar.take<float>((size_t)B * s * v.m);
     b.Q = ar.take<float>((size_t)B * s * v.m);
     b.UW = ar.take<float>((size_t)B * (s + r) * v.n);
-    const QrPlan qp = qr_plan(v.m, s);
-    b.qr.B = (int32_t)B; b.qr.m = (int32_t)v.m; b.qr.s = s; b.qr.r = r; b.qr.R = qp.R; b.qr.nblk = qp.nblk;
-    b.qr.V = ar.take<double>((size_t)B * qp.nblk * s * qp.R);
-    b.qr.tau = ar.take<double>((size_t)B * qp.nblk * s);
-    b.qr.Rst = ar.take<double>((size_t)B * s * qp.nblk * s);
-    b.qr.Q2 = ar.take<double>((size_t)B * s * qp.nblk * s);
-    b.qr.Cpart = ar.take<double>((size_t)B * qp.nblk * s * r);
+    int32_t rows[kQrMaxLevels], nblk[kQrMaxLevels];
+    int64_t dbl = 0;
+    const int32_t nlev = qr_levels(v.m, s, rows, nblk, &dbl);
+    b.qr.B = (int32_t)B; b.qr.m = (int32_t)v.m; b.qr.s = s; b.qr.r = r; b.qr.nlev = nlev;
+    for (int l = 0; l < nlev; ++l) {
+      QrLevel& L = b.qr.lev[l];
+      L.rows = rows[l]; L.nblk = nblk[l];
+      L.V = ar.take<double>((size_t)B * nblk[l] * s * kQrRows);
+      L.tau = ar.take<double>((size_t)B * nblk[l] * s);
+      L.M = l > 0 ? ar.take<double>((size_t)B * s * rows[l]) : nullptr;
+      L.Q = l > 0 ? ar.take<double>((size_t)B * s * rows[l]) : nullptr;
+    }
+    b.qr.Cpart = ar.take<double>((size_t)B * (nlev > 0 ? nblk[0] : 1) * s * r);
     b.fin.nchunk = final_chunks(v.n);
     b.fin.Fpart = ar.take<double>((size_t)B * b.fin.nchunk * 2);
   }
@@ -336,7 +342,8 @@ size_t hutchpp_layout(const View& v, int32_t s, int32_t r, void* ws, PPBufs* out
   return ar.off;
 }
 
-// Q = orth(O S) (three TSQR launches), with C = Q^T P formed alongside.
+// Q = orth(O S) (a TSQR tree: factor launches up, expansion launches down), with C = Q^T P
+// formed alongside by the last expansion.
 dprc_status run_qr(PPBufs& b, const View& v, uint32_t k0, uint32_t k1, bool bf16_out, hipStream_t st) {
   QrArgs& q = b.qr;
   q.OS = b.OS; q.os_ld = v.m; q.os_ss = (int64_t)q.s * v.m;
@@ -344,9 +351,15 @@ dprc_status run_qr(PPBufs& b, const View& v, uint32_t k0, uint32_t k1, bool bf16
   q.Q = b.Q; q.q_ld = v.m; q.q_ss = (int64_t)q.s * v.m;
   q.Qhi = bf16_out ? b.Qhi : nullptr; q.Qlo = bf16_out ? b.Qlo : nullptr;
   q.qh_ld = bf16_out ? b.ld_q : 0; q.qh_ss = (int64_t)q.s * q.qh_ld;
-  if (traced(DPRC_KERNEL_QR, st, [&] { return launch_qr_blocks(q, st); }) != hipSuccess) return DPRC_ERROR_HIP;
-  if (traced(DPRC_KERNEL_QR_COMBINE, st, [&] { return launch_qr_combine(q, st); }) != hipSuccess) return DPRC_ERROR_HIP;
-  return hip_status(traced(DPRC_KERNEL_QR_EXPAND, st, [&] { return launch_qr_expand(q, st); }));
+  if (q.nlev < 1) return DPRC_ERROR_NOT_SUPPORTED;
+  for (int l = 0; l < q.nlev; ++l)
+    if (traced(l == 0 ? DPRC_KERNEL_QR : DPRC_KERNEL_QR_COMBINE, st,
+               [&] { return launch_qr_factor(q, l, st); }) != hipSuccess)
+      return DPRC_ERROR_HIP;
+  for (int l = q.nlev - 1; l >= 0; --l)
+    if (traced(DPRC_KERNEL_QR_EXPAND, st, [&] { return launch_qr_expand(q, l, st); }) != hipSuccess)
+      return DPRC_ERROR_HIP;
+  return DPRC_SUCCESS;
 }
 
 dprc_status hutchpp_layer(const View& v, int32_t s, int32_t r, uint32_t k0, uint32_t k1, float* n2,
@@ -417,7 +430,7 @@ dprc_status hutchpp_layer(const View& v, int32_t s, int32_t r, uint32_t k0, uint
   }
   FinalArgs fa = b.fin;
   fa.UW = b.UW; fa.uw_ld = v.n; fa.uw_ss = (int64_t)(s + r) * v.n;
-  fa.B = (int32_t)B; fa.n = (int32_t)v.n; fa.s = s; fa.r = r; fa.nblk = b.qr.nblk;
+  fa.B = (int32_t)B; fa.n = (int32_t)v.n; fa.s = s; fa.r = r; fa.nblk = b.qr.nlev > 0 ? b.qr.lev[0].nblk : 0;
   fa.Cpart = b.qr.Cpart; fa.n2 = n2; fa.n2_layer = n2_layer; fa.accumulate = accumulate;
   if ((e = traced(DPRC_KERNEL_HUTCHPP_FINAL, st, [&] { return launch_hpp_rows(fa, st); })) != hipSuccess)
     return DPRC_ERROR_HIP;
@@ -505,8 +518,12 @@ dprc_status dprc_norm_hutchpp(const dprc_layer* layers, int32_t num_layers, int3
   dprc_status st = check_layers(layers, num_layers, side);
   if (st != DPRC_SUCCESS) return st;
   if (s < 0 || s > 32 || r < 1 || r > 256 || s + r > 256 || !n2) return DPRC_ERROR_INVALID_VALUE;
-  for (int32_t l = 0; l < num_layers; ++l)
-    if (s > view_of(layers[l], side).m) return DPRC_ERROR_INVALID_VALUE;
+  for (int32_t l = 0; l < num_layers; ++l) {
+    const View v = view_of(layers[l], side);
+    if (s > v.m) return DPRC_ERROR_INVALID_VALUE;
+    int32_t rows[kQrMaxLevels], nblk[kQrMaxLevels];
+    if (s > 0 && qr_levels(v.m, s, rows, nblk, nullptr) == 0) return DPRC_ERROR_NOT_SUPPORTED;
+  }
   const size_t need = dprc_norm_hutchpp_workspace(layers, num_layers, s, r, side);
   if (ws_bytes < need) return DPRC_ERROR_WORKSPACE_TOO_SMALL;
   if (!ws || !aligned(ws, kAlign)) return DPRC_ERROR_INVALID_VALUE;

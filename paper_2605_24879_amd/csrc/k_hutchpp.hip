@@ -1,12 +1,16 @@
 // Hutch++ pieces that are not token streams (Algorithm 2, Hutch++ branch):
 //
 //  * Q = orthonormal basis of the sketch O S (m x s per sample) by a tall-skinny
-//    Householder QR (TSQR): each workgroup factors a block of rows in LDS, one
-//    workgroup per sample factors the stacked s x s R factors, and each block
-//    workgroup then expands its rows of Q = Q_block * Q_stack.  Householder
-//    keeps Q orthonormal when O S is rank deficient (a Gram/Cholesky QR breaks
-//    down there), and the blocks make the work parallel over rows.  All in fp64.
-//  * While it holds its rows of Q, a block workgroup also forms its share of
+//    Householder QR as a tree: one wavefront factors a block of 128 rows held in
+//    registers (two rows per lane, fp64), the s x s R factors of the blocks are
+//    stacked and factored the same way at the next level, until one block is
+//    left.  The expansion runs back down the tree: each block starts from its s
+//    rows of the level above's Q (the identity at the top) and applies its own
+//    reflectors.  Householder keeps Q orthonormal when O S is rank deficient (a
+//    Gram/Cholesky QR breaks down there).  Dot products over a block's rows are
+//    summed across the wave through LDS in a fixed order, so the result does not
+//    depend on scheduling.
+//  * While it holds its rows of Q, a level-1 block also forms its share of
 //    C = Q^T P (P the residual probes, regenerated from Philox).
 //  * The finalize step V = W_P - U C and the sums ||U||^2, ||V||^2 run
 //    row-parallel; a last kernel adds the row chunks in a fixed order:
@@ -17,8 +21,8 @@
 
 namespace dprc {
 
-constexpr int kQrThreads = 256;
-constexpr int kQrGroup = 16;  // columns whose dot products are reduced together
+constexpr int kQrThreads = 256;   // finalize kernels
+constexpr int kRedLd = 65;        // padded row of the per-column lane sums
 
 __device__ __forceinline__ double qr_block_sum(double v, double* sh) {
   const int tid = threadIdx.x;
@@ -29,253 +33,275 @@ __device__ __forceinline__ double qr_block_sum(double v, double* sh) {
   return (sh[0] + sh[1]) + (sh[2] + sh[3]);
 }
 
-// Sum over the workgroup of v[0..kQrGroup) (entries >= cnt are zero); every
-// thread gets the sums.  A reduce-scatter inside the wave halves the vector at
-// each of the exchanges over lane bits 5, 4, 3, 2 (8 + 4 + 2 + 1 shuffles), so
-// lane l ends with column (l >> 2) & 15 summed over 16 lanes; two more
-// exchanges finish the wave, and the four waves are added in a fixed order.
-__device__ __forceinline__ void qr_block_sum_vec(double* v, int cnt, double* sh /*[4][kQrGroup]*/, double* out) {
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-#pragma unroll
-  for (int st = 0, o = 32, n = kQrGroup; st < 4; ++st, o >>= 1, n >>= 1) {
-    const bool up = (lane & o) != 0;
-    const int half = n >> 1;
-#pragma unroll
-    for (int j = 0; j < kQrGroup / 2; ++j) {
-      if (j < half) {
-        const double send = up ? v[j] : v[j + half];
-        const double keep = up ? v[j + half] : v[j];
-        v[j] = keep + __shfl_xor(send, o, 64);
-      }
-    }
-  }
-  double x = v[0];
-  x += __shfl_xor(x, 2, 64);
-  x += __shfl_xor(x, 1, 64);
-  __syncthreads();
-  if ((lane & 3) == 0) sh[wv * kQrGroup + ((lane >> 2) & 15)] = x;
-  __syncthreads();
-#pragma unroll
-  for (int q = 0; q < kQrGroup; ++q)
-    out[q] = q < cnt ? (sh[q] + sh[kQrGroup + q]) + (sh[2 * kQrGroup + q] + sh[3 * kQrGroup + q]) : 0.0;
+// Orders a wave's LDS accesses around a hand-off between its lanes (LDS
+// operations of one wave execute in issue order; this keeps the compiler from
+// moving them across).
+__device__ __forceinline__ void qr_wave_fence() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// In-place Householder QR of A (rows x s, column-major, leading dimension ld;
-// LDS or global).  Afterwards column k holds v_k in rows k..rows-1 (v_k[k] =
-// x_k - alpha_k), tau[k] = 2 / |v_k|^2 (0: identity reflector for a zero
-// column), alpha[k] = R_kk, and rows 0..k-1 of column k hold R.
-__device__ __forceinline__ void householder_qr(double* A, int ld, int rows, int s, double* tau, double* alpha, double* sh) {
-  const int tid = threadIdx.x;
-  double part[kQrGroup], tot[kQrGroup];
+__device__ __forceinline__ double readlane_f64(double v, int l) {
+  const uint64_t u = (uint64_t)__double_as_longlong(v);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, l);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), l);
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+// v[c] <- sum over the 64 lanes of v[c], for c >= c_lo (c_lo a constant after
+// unrolling).  Lane sums go to LDS column by column; lane (c, g) adds the g-th
+// run of SP of them, and shuffles over the run bits finish the sum.
+template <int SP>
+__device__ __forceinline__ void wave_vec_sum(double (&v)[SP], int c_lo, double* red, double* tot) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int c = 0; c < SP; ++c)
+    if (c >= c_lo) red[c * kRedLd + lane] = v[c];
+  qr_wave_fence();
+  const int c = lane % SP, g = lane / SP;
+  double x = 0.0;
+  if (c >= c_lo) {
+#pragma unroll
+    for (int q = 0; q < SP; ++q) x += red[c * kRedLd + g * SP + q];
+  }
+#pragma unroll
+  for (int e = 0; e < 6; ++e)
+    if ((SP << e) < 64) x += __shfl_xor(x, SP << e, 64);
+  if (g == 0) tot[c] = x;
+  qr_wave_fence();
+#pragma unroll
+  for (int q = 0; q < SP; ++q)
+    if (q >= c_lo) v[q] = tot[q];
+  qr_wave_fence();
+}
+
+// ---- factor one 128-row block of a level ----------------------------------------------------------
+// Lane l holds rows l and l + 64 of the block.  Step k works on column k, held in
+// register column 0: the columns not yet factored shift down one place after each
+// step, so every register index is a constant.  v_k = x_k - alpha_k e_k over rows
+// >= k, tau_k = 2 / |v_k|^2 (0: identity reflector for a zero column), alpha_k =
+// R_kk; the dot products v_k . A_c come from one pass with the norm: x_k . A_c -
+// alpha_k A_kc.  v_k, tau_k and row k of R are written out as each step ends.
+template <int SP>
+__global__ __launch_bounds__(64) void qr_factor_kernel(QrArgs a, int level) {
+  __shared__ double red[SP * kRedLd];
+  __shared__ double tot[SP];
+  const int b = blockIdx.x, i = blockIdx.y, lane = threadIdx.x;
+  const int s = a.s;
+  const QrLevel L = a.lev[level];
+  double A[2][SP];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int row = b * kQrRows + lane + 64 * u;
+#pragma unroll
+    for (int c = 0; c < SP; ++c) {
+      double x = 0.0;
+      if (c < s && row < L.rows)
+        x = level == 0 ? (double)a.OS[(int64_t)i * a.os_ss + (int64_t)c * a.os_ld + row]
+                       : L.M[((int64_t)i * s + c) * L.rows + row];
+      A[u][c] = x;
+    }
+  }
+  double* V = L.V + ((int64_t)i * L.nblk + b) * s * kQrRows;
+  double* tb = L.tau + ((int64_t)i * L.nblk + b) * s;
+  const bool has_next = level + 1 < a.nlev;
+  const QrLevel N = a.lev[has_next ? level + 1 : level];
   for (int k = 0; k < s; ++k) {
-    double* x = A + (int64_t)k * ld;
-    double p = 0.0;
-    for (int j = k + tid; j < rows; j += kQrThreads) p += x[j] * x[j];
-    const double nrm2 = qr_block_sum(p, sh);
-    const double x0 = k < rows ? x[k] : 0.0;
-    __syncthreads();
-    if (!(nrm2 > 0.0)) {
-      if (tid == 0) { tau[k] = 0.0; alpha[k] = 0.0; }
-      __syncthreads();
-      continue;
+    double pv[SP];
+#pragma unroll
+    for (int c = 0; c < SP; ++c) pv[c] = 0.0;
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const double xk = lane + 64 * u >= k ? A[u][0] : 0.0;
+#pragma unroll
+      for (int c = 0; c < SP; ++c) pv[c] += xk * A[u][c];
     }
-    const double al = -copysign(sqrt(nrm2), x0);
-    const double v0 = x0 - al;
-    const double vn2 = nrm2 - x0 * x0 + v0 * v0;
-    const double t = vn2 > 0.0 ? 2.0 / vn2 : 0.0;
-    if (tid == 0) { tau[k] = t; alpha[k] = al; x[k] = v0; }
-    __syncthreads();
-    for (int c0 = k + 1; c0 < s; c0 += kQrGroup) {
-      const int cnt = min(kQrGroup, s - c0);
-      for (int q = 0; q < kQrGroup; ++q) part[q] = 0.0;
-      for (int j = k + tid; j < rows; j += kQrThreads) {
-        const double vj = x[j];
+    wave_vec_sum<SP>(pv, 0, red, tot);
+    const double nrm2 = pv[0];
+    double t = 0.0, al = 0.0;
+    if (nrm2 > 0.0) {                               // uniform; a zero column keeps the identity reflector
+      const double x0 = readlane_f64(A[0][0], k);  // row k < 32 sits in lane k
+      al = -copysign(sqrt(nrm2), x0);
+      const double v0 = x0 - al;
+      const double vn2 = nrm2 - x0 * x0 + v0 * v0;
+      t = vn2 > 0.0 ? 2.0 / vn2 : 0.0;
+      double d[SP];
 #pragma unroll
-        for (int q = 0; q < kQrGroup; ++q)
-          if (q < cnt) part[q] += vj * A[(int64_t)(c0 + q) * ld + j];
-      }
-      qr_block_sum_vec(part, cnt, sh, tot);
-      for (int j = k + tid; j < rows; j += kQrThreads) {
-        const double vj = x[j];
+      for (int c = 1; c < SP; ++c) d[c] = pv[c] - al * readlane_f64(A[0][c], k);
 #pragma unroll
-        for (int q = 0; q < kQrGroup; ++q)
-          if (q < cnt) A[(int64_t)(c0 + q) * ld + j] -= t * tot[q] * vj;
+      for (int u = 0; u < 2; ++u) {
+        const int j = lane + 64 * u;
+        if (j >= k) {
+          const double vj = j == k ? v0 : A[u][0];
+#pragma unroll
+          for (int c = 1; c < SP; ++c) A[u][c] -= t * vj * d[c];
+          A[u][0] = vj;
+        }
       }
-      __syncthreads();
+    }
+    // v_k (zero above the diagonal; for a zero column the column itself, which is zero)
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int j = lane + 64 * u;
+      V[(int64_t)k * kQrRows + j] = j >= k ? A[u][0] : 0.0;
+    }
+    if (lane == 0) tb[k] = t;
+    // row k of R into row b*s + k of the next level's input: R_kk = alpha_k, R_kc (c > k)
+    if (has_next && lane == k) {
+      double* nm = N.M + (int64_t)i * s * N.rows + (int64_t)b * s + k;
+      nm[(int64_t)k * N.rows] = al;
+#pragma unroll
+      for (int c = 1; c < SP; ++c)
+        if (k + c < s) nm[(int64_t)(k + c) * N.rows] = A[0][c];
+      for (int c = 0; c < k; ++c) nm[(int64_t)c * N.rows] = 0.0;
+    }
+    // the remaining columns move down one register column
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+#pragma unroll
+      for (int c = 0; c + 1 < SP; ++c) A[u][c] = A[u][c + 1];
+      A[u][SP - 1] = 0.0;
     }
   }
 }
 
-// W <- H_0 H_1 ... H_{s-1} W for W (rows x s, column-major, ld_w), reflectors from householder_qr.
-__device__ __forceinline__ void apply_reflectors(const double* V, int ldv, const double* tau, int rows, int s, double* W,
-                                 int ldw, double* sh) {
-  const int tid = threadIdx.x;
-  double part[kQrGroup], tot[kQrGroup];
+// ---- expand one block: W = H_0 ... H_{s-1} [Q_up rows; 0]; level 0 writes Q and C_b = Q_b^T P_b ----
+template <int SP>
+__global__ __launch_bounds__(64) void qr_expand_kernel(QrArgs a, int level) {
+  __shared__ double red[SP * kRedLd];
+  __shared__ double tot[SP];
+  __shared__ double qs[SP * (kQrRows + 1)];
+  __shared__ uint32_t zw[256 * 4];
+  const int b = blockIdx.x, i = blockIdx.y, lane = threadIdx.x;
+  const int s = a.s;
+  const QrLevel L = a.lev[level];
+  const bool top = level + 1 == a.nlev;
+  const QrLevel U = a.lev[top ? level : level + 1];
+  double W[2][SP];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int j = lane + 64 * u;
+#pragma unroll
+    for (int c = 0; c < SP; ++c) {
+      double w = 0.0;
+      if (c < s && j < s) w = top ? (j == c ? 1.0 : 0.0) : U.Q[((int64_t)i * s + c) * U.rows + (int64_t)b * s + j];
+      W[u][c] = w;
+    }
+  }
+  const double* Vb = L.V + ((int64_t)i * L.nblk + b) * s * kQrRows;
+  const double* tb = L.tau + ((int64_t)i * L.nblk + b) * s;
   for (int k = s - 1; k >= 0; --k) {
-    const double t = tau[k];
-    if (t == 0.0) continue;
-    const double* v = V + (int64_t)k * ldv;
-    for (int c0 = 0; c0 < s; c0 += kQrGroup) {
-      const int cnt = min(kQrGroup, s - c0);
-      for (int q = 0; q < kQrGroup; ++q) part[q] = 0.0;
-      for (int j = k + tid; j < rows; j += kQrThreads) {
-        const double vj = v[j];
+    const double t = tb[k];
+    if (t == 0.0) continue;                       // uniform
+    const double v0 = Vb[(int64_t)k * kQrRows + lane], v1 = Vb[(int64_t)k * kQrRows + lane + 64];
+    double pv[SP];
 #pragma unroll
-        for (int q = 0; q < kQrGroup; ++q)
-          if (q < cnt) part[q] += vj * W[(int64_t)(c0 + q) * ldw + j];
-      }
-      qr_block_sum_vec(part, cnt, sh, tot);
-      for (int j = k + tid; j < rows; j += kQrThreads) {
-        const double vj = v[j];
+    for (int c = 0; c < SP; ++c) pv[c] = v0 * W[0][c] + v1 * W[1][c];
+    wave_vec_sum<SP>(pv, 0, red, tot);
 #pragma unroll
-        for (int q = 0; q < kQrGroup; ++q)
-          if (q < cnt) W[(int64_t)(c0 + q) * ldw + j] -= t * tot[q] * vj;
-      }
-      __syncthreads();
+    for (int c = 0; c < SP; ++c) {
+      W[0][c] -= t * v0 * pv[c];
+      W[1][c] -= t * v1 * pv[c];
     }
   }
-}
-
-// ---- level 1: Householder QR of each block of R rows ---------------------------------------------
-__global__ __launch_bounds__(kQrThreads) void qr_blocks_kernel(QrArgs a) {
-  extern __shared__ __attribute__((aligned(16))) double lds[];
-  __shared__ double sh[4 * kQrGroup];
-  __shared__ double tau[64], alpha[64];
-  const int b = blockIdx.x, i = blockIdx.y, tid = threadIdx.x;
-  const int R = a.R, s = a.s;
-  const int64_t row0 = (int64_t)b * R;
-  const float* os = a.OS + (int64_t)i * a.os_ss;
-  for (int c = 0; c < s; ++c)
-    for (int j = tid; j < R; j += kQrThreads)
-      lds[c * R + j] = row0 + j < a.m ? (double)os[(int64_t)c * a.os_ld + row0 + j] : 0.0;
-  __syncthreads();
-  householder_qr(lds, R, R, s, tau, alpha, sh);
-  __syncthreads();
-  double* V = a.V + ((int64_t)i * a.nblk + b) * s * R;
-  for (int e = tid; e < s * R; e += kQrThreads) V[e] = lds[e];
-  double* tb = a.tau + ((int64_t)i * a.nblk + b) * s;
-  if (tid < s) tb[tid] = tau[tid];
-  // R_b into the stacked matrix: column c, rows b*s .. b*s+s-1
-  const int ldst = a.nblk * s;
-  double* st = a.Rst + (int64_t)i * s * ldst;
-  for (int e = tid; e < s * s; e += kQrThreads) {
-    const int c = e / s, r = e - c * s;
-    st[(int64_t)c * ldst + b * s + r] = r < c ? lds[c * R + r] : (r == c ? alpha[c] : 0.0);
+  if (level > 0) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int row = b * kQrRows + lane + 64 * u;
+      if (row < L.rows) {
+#pragma unroll
+        for (int c = 0; c < SP; ++c)
+          if (c < s) L.Q[((int64_t)i * s + c) * L.rows + row] = W[u][c];
+      }
+    }
+    return;
   }
-}
-
-// ---- level 2: QR of the stacked R factors and its explicit Q (one workgroup per sample) ---------
-__global__ __launch_bounds__(kQrThreads) void qr_combine_kernel(QrArgs a, int in_lds) {
-  extern __shared__ __attribute__((aligned(16))) double lds[];
-  __shared__ double sh[4 * kQrGroup];
-  __shared__ double tau[64], alpha[64];
-  const int i = blockIdx.x, tid = threadIdx.x, s = a.s;
-  const int rows = a.nblk * s;
-  double* stg = a.Rst + (int64_t)i * s * rows;
-  double* q2g = a.Q2 + (int64_t)i * s * rows;
-  double* st = in_lds ? lds : stg;                  // LDS copies when both s x rows matrices fit
-  double* q2 = in_lds ? lds + s * rows : q2g;
-  if (in_lds) {
-    for (int e = tid; e < s * rows; e += kQrThreads) st[e] = stg[e];
-    __syncthreads();
-  }
-  householder_qr(st, rows, rows, s, tau, alpha, sh);
-  for (int c = 0; c < s; ++c)
-    for (int j = tid; j < rows; j += kQrThreads) q2[(int64_t)c * rows + j] = (j == c) ? 1.0 : 0.0;
-  __syncthreads();
-  apply_reflectors(st, rows, tau, rows, s, q2, rows, sh);
-  if (in_lds) {
-    __syncthreads();
-    for (int e = tid; e < s * rows; e += kQrThreads) q2g[e] = q2[e];
-  }
-}
-
-// ---- level 3: rows of Q = Q_block [Q2_b; 0], and the block's share of C = Q^T P -------------------
-__global__ __launch_bounds__(kQrThreads) void qr_expand_kernel(QrArgs a) {
-  extern __shared__ __attribute__((aligned(16))) double lds[];
-  __shared__ double sh[4 * kQrGroup];
-  __shared__ double tau[64];
-  const int b = blockIdx.x, i = blockIdx.y, tid = threadIdx.x;
-  const int R = a.R, s = a.s, rows2 = a.nblk * s;
-  double* W = lds;                                           // [s][R]
-  uint32_t* zw = reinterpret_cast<uint32_t*>(W + s * R);     // [r][R/32] probe words of this block
-  const double* V = a.V + ((int64_t)i * a.nblk + b) * s * R; // reflectors (read-only, global)
-  if (tid < s) tau[tid] = a.tau[((int64_t)i * a.nblk + b) * s + tid];
-  const double* q2 = a.Q2 + (int64_t)i * s * rows2;
-  for (int e = tid; e < s * R; e += kQrThreads) {
-    const int c = e / R, j = e - c * R;
-    W[e] = j < s ? q2[(int64_t)c * rows2 + b * s + j] : 0.0;
-  }
-  // probe words for rows b*R .. b*R+R-1 (R is a multiple of 128)
-  const int wpb = R / 32;
-  for (int e = tid; e < a.r * (wpb / 4); e += kQrThreads) {
-    const int c = e / (wpb / 4), blk = e - c * (wpb / 4);
-    const u32x4 v = rademacher_block(a.key0, a.key1, a.layer, kStreamProbe, (uint32_t)(b * (R / 128) + blk),
-                                     (uint32_t)c);
-    uint32_t* d = zw + c * wpb + 4 * blk;
-    d[0] = v.x; d[1] = v.y; d[2] = v.z; d[3] = v.w;
-  }
-  __syncthreads();
-  apply_reflectors(V, R, tau, R, s, W, R, sh);
-  __syncthreads();
-  const int64_t row0 = (int64_t)b * R;
-  for (int c = 0; c < s; ++c) {
-    for (int j = tid; j < R; j += kQrThreads) {
-      const int64_t row = row0 + j;
-      const double q = row < a.m ? W[c * R + j] : 0.0;
-      if (a.Q && row < a.m) a.Q[(int64_t)i * a.q_ss + (int64_t)c * a.q_ld + row] = (float)q;
-      if (a.Qhi && row < a.qh_ld) {
-        uint32_t h, l;
-        split_bf16((float)q, h, l);
-        a.Qhi[(int64_t)i * a.qh_ss + (int64_t)c * a.qh_ld + row] = (uint16_t)h;
-        a.Qlo[(int64_t)i * a.qh_ss + (int64_t)c * a.qh_ld + row] = (uint16_t)l;
+  // level 0: rows of Q (rows >= m are zero: their reflector entries are zero)
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int64_t row = (int64_t)b * kQrRows + lane + 64 * u;
+#pragma unroll
+    for (int c = 0; c < SP; ++c) {
+      if (c < s) {
+        const double q = row < a.m ? W[u][c] : 0.0;
+        qs[c * (kQrRows + 1) + lane + 64 * u] = q;
+        if (a.Q && row < a.m) a.Q[(int64_t)i * a.q_ss + (int64_t)c * a.q_ld + row] = (float)q;
+        if (a.Qhi && row < a.qh_ld) {
+          uint32_t h, l;
+          split_bf16((float)q, h, l);
+          a.Qhi[(int64_t)i * a.qh_ss + (int64_t)c * a.qh_ld + row] = (uint16_t)h;
+          a.Qlo[(int64_t)i * a.qh_ss + (int64_t)c * a.qh_ld + row] = (uint16_t)l;
+        }
       }
     }
   }
-  // C_b[c][c'] = sum_j Q[j][c] z(j, c') over this block's rows (rows >= m count as zero)
-  double* cp = a.Cpart + ((int64_t)i * a.nblk + b) * s * a.r;
-  for (int pr = tid; pr < s * a.r; pr += kQrThreads) {
+  // probe words of rows b*128 .. b*128+127 (one Philox block per column)
+  for (int cc = lane; cc < a.r; cc += 64) {
+    const u32x4 v = rademacher_block(a.key0, a.key1, a.layer, kStreamProbe, (uint32_t)b, (uint32_t)cc);
+    zw[cc * 4 + 0] = v.x; zw[cc * 4 + 1] = v.y; zw[cc * 4 + 2] = v.z; zw[cc * 4 + 3] = v.w;
+  }
+  qr_wave_fence();
+  // C_b[c][cc] = sum_j Q[j][c] z(j, cc) over this block's rows
+  double* cp = a.Cpart + ((int64_t)i * L.nblk + b) * s * a.r;
+  for (int pr = lane; pr < s * a.r; pr += 64) {
     const int c = pr / a.r, cc = pr - c * a.r;
-    const double* wc = W + c * R;
-    const uint32_t* zb = zw + cc * wpb;
+    const double* qc = qs + c * (kQrRows + 1);
     double acc = 0.0;
-    for (int j = 0; j < R; ++j) {
-      const double q = (row0 + j < a.m) ? wc[j] : 0.0;
-      acc += ((zb[j >> 5] >> (j & 31)) & 1u) ? -q : q;
+    for (int w = 0; w < 4; ++w) {
+      const uint32_t bits = zw[cc * 4 + w];
+#pragma unroll
+      for (int jj = 0; jj < 32; ++jj) {
+        const double q = qc[32 * w + jj];
+        acc += ((bits >> jj) & 1u) ? -q : q;
+      }
     }
     cp[pr] = acc;
   }
 }
 
-QrPlan qr_plan(int64_t m, int s) {
-  QrPlan p;
-  // block rows: R x s fp64 in LDS (64 KB), R a multiple of 128 (whole probe blocks)
-  p.R = (int32_t)std::min<int64_t>(512, std::max<int64_t>(128, (8192 / std::max(s, 1)) / 128 * 128));
-  p.nblk = (int32_t)ceil_div(m, p.R);
-  return p;
+int32_t qr_levels(int64_t m, int s, int32_t rows[kQrMaxLevels], int32_t nblk[kQrMaxLevels], int64_t* dbl) {
+  int32_t n = 0;
+  int64_t r = m, total = 0;
+  while (n < kQrMaxLevels) {
+    rows[n] = (int32_t)r;
+    nblk[n] = (int32_t)ceil_div(r, kQrRows);
+    total += (int64_t)nblk[n] * s * kQrRows + (int64_t)nblk[n] * s;   // V, tau
+    if (n > 0) total += 2 * r * s;                                     // M, Q
+    ++n;
+    if (nblk[n - 1] == 1) break;
+    r = (int64_t)nblk[n - 1] * s;
+  }
+  if (nblk[n - 1] != 1) return 0;
+  if (dbl) *dbl = total;
+  return n;
 }
 
-static size_t qr_lds_expand(const QrArgs& a) {
-  return (size_t)a.s * a.R * 8 + (size_t)a.r * (a.R / 32) * 4;
-}
-
-hipError_t launch_qr_blocks(const QrArgs& a, hipStream_t st) {
-  DPRC_LAUNCH(qr_blocks_kernel, dim3((unsigned)a.nblk, (unsigned)a.B), dim3(kQrThreads),
-                     (size_t)a.s * a.R * 8, st, a);
+template <template <int> class K>
+static hipError_t launch_qr_sp(const QrArgs& a, int level, hipStream_t st) {
+  const dim3 grid((unsigned)a.lev[level].nblk, (unsigned)a.B);
+  if (a.s <= 8) DPRC_LAUNCH(K<8>::fn, grid, dim3(64), 0, st, a, level);
+  else if (a.s <= 16) DPRC_LAUNCH(K<16>::fn, grid, dim3(64), 0, st, a, level);
+  else DPRC_LAUNCH(K<32>::fn, grid, dim3(64), 0, st, a, level);
   return hipGetLastError();
 }
+template <int SP>
+struct QrFactorK {
+  static constexpr auto fn = qr_factor_kernel<SP>;
+};
+template <int SP>
+struct QrExpandK {
+  static constexpr auto fn = qr_expand_kernel<SP>;
+};
 
-hipError_t launch_qr_combine(const QrArgs& a, hipStream_t st) {
-  const size_t bytes = (size_t)2 * a.s * a.nblk * a.s * 8;
-  const int in_lds = bytes <= 96 * 1024;
-  DPRC_LAUNCH(qr_combine_kernel, dim3((unsigned)a.B), dim3(kQrThreads), in_lds ? bytes : 0, st, a, in_lds);
-  return hipGetLastError();
+hipError_t launch_qr_factor(const QrArgs& a, int level, hipStream_t st) {
+  if (a.s < 1 || a.s > 32 || a.r > 256 || level < 0 || level >= a.nlev) return hipErrorInvalidValue;
+  return launch_qr_sp<QrFactorK>(a, level, st);
 }
 
-hipError_t launch_qr_expand(const QrArgs& a, hipStream_t st) {
-  DPRC_LAUNCH(qr_expand_kernel, dim3((unsigned)a.nblk, (unsigned)a.B), dim3(kQrThreads), qr_lds_expand(a),
-                     st, a);
-  return hipGetLastError();
+hipError_t launch_qr_expand(const QrArgs& a, int level, hipStream_t st) {
+  if (a.s < 1 || a.s > 32 || a.r > 256 || level < 0 || level >= a.nlev) return hipErrorInvalidValue;
+  return launch_qr_sp<QrExpandK>(a, level, st);
 }
 
 // ---- finalize -----------------------------------------------------------------------------------------

@@ -130,28 +130,37 @@ struct TokredF32Args {
   int64_t m_ld, m_ss;
 };
 
-// Tall-skinny QR of O S (m x s per sample) and C = Q^T P (Hutch++).
+// Tall-skinny QR of O S (m x s per sample, s <= 32) and C = Q^T P (Hutch++), as a
+// tree of 128-row Householder block factorizations (one wavefront per block).
+// Level 1 factors 128-row blocks of O S; level l + 1 factors the stacked s x s R
+// factors of level l, until one block remains.  The expansion runs back down:
+// block b of level l starts from rows b*s .. b*s+s-1 of level l+1's Q (the identity
+// at the top) and applies its reflectors.
+constexpr int kQrRows = 128;   // rows per block (two per lane)
+constexpr int kQrMaxLevels = 8;
+struct QrLevel {
+  int32_t rows, nblk;            // input rows, blocks (= ceil(rows / 128))
+  double* V;                     // [B][nblk][s][128] reflectors, zero above the diagonal
+  double* tau;                   // [B][nblk][s]
+  double* M;                     // [B][s][rows] fp64 input (levels >= 2); level 1 reads O S
+  double* Q;                     // [B][s][rows] explicit Q of this level (levels >= 2)
+};
 struct QrArgs {
-  const float* OS;        // OS[i*os_ss + c*os_ld + j]
-  int64_t os_ld, os_ss;
   int32_t B, m, s, r;
-  int32_t R, nblk;        // rows per block, blocks
-  double* V;              // [B][nblk][s][R] block reflectors
-  double* tau;            // [B][nblk][s]
-  double* Rst;            // [B][s][nblk*s] stacked R factors, then their reflectors
-  double* Q2;             // [B][s][nblk*s]
-  double* Cpart;          // [B][nblk][s][r]
+  int32_t nlev;
+  QrLevel lev[kQrMaxLevels];
+  const float* OS;               // OS[i*os_ss + c*os_ld + j]
+  int64_t os_ld, os_ss;
+  double* Cpart;                 // [B][nblk1][s][r]
   uint32_t key0, key1, layer;
-  float* Q;               // Q[i*q_ss + c*q_ld + j] (may be null)
+  float* Q;                      // Q[i*q_ss + c*q_ld + j] (may be null)
   int64_t q_ld, q_ss;
-  uint16_t* Qhi;          // bf16 hi/lo pairs, zero for rows m .. qh_ld-1 (may be null)
+  uint16_t* Qhi;                 // bf16 hi/lo pairs, zero for rows m .. qh_ld-1 (may be null)
   uint16_t* Qlo;
   int64_t qh_ld, qh_ss;
 };
-struct QrPlan {
-  int32_t R, nblk;
-};
-QrPlan qr_plan(int64_t m, int s);
+// Level geometry for m rows and s columns; doubles of workspace per sample in *dbl.
+int32_t qr_levels(int64_t m, int s, int32_t rows[kQrMaxLevels], int32_t nblk[kQrMaxLevels], int64_t* dbl);
 
 // Hutch++ estimate from U | W_P (UW[i*uw_ss + c*uw_ld + j], c < s + r) and C.
 struct FinalArgs {
@@ -180,9 +189,8 @@ hipError_t launch_tokred_f32(const TokredF32Args& a, hipStream_t st);
 hipError_t launch_sample_sq(const float* M, int64_t m_ld, int64_t m_ss, int32_t B, int32_t ncols,
                             int32_t n, float scale, float* n2, float* n2_layer, int accumulate,
                             hipStream_t st);
-hipError_t launch_qr_blocks(const QrArgs& a, hipStream_t st);
-hipError_t launch_qr_combine(const QrArgs& a, hipStream_t st);
-hipError_t launch_qr_expand(const QrArgs& a, hipStream_t st);
+hipError_t launch_qr_factor(const QrArgs& a, int level, hipStream_t st);   // level 0 reads O S
+hipError_t launch_qr_expand(const QrArgs& a, int level, hipStream_t st);   // level 0 writes Q and C
 hipError_t launch_hpp_rows(const FinalArgs& a, hipStream_t st);
 hipError_t launch_hpp_sum(const FinalArgs& a, hipStream_t st);
 hipError_t launch_clip_scale(const float* n2, int64_t B, float C, float* c, hipStream_t st);
