@@ -326,6 +326,7 @@ size_t hutchpp_layout(const View& v, int32_t s, int32_t r, void* ws, PPBufs* out
     b.qr.Cpart = ar.take<double>((size_t)B * (nlev > 0 ? nblk[0] : 1) * s * r);
     b.fin.nchunk = final_chunks(v.n);
     b.fin.Fpart = ar.take<double>((size_t)B * b.fin.nchunk * 2);
+    b.fin.C = ar.take<double>((size_t)B * s * r);
   }
   if (v.dtype == DPRC_BF16) {
     b.pass_ws = ar.base ? ar.base + ((ar.off + kAlign - 1) / kAlign) * kAlign : nullptr;
@@ -432,6 +433,8 @@ dprc_status hutchpp_layer(const View& v, int32_t s, int32_t r, uint32_t k0, uint
   fa.UW = b.UW; fa.uw_ld = v.n; fa.uw_ss = (int64_t)(s + r) * v.n;
   fa.B = (int32_t)B; fa.n = (int32_t)v.n; fa.s = s; fa.r = r; fa.nblk = b.qr.nlev > 0 ? b.qr.lev[0].nblk : 0;
   fa.Cpart = b.qr.Cpart; fa.n2 = n2; fa.n2_layer = n2_layer; fa.accumulate = accumulate;
+  if ((e = traced(DPRC_KERNEL_QR_EXPAND, st, [&] { return launch_hpp_csum(fa, st); })) != hipSuccess)
+    return DPRC_ERROR_HIP;
   if ((e = traced(DPRC_KERNEL_HUTCHPP_FINAL, st, [&] { return launch_hpp_rows(fa, st); })) != hipSuccess)
     return DPRC_ERROR_HIP;
   return hip_status(traced(DPRC_KERNEL_HUTCHPP_SUM, st, [&] { return launch_hpp_sum(fa, st); }));

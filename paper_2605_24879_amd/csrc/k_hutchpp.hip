@@ -90,17 +90,32 @@ __global__ __launch_bounds__(64) void qr_factor_kernel(QrArgs a, int level) {
   const int b = blockIdx.x, i = blockIdx.y, lane = threadIdx.x;
   const int s = a.s;
   const QrLevel L = a.lev[level];
+  // all loads are issued before the first use: masked entries read a valid address
+  // and are replaced by zero
   double A[2][SP];
+  if (level == 0) {
+    const float* os = a.OS + (int64_t)i * a.os_ss;
 #pragma unroll
-  for (int u = 0; u < 2; ++u) {
-    const int row = b * kQrRows + lane + 64 * u;
+    for (int u = 0; u < 2; ++u) {
+      const int row = b * kQrRows + lane + 64 * u;
 #pragma unroll
-    for (int c = 0; c < SP; ++c) {
-      double x = 0.0;
-      if (c < s && row < L.rows)
-        x = level == 0 ? (double)a.OS[(int64_t)i * a.os_ss + (int64_t)c * a.os_ld + row]
-                       : L.M[((int64_t)i * s + c) * L.rows + row];
-      A[u][c] = x;
+      for (int c = 0; c < SP; ++c) {
+        const bool ok = c < s && row < L.rows;
+        const float x = os[ok ? (int64_t)c * a.os_ld + row : 0];
+        A[u][c] = ok ? (double)x : 0.0;
+      }
+    }
+  } else {
+    const double* ms = L.M + (int64_t)i * s * L.rows;
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int row = b * kQrRows + lane + 64 * u;
+#pragma unroll
+      for (int c = 0; c < SP; ++c) {
+        const bool ok = c < s && row < L.rows;
+        const double x = ms[ok ? (int64_t)c * L.rows + row : 0];
+        A[u][c] = ok ? x : 0.0;
+      }
     }
   }
   double* V = L.V + ((int64_t)i * L.nblk + b) * s * kQrRows;
@@ -178,23 +193,47 @@ __global__ __launch_bounds__(64) void qr_expand_kernel(QrArgs a, int level) {
   const QrLevel L = a.lev[level];
   const bool top = level + 1 == a.nlev;
   const QrLevel U = a.lev[top ? level : level + 1];
+  // all loads are issued before the first use (masked entries read a valid address)
   double W[2][SP];
+  const double* uq = U.Q + (int64_t)i * s * U.rows + (int64_t)b * s;
 #pragma unroll
   for (int u = 0; u < 2; ++u) {
     const int j = lane + 64 * u;
 #pragma unroll
     for (int c = 0; c < SP; ++c) {
+      const bool ok = c < s && j < s;
       double w = 0.0;
-      if (c < s && j < s) w = top ? (j == c ? 1.0 : 0.0) : U.Q[((int64_t)i * s + c) * U.rows + (int64_t)b * s + j];
+      if (top) w = ok && j == c ? 1.0 : 0.0;
+      else {
+        const double x = uq[ok ? (int64_t)c * U.rows + j : 0];
+        w = ok ? x : 0.0;
+      }
       W[u][c] = w;
     }
   }
+  // reflectors in reverse order: register column e holds v_{s-1-e}; the columns
+  // move down one place after each step, so every register index is a constant
   const double* Vb = L.V + ((int64_t)i * L.nblk + b) * s * kQrRows;
+  double Vr[2][SP];
+#pragma unroll
+  for (int u = 0; u < 2; ++u)
+#pragma unroll
+    for (int e = 0; e < SP; ++e) {
+      const bool ok = e < s;
+      const double x = Vb[ok ? (int64_t)(s - 1 - e) * kQrRows + lane + 64 * u : 0];
+      Vr[u][e] = ok ? x : 0.0;
+    }
   const double* tb = L.tau + ((int64_t)i * L.nblk + b) * s;
   for (int k = s - 1; k >= 0; --k) {
     const double t = tb[k];
+    const double v0 = Vr[0][0], v1 = Vr[1][0];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+#pragma unroll
+      for (int e = 0; e + 1 < SP; ++e) Vr[u][e] = Vr[u][e + 1];
+      Vr[u][SP - 1] = 0.0;
+    }
     if (t == 0.0) continue;                       // uniform
-    const double v0 = Vb[(int64_t)k * kQrRows + lane], v1 = Vb[(int64_t)k * kQrRows + lane + 64];
     double pv[SP];
 #pragma unroll
     for (int c = 0; c < SP; ++c) pv[c] = v0 * W[0][c] + v1 * W[1][c];
@@ -307,33 +346,62 @@ hipError_t launch_qr_expand(const QrArgs& a, int level, hipStream_t st) {
 // ---- finalize -----------------------------------------------------------------------------------------
 constexpr int kFinRows = 256;
 
+// C = sum of the block partials C_b, in block order (one thread per entry).
+__global__ __launch_bounds__(kFinRows) void hpp_csum_kernel(FinalArgs a) {
+  const int i = blockIdx.y;
+  const int sr = a.s * a.r;
+  const int e = blockIdx.x * kFinRows + threadIdx.x;
+  if (e >= sr) return;
+  const double* cp = a.Cpart + (int64_t)i * a.nblk * sr + e;
+  double v = 0.0;
+  int b = 0;
+  for (; b + 8 <= a.nblk; b += 8) {              // eight loads in flight, added in block order
+    double x[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) x[u] = cp[(int64_t)(b + u) * sr];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v += x[u];
+  }
+  for (; b < a.nblk; ++b) v += cp[(int64_t)b * sr];
+  a.C[(int64_t)i * sr + e] = v;
+}
+
 // Rows j of one chunk: ||U_j||^2 and ||W_P,j - U_j C||^2 summed over the chunk.
+template <int SP>
 __global__ __launch_bounds__(kFinRows) void hpp_rows_kernel(FinalArgs a) {
   extern __shared__ __attribute__((aligned(16))) float fs[];
   __shared__ double sh[4];
   const int ch = blockIdx.x, i = blockIdx.y, tid = threadIdx.x;
   const int s = a.s, r = a.r;
   float* C = fs;                           // [s][r]
-  // C = sum over blocks of the partial C_b, in block order
-  const double* cp = a.Cpart + (int64_t)i * a.nblk * s * r;
-  for (int e = tid; e < s * r; e += kFinRows) {
-    double v = 0.0;
-    for (int b = 0; b < a.nblk; ++b) v += cp[(int64_t)b * s * r + e];
-    C[e] = (float)v;
-  }
+  for (int e = tid; e < s * r; e += kFinRows) C[e] = (float)a.C[(int64_t)i * s * r + e];
   __syncthreads();
   const int64_t j = (int64_t)ch * kFinRows + tid;
   double su = 0.0, sv = 0.0;
   if (j < a.n) {
     const float* uw = a.UW + (int64_t)i * a.uw_ss + j;
-    for (int b2 = 0; b2 < r; ++b2) {
-      double v = (double)uw[(int64_t)(s + b2) * a.uw_ld];
-      for (int c = 0; c < s; ++c) v -= (double)uw[(int64_t)c * a.uw_ld] * (double)C[c * r + b2];
-      sv += v * v;
+    double u[SP];                                  // row j of U, loaded once
+#pragma unroll
+    for (int c = 0; c < SP; ++c) {
+      const float x = uw[(int64_t)(c < s ? c : 0) * a.uw_ld];
+      u[c] = c < s ? (double)x : 0.0;
+      su += u[c] * u[c];
     }
-    for (int c = 0; c < s; ++c) {
-      const double u = (double)uw[(int64_t)c * a.uw_ld];
-      su += u * u;
+    // residual columns 16 at a time: their loads are in flight together
+    for (int b0 = 0; b0 < r; b0 += 16) {
+      float w[16];
+#pragma unroll
+      for (int q = 0; q < 16; ++q) w[q] = uw[(int64_t)(s + (b0 + q < r ? b0 + q : 0)) * a.uw_ld];
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        if (b0 + q < r) {
+          double v = (double)w[q];
+#pragma unroll
+          for (int c = 0; c < SP; ++c)
+            if (c < s) v -= u[c] * (double)C[c * r + b0 + q];
+          sv += v * v;
+        }
+      }
     }
   }
   su = qr_block_sum(su, sh);
@@ -362,8 +430,17 @@ __global__ __launch_bounds__(kQrThreads) void hpp_sum_kernel(FinalArgs a) {
 }
 
 hipError_t launch_hpp_rows(const FinalArgs& a, hipStream_t st) {
-  DPRC_LAUNCH(hpp_rows_kernel, dim3((unsigned)a.nchunk, (unsigned)a.B), dim3(kFinRows),
-                     (size_t)a.s * a.r * 4, st, a);
+  const dim3 grid((unsigned)a.nchunk, (unsigned)a.B);
+  const size_t lds = (size_t)a.s * a.r * 4;
+  if (a.s <= 8) DPRC_LAUNCH(hpp_rows_kernel<8>, grid, dim3(kFinRows), lds, st, a);
+  else if (a.s <= 16) DPRC_LAUNCH(hpp_rows_kernel<16>, grid, dim3(kFinRows), lds, st, a);
+  else DPRC_LAUNCH(hpp_rows_kernel<32>, grid, dim3(kFinRows), lds, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_hpp_csum(const FinalArgs& a, hipStream_t st) {
+  DPRC_LAUNCH(hpp_csum_kernel, dim3((unsigned)ceil_div((int64_t)a.s * a.r, kFinRows), (unsigned)a.B),
+              dim3(kFinRows), 0, st, a);
   return hipGetLastError();
 }
 

@@ -38,11 +38,14 @@ struct PInt {
   static constexpr int value = V;
 };
 
-template <int RB, int NB, bool DENSE, bool FAST>
+// NBD: column blocks (of 16) holding dense columns, 0 when all columns are probes.
+template <int RB, int NB, int NBD, bool FAST>
 __global__ __launch_bounds__(kBlock) void project_kernel(ProjectArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint32_t smem[];
-  constexpr int P = RB == 1 ? 4 : 2;            // stages in flight per wave
+  constexpr bool DENSE = NBD > 0;
+  constexpr int P = (RB == 1 && !DENSE) ? 4 : 2;  // stages in flight per wave
   constexpr int NL = 4 * RB;                    // loads per lane per stage
+  constexpr int ND = DENSE ? 4 * NBD : 1;       // dense operand fragments (hi and lo) per stage
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int g = lane >> 4, l16 = lane & 15;
   const int i = blockIdx.y;
@@ -101,7 +104,12 @@ __global__ __launch_bounds__(kBlock) void project_kernel(ProjectArgs a) {
   // Stage st (absolute) of this wave: columns st*512 + 128*wv .. + 127.  Stages past
   // the chunk are issued too, out of range, so every stage has the same loads and
   // the waits on the in-order load counter count exactly.
-  auto gload = [&](uint4 (&dst)[NL], int st, int col_end) __attribute__((always_inline)) {
+  // Dense operand fragments of the stage travel in the same ring: fragment
+  // (kb, nbd) of a lane is R[16 nbd + l16][c0 + 32 kb + 8 g .. + 7] (R rows are
+  // zero-padded to a multiple of 128 columns); a lane past the dense columns or a
+  // slice past the width reads a valid address, and its value is not used.
+  auto gload = [&](uint4 (&dst)[NL], uint4 (&dh)[ND], uint4 (&dl)[ND], int st, int col_end)
+                   __attribute__((always_inline)) {
     const int c0 = st * kProjStage + kProjSlice * wv;
 #pragma unroll
     for (int j = 0; j < NL; ++j) {
@@ -113,6 +121,19 @@ __global__ __launch_bounds__(kBlock) void project_kernel(ProjectArgs a) {
         dst[j] = load8_elem(rowp[j], col, col_end, t0 + 4 * j + lrow < a.T);
       }
     }
+    if constexpr (DENSE) {
+      const int cb = c0 < col_end ? c0 : 0;
+#pragma unroll
+      for (int nbd = 0; nbd < NBD; ++nbd) {
+        const int c = 16 * nbd + l16;
+        const int64_t rowoff = (int64_t)(c < a.nd ? c : 0) * a.ld_r + cb + 8 * g;
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) {
+          dh[4 * nbd + kb] = *reinterpret_cast<const uint4*>(rhi + rowoff + 32 * kb);
+          dl[4 * nbd + kb] = *reinterpret_cast<const uint4*>(rlo + rowoff + 32 * kb);
+        }
+      }
+    }
   };
   auto to_lds = [&](const uint4 (&src)[NL]) __attribute__((always_inline)) {
     wave_lds_fence();                              // the previous stage's reads are done
@@ -121,7 +142,7 @@ __global__ __launch_bounds__(kBlock) void project_kernel(ProjectArgs a) {
       *reinterpret_cast<uint4*>(&xt[(4 * j + lrow) * kProjSlice + 8 * lslot]) = src[j];
     wave_lds_fence();
   };
-  auto mult = [&](int st, int uc) __attribute__((always_inline)) {
+  auto mult = [&](int st, int uc, const uint4 (&dh)[ND], const uint4 (&dl)[ND]) __attribute__((always_inline)) {
     const int c0 = st * kProjStage + kProjSlice * wv;
     if (c0 >= a.m) return;                         // wave-uniform: slice past the width
 #pragma unroll
@@ -134,21 +155,19 @@ __global__ __launch_bounds__(kBlock) void project_kernel(ProjectArgs a) {
           const uint32_t word = zw[zrow[nb] + w];
           bh = expand_signs(__builtin_amdgcn_perm(word, word, psel), zmask[nb], zone[nb]);
         }
-        if (DENSE && 16 * nb < a.nd) {   // uniform: only column blocks that hold dense columns load them
-          const int c = 16 * nb + l16;
-          const bool isd = c < a.nd;
-          const int64_t off = (int64_t)(isd ? c : 0) * a.ld_r + c0 + 32 * kb + 8 * g;
-          const uint4 dh = *reinterpret_cast<const uint4*>(rhi + off);
-          const uint4 dl = *reinterpret_cast<const uint4*>(rlo + off);
-          bh = select4(isd, dh, bh);
-          bl = select4(isd, dl, bl);
+        if constexpr (DENSE) {
+          if (nb < NBD) {                          // static: column blocks that hold dense columns
+            const bool isd = 16 * nb + l16 < a.nd;
+            bh = select4(isd, dh[4 * nb + kb], bh);
+            bl = select4(isd, dl[4 * nb + kb], bl);
+          }
         }
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) {
           const int r = 16 * rb + l16;
           const uint4 av = *reinterpret_cast<const uint4*>(&xt[r * kProjSlice + 8 * ((4 * kb + g) ^ l16)]);
           acc[rb][nb] = mfma16x16x32(av, bh, acc[rb][nb]);
-          if (DENSE) acc[rb][nb] = mfma16x16x32(av, bl, acc[rb][nb]);
+          if (DENSE && nb < NBD) acc[rb][nb] = mfma16x16x32(av, bl, acc[rb][nb]);
         }
       }
     }
@@ -158,9 +177,9 @@ __global__ __launch_bounds__(kBlock) void project_kernel(ProjectArgs a) {
     const int col_end = min(a.m, uc + 32 * wpc);
     const int s0 = uc / kProjStage;
     const int nst = (col_end - uc + kProjStage - 1) / kProjStage;
-    uint4 ring[P][NL];
+    uint4 ring[P][NL], rdh[P][ND], rdl[P][ND];
 #pragma unroll
-    for (int q = 0; q < P; ++q) gload(ring[q], s0 + q, q < nst ? col_end : 0);
+    for (int q = 0; q < P; ++q) gload(ring[q], rdh[q], rdl[q], s0 + q, q < nst ? col_end : 0);
     if (a.nz > 0) {                                // generated while the first stages are in flight
       __syncthreads();
       const int nblk = wpc >> 2;
@@ -182,9 +201,15 @@ __global__ __launch_bounds__(kBlock) void project_kernel(ProjectArgs a) {
     auto step = [&](int k, auto ph) __attribute__((always_inline)) {
       constexpr int q = decltype(ph)::value;
       const int st = s0 + k;
+      uint4 dh[ND], dl[ND];
+#pragma unroll
+      for (int e = 0; e < ND; ++e) {
+        dh[e] = rdh[q][e];
+        dl[e] = rdl[q][e];
+      }
       to_lds(ring[q]);
-      gload(ring[q], st + P, k + P < nst ? col_end : 0);
-      mult(st, uc);
+      gload(ring[q], rdh[q], rdl[q], st + P, k + P < nst ? col_end : 0);
+      mult(st, uc, dh, dl);
     };
     // whole groups of P stages in the loop (no early exit reaches its back edge,
     // so the compiler's wait counting stays exact), the remainder after it
@@ -240,18 +265,20 @@ static hipError_t launch_rb_nb(const ProjectArgs& a, hipStream_t st) {
   const size_t zbytes = a.nz > 0 ? (size_t)a.nz * (a.words_per_chunk + 1) * 4 : 0;
   const size_t rbytes = std::max((size_t)4 * 16 * RB * (16 * NB + 4) * 4, (size_t)4 * 16 * RB * kProjSlice * 2);
   const size_t lds = zbytes + rbytes;
-  if (a.words_per_chunk % 16 != 0) return hipErrorInvalidValue;
+  if (a.words_per_chunk % 16 != 0 || a.nd > 32 || a.nd > 16 * NB) return hipErrorInvalidValue;
   dim3 grid((unsigned)(a.T_pad / (16 * RB)), (unsigned)a.B);
   // buffer offsets of one workgroup's rows stay below 2^31
   const bool fast = a.vec && a.m % 8 == 0 && (int64_t)16 * RB * a.ldx * 2 < ((int64_t)1 << 31);
-  if (a.nd > 0 && fast)
-    DPRC_LAUNCH((project_kernel<RB, NB, true, true>), grid, dim3(kBlock), lds, st, a);
-  else if (a.nd > 0)
-    DPRC_LAUNCH((project_kernel<RB, NB, true, false>), grid, dim3(kBlock), lds, st, a);
-  else if (fast)
-    DPRC_LAUNCH((project_kernel<RB, NB, false, true>), grid, dim3(kBlock), lds, st, a);
-  else
-    DPRC_LAUNCH((project_kernel<RB, NB, false, false>), grid, dim3(kBlock), lds, st, a);
+  const int nbd = (a.nd + 15) / 16;
+#define DPRC_PROJECT_CASE(NBD)                                                           \
+  if (nbd == NBD) {                                                                      \
+    if (fast) DPRC_LAUNCH((project_kernel<RB, NB, NBD, true>), grid, dim3(kBlock), lds, st, a);  \
+    else DPRC_LAUNCH((project_kernel<RB, NB, NBD, false>), grid, dim3(kBlock), lds, st, a);      \
+  }
+  DPRC_PROJECT_CASE(0)
+  if constexpr (NB >= 1) { DPRC_PROJECT_CASE(1) }
+  if constexpr (NB >= 2) { DPRC_PROJECT_CASE(2) }
+#undef DPRC_PROJECT_CASE
   return hipGetLastError();
 }
 

@@ -168,6 +168,7 @@ struct FinalArgs {
   int64_t uw_ld, uw_ss;
   int32_t B, n, s, r, nblk, nchunk;
   const double* Cpart;    // [B][nblk][s][r]
+  double* C;              // [B][s][r]: C = Q^T P, the block partials summed in block order
   double* Fpart;          // [B][nchunk][2]
   float* n2;
   float* n2_layer;
@@ -191,6 +192,7 @@ hipError_t launch_sample_sq(const float* M, int64_t m_ld, int64_t m_ss, int32_t 
                             hipStream_t st);
 hipError_t launch_qr_factor(const QrArgs& a, int level, hipStream_t st);   // level 0 reads O S
 hipError_t launch_qr_expand(const QrArgs& a, int level, hipStream_t st);   // level 0 writes Q and C
+hipError_t launch_hpp_csum(const FinalArgs& a, hipStream_t st);
 hipError_t launch_hpp_rows(const FinalArgs& a, hipStream_t st);
 hipError_t launch_hpp_sum(const FinalArgs& a, hipStream_t st);
 hipError_t launch_clip_scale(const float* n2, int64_t B, float C, float* c, hipStream_t st);
