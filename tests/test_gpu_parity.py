@@ -138,10 +138,16 @@ def test_hutch_deterministic(D):
 
 # ---- Hutch++ ------------------------------------------------------------------------------
 
+# The QR tree factors 128-row blocks and stacks their s x s R factors: the cases
+# below take 2 and 3 levels, odd s (s = 5, padded to 8 register columns), s = 1
+# and s = 32 (the largest), with ragged last blocks.
 @pytest.mark.parametrize("B,T,d,p,s,r,side,dtype", [
     (2, 300, 200, 150, 8, 12, 0, "bf16"),
     (1, 520, 136, 300, 16, 32, 1, "bf16"),
     (2, 64, 64, 48, 4, 4, 0, "f32"),
+    (1, 200, 600, 96, 32, 16, 1, "bf16"),      # m = 600: 5 blocks -> 160 rows -> 2 -> 1 (3 levels)
+    (2, 150, 64, 1100, 5, 7, 0, "bf16"),       # m = 1100: 9 blocks -> 45 rows -> 1
+    (2, 100, 50, 260, 1, 3, 0, "bf16"),        # s = 1
 ])
 def test_hutchpp_parity(D, B, T, d, p, s, r, side, dtype):
     A, E = _draw(B, T, d, p, dtype=dtype, law="student_t", layer=2)
@@ -154,6 +160,15 @@ def test_hutchpp_parity(D, B, T, d, p, s, r, side, dtype):
 def test_hutchpp_low_rank_is_exact(D, dtype):
     A, E = _draw(2, 12, 80, 96, dtype=dtype, layer=7)      # rank(A_i^T E_i) <= 12 <= s
     n2 = D.dprc_norm_hutchpp([(A, E, 0)], 16, 8, 11)
+    exact = est.exact_layer(_np(A), _np(E))
+    assert np.all(_rel(n2.cpu().numpy(), exact) < NORM_RTOL)
+
+
+@pytest.mark.parametrize("side", [0, 1])
+def test_hutchpp_low_rank_is_exact_deep_tree(D, side):
+    # rank(A_i^T E_i) <= 12 <= s; the sketched width 1500 takes a 3-level QR tree
+    A, E = _draw(2, 12, 1500 if side == 1 else 80, 80 if side == 1 else 1500, layer=9)
+    n2 = D.dprc_norm_hutchpp([(A, E, 0)], 16, 8, 13, side=side)
     exact = est.exact_layer(_np(A), _np(E))
     assert np.all(_rel(n2.cpu().numpy(), exact) < NORM_RTOL)
 

@@ -86,6 +86,9 @@ def test_hutchpp_and_accumulate_validation():
     assert L.dprc_norm_hutchpp(arr, 1, 4, 0, 0, 0, 0x40000, None, 0, 0x30000, 1 << 30, None) == 1
     assert L.dprc_norm_hutchpp(arr, 1, 49, 4, 0, 0, 0x40000, None, 0, 0x30000, 1 << 30, None) == 1  # s > p
     assert L.dprc_norm_hutchpp(arr, 1, 4, 4, 0, 0, 0x40000, None, 0, 0x30000, 0, None) == 3
+    # a sketched width of 2^22 rows needs a QR tree deeper than eight levels
+    wide = (dprc.Layer * 1)(_fake_layer(p=1 << 22, lde=1 << 22))
+    assert L.dprc_norm_hutchpp(wide, 1, 32, 4, 0, 0, 0x40000, None, 0, 0x30000, 1 << 40, None) == 2
     lay = _fake_layer()
     assert L.dprc_clip_accumulate(ctypes.byref(lay), None, 0x50000, 48, 0, None, 0, None) == 1
     assert L.dprc_clip_accumulate(ctypes.byref(lay), 0x60000, 0x50000, 47, 0, None, 0, None) == 1
