@@ -62,8 +62,11 @@ __device__ __forceinline__ void wave_vec_sum(double (&v)[SP], int c_lo, double* 
   const int c = lane % SP, g = lane / SP;
   double x = 0.0;
   if (c >= c_lo) {
+    double t[SP];                                 // all reads in flight before the adds
 #pragma unroll
-    for (int q = 0; q < SP; ++q) x += red[c * kRedLd + g * SP + q];
+    for (int q = 0; q < SP; ++q) t[q] = red[c * kRedLd + g * SP + q];
+#pragma unroll
+    for (int q = 0; q < SP; ++q) x += t[q];
   }
 #pragma unroll
   for (int e = 0; e < 6; ++e)
@@ -281,21 +284,38 @@ __global__ __launch_bounds__(64) void qr_expand_kernel(QrArgs a, int level) {
     zw[cc * 4 + 0] = v.x; zw[cc * 4 + 1] = v.y; zw[cc * 4 + 2] = v.z; zw[cc * 4 + 3] = v.w;
   }
   qr_wave_fence();
-  // C_b[c][cc] = sum_j Q[j][c] z(j, cc) over this block's rows
+  // C_b[c][cc] = sum_j Q[j][c] z(j, cc) over this block's rows; a lane takes
+  // outputs pr = lane + 64 t, four at a time so that four sums advance together
   double* cp = a.Cpart + ((int64_t)i * L.nblk + b) * s * a.r;
-  for (int pr = lane; pr < s * a.r; pr += 64) {
-    const int c = pr / a.r, cc = pr - c * a.r;
-    const double* qc = qs + c * (kQrRows + 1);
-    double acc = 0.0;
+  for (int p0 = lane; p0 < s * a.r; p0 += 256) {
+    const double* qc[4];
+    uint32_t zoff[4];
+    bool on[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int pr = p0 + 64 * t;
+      on[t] = pr < s * a.r;
+      const int c = on[t] ? pr / a.r : 0, cc = on[t] ? pr - c * a.r : 0;
+      qc[t] = qs + c * (kQrRows + 1);
+      zoff[t] = (uint32_t)cc * 4;
+    }
+    double acc[4] = {0.0, 0.0, 0.0, 0.0};
     for (int w = 0; w < 4; ++w) {
-      const uint32_t bits = zw[cc * 4 + w];
+      uint32_t bits[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) bits[t] = zw[zoff[t] + w];
 #pragma unroll
       for (int jj = 0; jj < 32; ++jj) {
-        const double q = qc[32 * w + jj];
-        acc += ((bits >> jj) & 1u) ? -q : q;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const double q = qc[t][32 * w + jj];
+          acc[t] += ((bits[t] >> jj) & 1u) ? -q : q;
+        }
       }
     }
-    cp[pr] = acc;
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+      if (on[t]) cp[p0 + 64 * t] = acc[t];
   }
 }
 
