@@ -81,10 +81,15 @@ def _oriented(G, side):
 
 
 def probe_matrix(kind, seed, layer_id, stream_id, m, k):
+    """m x k probes: +-1 from stream `stream_id`, Sylvester-Hadamard signs, or
+    standard normals (the Gaussian probes of Algorithm 2 scaled by sqrt(k); they
+    have their own stream, 3, whatever `stream_id` says)."""
     if kind == "rademacher":
         return philox.rademacher_matrix(seed, layer_id, stream_id, m, k)
     if kind == "hadamard":
         return philox.hadamard_matrix(m, k)
+    if kind == "gaussian":
+        return philox.gaussian_probe_matrix(seed, layer_id, m, k)
     raise ValueError(kind)
 
 

@@ -24,7 +24,11 @@ definition independently):
   layer_id, s)).  Bit ``b`` of the word is row ``32w+b``; bit 0 means +1 and
   bit 1 means -1.
 * streams: 0 = Hutchinson probes P (also the Hutch++ residual probes),
-  1 = Hutch++ sketch S, 2 = Gaussian noise.
+  1 = Hutch++ sketch S, 2 = Gaussian noise, 3 = Gaussian Hutchinson probes.
+* Gaussian probe entry of row ``u`` and column ``j`` (the Gaussian probes of
+  Algorithm 2, standard normal here and divided by k in the estimate): block
+  q = u div 4, counter = (q, j, layer_id, 3); words (x0,x1) give rows 4q, 4q+1
+  and (x2,x3) give 4q+2, 4q+3 by the same Box-Muller transform as the noise.
 * noise element ``e`` of tensor ``t``: block q = e div 4, counter =
   (q mod 2^32, q div 2^32, t, 2); words (x0,x1) give elements 4q, 4q+1 and
   (x2,x3) give 4q+2, 4q+3 by the Box-Muller transform with
@@ -43,6 +47,7 @@ _SH = np.uint64(32)
 STREAM_PROBE = 0
 STREAM_SKETCH = 1
 STREAM_NOISE = 2
+STREAM_GAUSS_PROBE = 3
 
 
 def philox4x32_10(ctr, key):
@@ -143,3 +148,32 @@ def gaussian(seed, tensor_id, start, count):
     flat = out.reshape(-1)
     off = start - 4 * q0
     return flat[off:off + count]
+
+
+def _box_muller_blocks(x):
+    """Four standard normals per Philox block: (x0,x1) and (x2,x3) through Box-Muller."""
+    out = np.empty(x.shape[:-1] + (4,), dtype=np.float64)
+    for pair in range(2):
+        u1 = _uniform_open(x[..., 2 * pair])
+        u2 = _uniform_open(x[..., 2 * pair + 1])
+        r = np.sqrt(-2.0 * np.log(u1))
+        out[..., 2 * pair] = r * np.cos(2.0 * np.pi * u2)
+        out[..., 2 * pair + 1] = r * np.sin(2.0 * np.pi * u2)
+    return out
+
+
+def gaussian_probe_matrix(seed, layer_id, m, k):
+    """m x k standard-normal probes (fp64) of the Gaussian Hutchinson option."""
+    if m <= 0 or k <= 0:
+        return np.zeros((max(m, 0), max(k, 0)))
+    nq = (m + 3) // 4
+    q = np.arange(nq, dtype=np.uint64)
+    j = np.arange(k, dtype=np.uint64)
+    ctr = np.zeros((k, nq, 4), dtype=np.uint64)
+    ctr[:, :, 0] = q[None, :]
+    ctr[:, :, 1] = j[:, None]
+    ctr[:, :, 2] = np.uint64(layer_id & 0xFFFFFFFF)
+    ctr[:, :, 3] = np.uint64(STREAM_GAUSS_PROBE)
+    x = philox4x32_10(ctr, _key(seed))                     # [k, nq, 4]
+    z = _box_muller_blocks(x).reshape(k, 4 * nq)[:, :m]    # [k, m]
+    return z.T.copy()

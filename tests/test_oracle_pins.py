@@ -100,6 +100,39 @@ def test_gaussian_moments_and_ks():
     assert abs(np.corrcoef(x[:10_000], y)[0, 1]) < 0.05
 
 
+def test_gaussian_probes_are_standard_normal_and_independent():
+    """The Gaussian probe option (Algorithm 2 draws P from a normal law): moments, a KS test,
+    kurtosis 3 (+-1 probes have 1), and uncorrelated columns and layers."""
+    Z = philox.gaussian_probe_matrix(3, 7, 4099, 64)          # ragged m: the last block is cut
+    x = Z.reshape(-1)
+    assert Z.shape == (4099, 64)
+    assert abs(x.mean()) < 5 / math.sqrt(x.size)
+    assert abs(x.var() - 1.0) < 5 * math.sqrt(2.0 / x.size)
+    assert abs(scipy.stats.kurtosis(x, fisher=False) - 3.0) < 0.1
+    assert scipy.stats.kstest(x, "norm").pvalue > 1e-4
+    C = np.corrcoef(Z.T)
+    assert np.max(np.abs(C - np.eye(64))) < 5.5 / math.sqrt(4099)
+    Z2 = philox.gaussian_probe_matrix(3, 8, 4099, 4)
+    assert abs(np.corrcoef(Z[:, 0], Z2[:, 0])[0, 1]) < 5 / math.sqrt(4099)
+    # a prefix of rows does not depend on m
+    assert np.array_equal(philox.gaussian_probe_matrix(3, 7, 10, 2), Z[:10, :2])
+
+
+def test_hutch_gaussian_moments_match_closed_form():
+    """Gaussian probes: mean -> ||G||_F^2 and variance -> (2/k) ||O||_F^2, O = G^T G, which
+    differs from the +-1 value (2/k)(||O||_F^2 - sum_u O_uu^2) by the diagonal term."""
+    A, E = _rng_inputs(1, 4, 3, 6, seed=5)
+    G = est.per_sample_grad(A[0], E[0])
+    O = G.T @ G
+    k, n = 2, 6000
+    vals = np.array([est.hutch_layer(A, E, k, seed, 0, probe="gaussian")[0] for seed in range(n)])
+    var_th = 2.0 / k * np.sum(O * O)
+    var_rad = 2.0 / k * (np.sum(O * O) - np.sum(np.diag(O) ** 2))
+    assert var_th > 1.5 * var_rad                      # the two laws are told apart below
+    assert abs(vals.mean() - np.sum(G * G)) < 5 * math.sqrt(var_th / n)
+    assert 0.85 < vals.var(ddof=1) / var_th < 1.18
+
+
 # ---- exact norms -------------------------------------------------------------
 
 @pytest.mark.parametrize("T,d,p", [(64, 64, 48), (7, 3, 5), (33, 17, 70)])
