@@ -2,6 +2,7 @@
 """Throughput of randomized per-sample norm estimation (DP-SGD-RC) on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload q_proj|tiny|mlp|decoder|stack]
+                    [--probe rademacher|gaussian]
 
 One step is one pass of the workload's hot path over one batch already
 resident in HBM: the norm estimates of every layer (Hutchinson, or Hutch++ for
@@ -37,6 +38,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="q_proj")
+    ap.add_argument("--probe", default="rademacher", choices=["rademacher", "gaussian"],
+                    help="Hutchinson probe family (Gaussian: dense columns, k <= 32)")
     ap.add_argument("--rotate-bytes", type=float, default=1.2e9,
                     help="total bytes of rotated input copies (defeats the 256 MB Infinity Cache)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU oracle sample")
@@ -91,12 +94,17 @@ def make_inputs(cfg, torch, workloads, copies):
     return sets
 
 
+def probe_id(D, cfg):
+    return D.PROBE_GAUSSIAN if cfg.get("probe") == "gaussian" else D.PROBE_RADEMACHER
+
+
 def step_fn(cfg, D, torch, ws_norm, grads, ws_acc):
     C = cfg["C"]
+    probe = probe_id(D, cfg)
 
     def step(layers, n2, c):
         if cfg["estimator"] == "hutch":
-            D.dprc_norm_hutch(layers, cfg["k"], 0, n2=n2, ws=ws_norm)
+            D.dprc_norm_hutch(layers, cfg["k"], 0, n2=n2, ws=ws_norm, probe=probe)
         else:
             D.dprc_norm_hutchpp(layers, cfg["s"], cfg["r"], 0, n2=n2, ws=ws_norm)
         D.dprc_clip_scale(n2, C, c=c)
@@ -185,8 +193,9 @@ def cpu_baseline(cfg, sets, budget_s):
             Ai = A[i].float().cpu().numpy().astype(np.float64)
             Ei = E[i].float().cpu().numpy().astype(np.float64)
             if cfg["estimator"] == "hutch":
-                Z = philox.rademacher_matrix(0, li, 0, p, cfg["k"])
-                est.hutch_layer(Ai[None], Ei[None], cfg["k"], 0, li, Z=Z)
+                kind = cfg.get("probe", "rademacher")
+                Z = est.probe_matrix(kind, 0, li, 0, p, cfg["k"])
+                est.hutch_layer(Ai[None], Ei[None], cfg["k"], 0, li, probe=kind, Z=Z)
             else:
                 est.hutchpp_layer(Ai[None], Ei[None], cfg["s"], cfg["r"], 0, li)
             done_tokens += T
@@ -263,7 +272,11 @@ def main():
         print(json.dumps({"copy_calibration_bytes": n, "copies": 5}))
         return
     D.lib()
-    cfg = workloads.BY_NAME[args.workload]
+    cfg = dict(workloads.BY_NAME[args.workload])
+    if args.probe != "rademacher":
+        if cfg["estimator"] != "hutch":
+            sys.exit(f"--probe {args.probe} applies to Hutchinson workloads only")
+        cfg["probe"] = args.probe
     B, T = cfg["B"], cfg["T"]
     elem = 4 if cfg["dtype"] == "f32" else 2
     in_bytes = sum(B * T * (d + p) * elem for (_, d, p) in cfg["layers"])
@@ -273,7 +286,7 @@ def main():
     sets = make_inputs(cfg, torch, workloads, copies)
     pairs0 = sets[0]
     if cfg["estimator"] == "hutch":
-        ws_n = torch.empty(max(1, D.dprc_norm_hutch_workspace(pairs0, cfg["k"])), dtype=torch.uint8, device="cuda")
+        ws_n = torch.empty(max(1, D.dprc_norm_hutch_workspace(pairs0, cfg["k"], probe=probe_id(D, cfg))), dtype=torch.uint8, device="cuda")
     else:
         ws_n = torch.empty(max(1, D.dprc_norm_hutchpp_workspace(pairs0, cfg["s"], cfg["r"])), dtype=torch.uint8,
                            device="cuda")
@@ -340,7 +353,7 @@ def main():
         bytes_per_launch = kb[dom] / launches_per_step
         achieved = kb[dom] * args.steps / (tot_ms * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": measured_traffic(cfg["name"], dom),
+                "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": measured_traffic(cfg["name"] + ("_gaussian" if cfg.get("probe") == "gaussian" else ""), dom),
                 "kernel": dom,
                 "bytes_per_launch": int(bytes_per_launch), "avg_launch_us": round(tot_ms / cnt * 1e3, 2)}
     elif dom == "accumulate":
@@ -356,7 +369,7 @@ def main():
     norm_ms = sum(per_kind.get(k, (0.0, 0))[0] for k in ("project", "token_reduce", "qr", "hutchpp_final",
                                                           "project_f32", "token_reduce_f32", "sample_sq",
                                                           "probe_bits", "token_splits", "sample_sum", "qr_combine", "qr_expand",
-                                                          "hutchpp_sum")) / args.steps
+                                                          "hutchpp_sum", "probe_gauss")) / args.steps
     kernels = {k: {"launches_per_step": v[1] / args.steps, "avg_launch_us": round(v[0] / v[1] * 1e3, 2),
                    "us_per_step": round(v[0] / args.steps * 1e3, 2)} for k, v in sorted(per_kind.items())}
     extra = {"norm_kernels_us_per_step": round(norm_ms * 1e3, 2),

@@ -72,8 +72,14 @@ typedef enum { DPRC_SIDE_OUT = 0, DPRC_SIDE_IN = 1, DPRC_SIDE_AUTO = 2 } dprc_si
 /* Probe family.  RADEMACHER: the counter-generated +-1 probes above.
  * HADAMARD: the deterministic Sylvester-Hadamard signs z(u,j) =
  * (-1)^popcount(u & j) (verification: with k = 2^q >= the sketched dimension
- * the estimate equals the exact squared norm). */
-typedef enum { DPRC_PROBE_RADEMACHER = 0, DPRC_PROBE_HADAMARD = 1 } dprc_probe;
+ * the estimate equals the exact squared norm).  GAUSSIAN (Hutchinson only,
+ * k <= 32): the normal-law probes of Algorithm 2 (standard normal entries, the
+ * estimate divided by k as for the other families), entry (u, j) from Philox
+ * stream 3 block (u div 4, j, layer_id, 3) through the Box-Muller transform of
+ * dprc_add_noise: words (x0, x1) give rows 4q, 4q+1 and (x2, x3) rows 4q+2,
+ * 4q+3.  They are generated into the workspace as bf16 hi + lo pairs (fp32 for
+ * fp32 layers) and applied as dense probe columns. */
+typedef enum { DPRC_PROBE_RADEMACHER = 0, DPRC_PROBE_HADAMARD = 1, DPRC_PROBE_GAUSSIAN = 2 } dprc_probe;
 
 /* One bias-free linear layer S = A W (section "Proposed Method"). */
 typedef struct {
@@ -93,10 +99,12 @@ typedef struct {
  *                           sum over the layers of the estimates (Algorithm 1,
  *                           layer-wise summation).  fp32, device.
  *   n2_layers[num_layers*B]: optional (may be NULL) per-layer estimates.
- *   k in [1, 256].  All layers must have the same B.
- * Workspace: dprc_norm_hutch_workspace() bytes for the same arguments. */
+ *   k in [1, 256] (GAUSSIAN probes: k <= 32, else DPRC_ERROR_NOT_SUPPORTED).
+ *   All layers must have the same B.
+ * Workspace: dprc_norm_hutch_workspace() bytes for the same arguments (0 when
+ * they are invalid). */
 size_t dprc_norm_hutch_workspace(const dprc_layer* layers, int32_t num_layers, int32_t k,
-                                 dprc_side side);
+                                 dprc_probe probe, dprc_side side);
 dprc_status dprc_norm_hutch(const dprc_layer* layers, int32_t num_layers, int32_t k,
                             dprc_probe probe, uint64_t seed, dprc_side side, float* n2,
                             float* n2_layers, int32_t accumulate, void* ws, size_t ws_bytes,
@@ -149,6 +157,12 @@ dprc_status dprc_probe_bits(dprc_probe probe, uint64_t seed, uint32_t layer_id,
                             uint32_t stream_id, int64_t m, int32_t k, uint32_t* out,
                             hipStream_t stream);
 
+/* ---- Gaussian probe values (verification) ----------------------------------------
+ * out[j*m + u] = the GAUSSIAN probe entry (u, j) in fp32, u < m, j < k (k in
+ * [1, 256]).  Device out. */
+dprc_status dprc_probe_gaussian(uint64_t seed, uint32_t layer_id, int64_t m, int32_t k, float* out,
+                                hipStream_t stream);
+
 /* ---- per-launch timing (diagnostics, for profilers and benchmarks) ------------
  * While `events` is non-NULL, every kernel that a dprc call enqueues from THIS
  * host thread is launched with hipExtLaunchKernelGGL and start/stop events that
@@ -177,7 +191,8 @@ typedef enum {
   DPRC_KERNEL_SAMPLE_SUM = 15,        /* per-sample sum of tile squares         */
   DPRC_KERNEL_QR_COMBINE = 16,        /* QR of stacked block R factors (upper tree levels) */
   DPRC_KERNEL_QR_EXPAND = 17,         /* rows of Q per tree level; Q^T P at the first */
-  DPRC_KERNEL_HUTCHPP_SUM = 18        /* per-sample Hutch++ estimate            */
+  DPRC_KERNEL_HUTCHPP_SUM = 18,       /* per-sample Hutch++ estimate            */
+  DPRC_KERNEL_PROBE_GAUSS = 19        /* Gaussian probe columns                  */
 } dprc_kernel_kind;
 dprc_status dprc_trace_launches(hipEvent_t* events, int32_t* kinds, int32_t capacity,
                                 int32_t* count);

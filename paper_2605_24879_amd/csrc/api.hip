@@ -177,6 +177,7 @@ struct PassSpec {
   const uint16_t* X; int64_t ldx, m;      // projected operand
   const uint16_t* Xo; int64_t ldo, n;     // reduced operand
   int32_t nd; const uint16_t* Rhi; const uint16_t* Rlo; int64_t ld_r;   // dense columns
+  bool shared_r;                                                        // one R for all samples
   int32_t nz; uint32_t stream_id; int probe_kind;                       // generated columns
   int mode; float scale; float* n2; float* n2_layer; int accumulate;    // mode 0
   float* M; int64_t m_ld; uint16_t* Mhi; uint16_t* Mlo; int64_t mh_ld;  // mode 1
@@ -207,7 +208,7 @@ dprc_status run_pass(const PassSpec& ps, int64_t B, int64_t T, uint32_t k0, uint
   pa.X = ps.X; pa.ldx = ps.ldx; pa.x_ss = T * ps.ldx;
   pa.B = (int32_t)B; pa.T = (int32_t)T; pa.m = (int32_t)ps.m; pa.T_pad = tp.T_pad;
   pa.nd = ps.nd; pa.nz = ps.nz; pa.ncols_pad = ncols_pad;
-  pa.Rhi = ps.Rhi; pa.Rlo = ps.Rlo; pa.ld_r = ps.ld_r; pa.r_ss = (int64_t)ps.nd * ps.ld_r;
+  pa.Rhi = ps.Rhi; pa.Rlo = ps.Rlo; pa.ld_r = ps.ld_r; pa.r_ss = ps.shared_r ? 0 : (int64_t)ps.nd * ps.ld_r;
   pa.probe_kind = ps.probe_kind; pa.key0 = k0; pa.key1 = k1; pa.layer_id = layer; pa.stream_id = ps.stream_id;
   pa.words_per_chunk = words_per_chunk(ps.m, ps.nz);
   pa.Yt = Yt; pa.yt_ld = B * tp.T_pad;
@@ -243,10 +244,31 @@ size_t pass_ws_bytes(int64_t B, int64_t T, int64_t n, int ncols) {
 }
 
 // ---- Hutchinson ---------------------------------------------------------------------------------
-size_t hutch_layer_ws(const View& v, int32_t k) {
-  if (v.dtype == DPRC_BF16) return pass_ws_bytes(v.B, v.T, v.n, k);
+constexpr int32_t kMaxGaussK = 32;   // Gaussian probes travel as dense columns (at most 32)
+
+// Gaussian probe columns, generated at the front of the workspace: bf16 hi + lo
+// pairs with rows padded to a multiple of 128 (the projection reads whole
+// 128-column slices), or fp32 for fp32 layers.
+struct GaussBufs { uint16_t *hi, *lo; float* f32; int64_t ld; };
+
+GaussBufs take_gauss(Arena& ar, const View& v, int32_t k) {
+  GaussBufs g{};
+  if (v.dtype == DPRC_BF16) {
+    g.ld = round_up(v.m, kTile);
+    g.hi = ar.take<uint16_t>((size_t)k * g.ld);
+    g.lo = ar.take<uint16_t>((size_t)k * g.ld);
+  } else {
+    g.ld = v.m;
+    g.f32 = ar.take<float>((size_t)k * g.ld);
+  }
+  return g;
+}
+
+size_t hutch_layer_ws(const View& v, int32_t k, int probe) {
   Arena ar(nullptr);
-  ar.take<uint32_t>((size_t)k * ceil_div(v.m, 32));
+  if (probe == DPRC_PROBE_GAUSSIAN) take_gauss(ar, v, k);
+  if (v.dtype == DPRC_BF16) return round_up((int64_t)ar.off, kAlign) + pass_ws_bytes(v.B, v.T, v.n, k);
+  if (probe != DPRC_PROBE_GAUSSIAN) ar.take<uint32_t>((size_t)k * ceil_div(v.m, 32));
   ar.take<float>((size_t)v.B * v.T * k);
   ar.take<float>((size_t)v.B * k * v.n);
   return ar.off;
@@ -254,22 +276,38 @@ size_t hutch_layer_ws(const View& v, int32_t k) {
 
 dprc_status hutch_layer(const View& v, int32_t k, int probe, uint32_t k0, uint32_t k1, float* n2,
                         float* n2_layer, int accumulate, void* ws, hipStream_t st) {
+  const bool gauss = probe == DPRC_PROBE_GAUSSIAN;
+  Arena ar(ws);
+  GaussBufs g{};
+  if (gauss) {
+    g = take_gauss(ar, v, k);
+    hipError_t e = traced(DPRC_KERNEL_PROBE_GAUSS, st, [&] {
+      return launch_gauss_probe(k0, k1, v.layer_id, v.m, k, g.ld, g.hi, g.lo, g.f32, st); });
+    if (e != hipSuccess) return DPRC_ERROR_HIP;
+  }
   if (v.dtype == DPRC_BF16) {
     PassSpec ps{};
     ps.X = (const uint16_t*)v.X; ps.ldx = v.ldx; ps.m = v.m;
     ps.Xo = (const uint16_t*)v.Xo; ps.ldo = v.ldo; ps.n = v.n;
-    ps.nd = 0; ps.nz = k; ps.stream_id = 0; ps.probe_kind = probe;
+    if (gauss) {
+      ps.nd = k; ps.Rhi = g.hi; ps.Rlo = g.lo; ps.ld_r = g.ld; ps.shared_r = true; ps.nz = 0;
+    } else {
+      ps.nd = 0; ps.nz = k; ps.stream_id = 0; ps.probe_kind = probe;
+    }
     ps.mode = 0; ps.scale = 1.0f / (float)k; ps.n2 = n2; ps.n2_layer = n2_layer; ps.accumulate = accumulate;
-    return run_pass(ps, v.B, v.T, k0, k1, v.layer_id, ws, st);
+    return run_pass(ps, v.B, v.T, k0, k1, v.layer_id, ar.take<char>(0), st);
   }
-  Arena ar(ws);
-  uint32_t* zb = ar.take<uint32_t>((size_t)k * ceil_div(v.m, 32));
+  uint32_t* zb = gauss ? nullptr : ar.take<uint32_t>((size_t)k * ceil_div(v.m, 32));
   float* Y = ar.take<float>((size_t)v.B * v.T * k);
   float* M = ar.take<float>((size_t)v.B * k * v.n);
-  hipError_t e = traced(DPRC_KERNEL_PROBE_BITS, st, [&] { return launch_probe_bits(probe, k0, k1, v.layer_id, 0, v.m, k, zb, st); });
-  if (e != hipSuccess) return DPRC_ERROR_HIP;
-  ProjectF32Args pa{(const float*)v.X, v.ldx, v.T * v.ldx, (int32_t)v.B, (int32_t)v.T, (int32_t)v.m,
-                    0, k, k, nullptr, 0, 0, zb, Y};
+  hipError_t e = hipSuccess;
+  if (!gauss && (e = traced(DPRC_KERNEL_PROBE_BITS, st, [&] { return launch_probe_bits(probe, k0, k1, v.layer_id, 0, v.m, k, zb, st); })) != hipSuccess)
+    return DPRC_ERROR_HIP;
+  ProjectF32Args pa = gauss
+      ? ProjectF32Args{(const float*)v.X, v.ldx, v.T * v.ldx, (int32_t)v.B, (int32_t)v.T, (int32_t)v.m,
+                       k, 0, k, g.f32, g.ld, 0, nullptr, Y}
+      : ProjectF32Args{(const float*)v.X, v.ldx, v.T * v.ldx, (int32_t)v.B, (int32_t)v.T, (int32_t)v.m,
+                       0, k, k, nullptr, 0, 0, zb, Y};
   if ((e = traced(DPRC_KERNEL_PROJECT_F32, st, [&] { return launch_project_f32(pa, st); })) != hipSuccess) return DPRC_ERROR_HIP;
   TokredF32Args ta{(const float*)v.Xo, v.ldo, v.T * v.ldo, (int32_t)v.B, (int32_t)v.T, (int32_t)v.n, Y, k,
                    M, v.n, (int64_t)k * v.n};
@@ -474,10 +512,13 @@ dprc_status dprc_trace_launches(hipEvent_t* events, int32_t* kinds, int32_t capa
   return DPRC_SUCCESS;
 }
 
-size_t dprc_norm_hutch_workspace(const dprc_layer* layers, int32_t num_layers, int32_t k, dprc_side side) {
+size_t dprc_norm_hutch_workspace(const dprc_layer* layers, int32_t num_layers, int32_t k, dprc_probe probe,
+                                 dprc_side side) {
   if (check_layers(layers, num_layers, side) != DPRC_SUCCESS || k < 1 || k > 256) return 0;
+  if (probe != DPRC_PROBE_RADEMACHER && probe != DPRC_PROBE_HADAMARD && probe != DPRC_PROBE_GAUSSIAN) return 0;
+  if (probe == DPRC_PROBE_GAUSSIAN && k > kMaxGaussK) return 0;
   size_t need = 0;
-  for (int32_t l = 0; l < num_layers; ++l) need = std::max(need, hutch_layer_ws(view_of(layers[l], side), k));
+  for (int32_t l = 0; l < num_layers; ++l) need = std::max(need, hutch_layer_ws(view_of(layers[l], side), k, (int)probe));
   return need;
 }
 
@@ -487,8 +528,10 @@ dprc_status dprc_norm_hutch(const dprc_layer* layers, int32_t num_layers, int32_
   dprc_status s = check_layers(layers, num_layers, side);
   if (s != DPRC_SUCCESS) return s;
   if (k < 1 || k > 256 || !n2) return DPRC_ERROR_INVALID_VALUE;
-  if (probe != DPRC_PROBE_RADEMACHER && probe != DPRC_PROBE_HADAMARD) return DPRC_ERROR_INVALID_VALUE;
-  const size_t need = dprc_norm_hutch_workspace(layers, num_layers, k, side);
+  if (probe != DPRC_PROBE_RADEMACHER && probe != DPRC_PROBE_HADAMARD && probe != DPRC_PROBE_GAUSSIAN)
+    return DPRC_ERROR_INVALID_VALUE;
+  if (probe == DPRC_PROBE_GAUSSIAN && k > kMaxGaussK) return DPRC_ERROR_NOT_SUPPORTED;
+  const size_t need = dprc_norm_hutch_workspace(layers, num_layers, k, probe, side);
   if (ws_bytes < need) return DPRC_ERROR_WORKSPACE_TOO_SMALL;
   if (!ws || !aligned(ws, kAlign)) return DPRC_ERROR_INVALID_VALUE;
   uint32_t k0, k1;
@@ -601,6 +644,16 @@ dprc_status dprc_probe_bits(dprc_probe probe, uint64_t seed, uint32_t layer_id, 
   uint32_t k0, k1;
   key_of(seed, k0, k1);
   return hip_status(traced(DPRC_KERNEL_PROBE_BITS, stream, [&] { return launch_probe_bits((int)probe, k0, k1, layer_id, stream_id, m, k, out, stream); }));
+}
+
+dprc_status dprc_probe_gaussian(uint64_t seed, uint32_t layer_id, int64_t m, int32_t k, float* out,
+                                hipStream_t stream) {
+  if (!out || m < 1 || k < 1 || k > 256 || m > (1LL << 36)) return DPRC_ERROR_INVALID_VALUE;
+  if (!aligned(out, 4)) return DPRC_ERROR_INVALID_VALUE;
+  uint32_t k0, k1;
+  key_of(seed, k0, k1);
+  return hip_status(traced(DPRC_KERNEL_PROBE_GAUSS, stream, [&] {
+    return launch_gauss_probe(k0, k1, layer_id, m, k, m, nullptr, nullptr, out, stream); }));
 }
 
 }  // extern "C"

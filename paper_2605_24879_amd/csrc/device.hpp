@@ -44,7 +44,7 @@ __device__ __forceinline__ u32x4 philox4x32_10(u32x4 c, uint32_t k0, uint32_t k1
   return c;
 }
 
-enum : uint32_t { kStreamProbe = 0, kStreamSketch = 1, kStreamNoise = 2 };
+enum : uint32_t { kStreamProbe = 0, kStreamSketch = 1, kStreamNoise = 2, kStreamGaussProbe = 3 };
 enum : int { kProbeRademacher = 0, kProbeHadamard = 1 };
 
 // Four consecutive probe words (rows 128*blk .. 128*blk+127) of column j.
@@ -170,6 +170,18 @@ __device__ __forceinline__ uint4 make_u4(uint2 a, uint2 b) { return uint4{a.x, a
 // their stack addresses)
 __device__ __forceinline__ uint4 select4(bool c, const uint4& a, const uint4& b) {
   return uint4{c ? a.x : b.x, c ? a.y : b.y, c ? a.z : b.z, c ? a.w : b.w};
+}
+
+// Two standard normals from two Philox words (Box-Muller): uniforms
+// (floor(x / 2^9) + 1/2) * 2^-23, exact in fp32 and never 0 or 1.
+__device__ __forceinline__ void box_muller(uint32_t x0, uint32_t x1, float& n0, float& n1) {
+  const float u1 = ((float)(x0 >> 9) + 0.5f) * 0x1p-23f;
+  const float u2 = ((float)(x1 >> 9) + 0.5f) * 0x1p-23f;
+  const float r = sqrtf(-2.f * logf(u1));
+  float sn, cs;
+  sincospif(2.f * u2, &sn, &cs);
+  n0 = r * cs;
+  n1 = r * sn;
 }
 
 __device__ __forceinline__ float wave_sum(float v) {

@@ -75,18 +75,7 @@ hipError_t launch_gemm_f32(const float* A, int64_t lda, int64_t a_ss, const floa
 }
 
 // ---- Gaussian noise ----------------------------------------------------------------------------
-// Element e: Philox block e/4 of stream 2 keyed by (seed, tensor); Box-Muller on
-// word pairs with uniforms (floor(x / 2^9) + 1/2) * 2^-23, exact in fp32.
-__device__ __forceinline__ void box_muller(uint32_t x0, uint32_t x1, float& n0, float& n1) {
-  const float u1 = ((float)(x0 >> 9) + 0.5f) * 0x1p-23f;
-  const float u2 = ((float)(x1 >> 9) + 0.5f) * 0x1p-23f;
-  const float r = sqrtf(-2.f * logf(u1));
-  float sn, cs;
-  sincospif(2.f * u2, &sn, &cs);
-  n0 = r * cs;
-  n1 = r * sn;
-}
-
+// Element e: Philox block e/4 of stream 2 keyed by (seed, tensor), through box_muller.
 __global__ void noise_kernel(float* g, int64_t numel, float scale, uint32_t key0, uint32_t key1,
                              uint32_t tensor_id) {
   const int64_t nq = (numel + 3) >> 2;

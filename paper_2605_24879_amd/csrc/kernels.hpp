@@ -179,6 +179,10 @@ int32_t final_chunks(int64_t n);
 hipError_t launch_probe_bits(int probe_kind, uint32_t key0, uint32_t key1, uint32_t layer,
                              uint32_t stream_id, int64_t m, int32_t k, uint32_t* out,
                              hipStream_t st);
+// Gaussian probe columns, column j at [j*ld .. j*ld + ld) (rows >= m zero);
+// any of hi/lo (both or neither) and f32 may be null.
+hipError_t launch_gauss_probe(uint32_t key0, uint32_t key1, uint32_t layer, int64_t m, int32_t k, int64_t ld,
+                              uint16_t* hi, uint16_t* lo, float* f32, hipStream_t st);
 hipError_t launch_fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t st);
 hipError_t launch_project(const ProjectArgs& a, int rows_per_wg, hipStream_t st);
 hipError_t launch_tokred(const TokredArgs& a, hipStream_t st);

@@ -19,12 +19,12 @@ LIB_PATH = os.path.join(_HERE, "libdprc.so")
 SUCCESS = 0
 F32, BF16 = 0, 1
 SIDE_OUT, SIDE_IN, SIDE_AUTO = 0, 1, 2
-PROBE_RADEMACHER, PROBE_HADAMARD = 0, 1
+PROBE_RADEMACHER, PROBE_HADAMARD, PROBE_GAUSSIAN = 0, 1, 2
 STREAM_PROBE, STREAM_SKETCH, STREAM_NOISE = 0, 1, 2
 
 EXPORTS = ["dprc_norm_hutch_workspace", "dprc_norm_hutch", "dprc_norm_hutchpp_workspace",
            "dprc_norm_hutchpp", "dprc_clip_scale", "dprc_clip_accumulate_workspace",
-           "dprc_clip_accumulate", "dprc_add_noise", "dprc_probe_bits", "dprc_status_string",
+           "dprc_clip_accumulate", "dprc_add_noise", "dprc_probe_bits", "dprc_probe_gaussian", "dprc_status_string",
            "dprc_version", "dprc_trace_launches"]
 
 
@@ -50,7 +50,7 @@ def lib():
                                          ctypes.c_uint64, ctypes.c_float, ctypes.c_size_t)
         LP = ctypes.POINTER(Layer)
         sig = {
-            "dprc_norm_hutch_workspace": (SZ, [LP, I32, I32, ctypes.c_int]),
+            "dprc_norm_hutch_workspace": (SZ, [LP, I32, I32, ctypes.c_int, ctypes.c_int]),
             "dprc_norm_hutch": (ctypes.c_int, [LP, I32, I32, ctypes.c_int, U64, ctypes.c_int, P, P, I32, P, SZ, P]),
             "dprc_norm_hutchpp_workspace": (SZ, [LP, I32, I32, I32, ctypes.c_int]),
             "dprc_norm_hutchpp": (ctypes.c_int, [LP, I32, I32, I32, U64, ctypes.c_int, P, P, I32, P, SZ, P]),
@@ -59,6 +59,7 @@ def lib():
             "dprc_clip_accumulate": (ctypes.c_int, [LP, P, P, I64, I32, P, SZ, P]),
             "dprc_add_noise": (ctypes.c_int, [P, I64, F, F, U64, U32, P]),
             "dprc_probe_bits": (ctypes.c_int, [ctypes.c_int, U64, U32, U32, I64, I32, P, P]),
+            "dprc_probe_gaussian": (ctypes.c_int, [U64, U32, I64, I32, P, P]),
             "dprc_status_string": (ctypes.c_char_p, [ctypes.c_int]),
             "dprc_version": (ctypes.c_char_p, []),
             "dprc_trace_launches": (ctypes.c_int, [P, P, I32, P]),
@@ -120,9 +121,9 @@ def _workspace(nbytes, dev, ws):
     return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=dev)
 
 
-def dprc_norm_hutch_workspace(pairs, k, side=SIDE_OUT):
+def dprc_norm_hutch_workspace(pairs, k, side=SIDE_OUT, probe=PROBE_RADEMACHER):
     arr, nl, _, _ = _layers(pairs)
-    return lib().dprc_norm_hutch_workspace(arr, nl, k, side)
+    return lib().dprc_norm_hutch_workspace(arr, nl, k, probe, side)
 
 
 def dprc_norm_hutch(pairs, k, seed, side=SIDE_OUT, probe=PROBE_RADEMACHER, n2=None, n2_layers=None,
@@ -131,7 +132,7 @@ def dprc_norm_hutch(pairs, k, seed, side=SIDE_OUT, probe=PROBE_RADEMACHER, n2=No
     arr, nl, B, dev = _layers(pairs)
     if n2 is None:
         n2 = torch.zeros(B, dtype=torch.float32, device=dev)
-    need = lib().dprc_norm_hutch_workspace(arr, nl, k, side)
+    need = lib().dprc_norm_hutch_workspace(arr, nl, k, probe, side)
     ws = _workspace(need, dev, ws)
     _check(lib().dprc_norm_hutch(arr, nl, k, probe, seed, side, n2.data_ptr(),
                                  n2_layers.data_ptr() if n2_layers is not None else None,
@@ -201,6 +202,14 @@ def dprc_probe_bits(probe, seed, layer_id, stream_id, m, k, device="cuda", out=N
     return out
 
 
+def dprc_probe_gaussian(seed, layer_id, m, k, device="cuda", out=None):
+    """Gaussian probe values [k, m] (fp32): out[j, u] = probe entry (u, j)."""
+    if out is None:
+        out = torch.empty(k, m, dtype=torch.float32, device=device)
+    _check(lib().dprc_probe_gaussian(seed, layer_id, m, k, out.data_ptr(), _stream(out.device)))
+    return out
+
+
 def dprc_version():
     return lib().dprc_version().decode()
 
@@ -208,7 +217,8 @@ def dprc_version():
 KERNEL_NAMES = {1: "project", 2: "token_reduce", 3: "qr", 4: "hutchpp_final", 5: "clip_scale",
                 6: "accumulate", 7: "splitk_reduce", 8: "noise", 9: "probe_bits", 10: "project_f32",
                 11: "token_reduce_f32", 12: "sample_sq", 13: "accumulate_f32",
-                14: "token_splits", 15: "sample_sum", 16: "qr_combine", 17: "qr_expand", 18: "hutchpp_sum"}
+                14: "token_splits", 15: "sample_sum", 16: "qr_combine", 17: "qr_expand", 18: "hutchpp_sum",
+                19: "probe_gauss"}
 
 
 def dprc_trace_launches(events_ptr, kinds_ptr, capacity, count_ptr):

@@ -116,6 +116,22 @@ def test_q_proj_full(D):
     _free()
 
 
+def test_q_proj_full_gaussian_probes(D):
+    # the q_proj workload with Gaussian probes (k = 16 dense columns), sampled samples
+    cfg = workloads.BY_NAME["q_proj"]
+    pairs = _inputs(cfg)
+    n2 = D.dprc_norm_hutch(pairs, cfg["k"], 5, probe=D.PROBE_GAUSSIAN)
+    torch.cuda.synchronize()
+    A, E, li = pairs[0]
+    Z = philox.gaussian_probe_matrix(5, li, E.shape[2], cfg["k"])
+    got = n2.cpu().numpy()
+    for i in (0, cfg["B"] // 2, cfg["B"] - 1):
+        ref = est.hutch_sample_projected(_np(A[i]), _np(E[i]), Z)
+        assert _rel(got[i], ref) < NORM_RTOL
+    del pairs, A, E
+    _free()
+
+
 def test_mlp_full(D):
     cfg = workloads.BY_NAME["mlp"]
     pairs = _inputs(cfg)

@@ -71,6 +71,16 @@ def test_hadamard_bits_bitexact(D, m, k):
     assert np.array_equal(got, _hadamard_words(m, k))
 
 
+@pytest.mark.parametrize("seed,layer,m,k", [
+    (0, 0, 48, 4), (7, 3, 130, 33), (2**64 - 1, 2**32 - 1, 1, 1), (11, 5, 4097, 2)])
+def test_gaussian_probe_values(D, seed, layer, m, k):
+    # fp32 Box-Muller on the GPU against the fp64 transform of the same Philox words
+    got = D.dprc_probe_gaussian(seed, layer, m, k).cpu().numpy().astype(np.float64).T
+    ref = philox.gaussian_probe_matrix(seed, layer, m, k)
+    assert got.shape == ref.shape
+    assert np.all(np.abs(got - ref) <= 2e-6 * np.maximum(1.0, np.abs(ref)))
+
+
 # ---- Hutchinson ---------------------------------------------------------------------------
 
 @pytest.mark.parametrize("B,T,d,p,k,side", [
@@ -87,6 +97,36 @@ def test_hutch_parity_bf16(D, B, T, d, p, k, side):
     ref = est.hutch_layer(_np(A), _np(E), k, 42, 1, side=side)
     assert np.all(_rel(n2.cpu().numpy(), ref) < NORM_RTOL)
     assert torch.equal(n2, n2l[0])
+
+
+@pytest.mark.parametrize("B,T,d,p,k,side,dtype", [
+    (3, 200, 300, 260, 16, 0, "bf16"),    # ragged tokens / widths
+    (2, 130, 72, 1100, 5, 1, "bf16"),     # side IN, odd k, wide reduced operand
+    (2, 96, 1100, 72, 32, 2, "bf16"),     # AUTO -> IN, 1100 sketched columns (3 stages), k at its maximum
+    (1, 1, 8, 8, 1, 0, "bf16"),           # a single token
+    (2, 64, 64, 48, 4, 0, "f32"),
+    (2, 100, 130, 70, 32, 1, "f32"),
+])
+def test_hutch_gaussian_parity(D, B, T, d, p, k, side, dtype):
+    A, E = _draw(B, T, d, p, dtype=dtype, layer=6)
+    n2 = D.dprc_norm_hutch([(A, E, 4)], k, 77, side=side, probe=D.PROBE_GAUSSIAN)
+    ref = est.hutch_layer(_np(A), _np(E), k, 77, 4, side=side, probe="gaussian")
+    assert np.all(_rel(n2.cpu().numpy(), ref) < NORM_RTOL)
+
+
+def test_hutch_gaussian_multilayer_accumulate(D):
+    # per-layer probes differ (layer id in the counter); the workspace is reused across layers
+    A1, E1 = _draw(2, 300, 256, 200, layer=0)
+    A2, E2 = _draw(2, 150, 136, 700, layer=1)
+    n2 = torch.tensor([0.5, 1.0], device="cuda")
+    n2l = torch.zeros(2, 2, device="cuda")
+    D.dprc_norm_hutch([(A1, E1, 20), (A2, E2, 21)], 8, 3, probe=D.PROBE_GAUSSIAN, n2=n2, n2_layers=n2l,
+                      accumulate=True)
+    r1 = est.hutch_layer(_np(A1), _np(E1), 8, 3, 20, probe="gaussian")
+    r2 = est.hutch_layer(_np(A2), _np(E2), 8, 3, 21, probe="gaussian")
+    got = n2l.cpu().numpy()
+    assert np.all(_rel(got[0], r1) < NORM_RTOL) and np.all(_rel(got[1], r2) < NORM_RTOL)
+    assert np.all(_rel(n2.cpu().numpy(), np.array([0.5, 1.0]) + r1 + r2) < NORM_RTOL)
 
 
 def test_hutch_tiny_workload_fp32(D):

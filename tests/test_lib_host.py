@@ -71,11 +71,33 @@ def test_hutch_argument_validation():
     assert _hutch(_fake_layer(E=0x20003), ws_bytes=1 << 30) == 2
     assert _hutch(_fake_layer(dtype=dprc.F32, A=0x10002), ws_bytes=1 << 30) == 2
     # workspace
-    need = L.dprc_norm_hutch_workspace((dprc.Layer * 1)(_fake_layer()), 1, 4, 0)
+    need = L.dprc_norm_hutch_workspace((dprc.Layer * 1)(_fake_layer()), 1, 4, dprc.PROBE_RADEMACHER, 0)
     assert need > 0
     assert _hutch(_fake_layer(), ws_bytes=need - 1) == 3
     assert _hutch(_fake_layer(), ws=0, ws_bytes=need) == 1
     assert _hutch(_fake_layer(), ws=0x30010, ws_bytes=need) == 1        # not 256-byte aligned
+
+
+def test_gaussian_probe_validation():
+    L = dprc.lib()
+    arr = (dprc.Layer * 1)(_fake_layer())
+    G = dprc.PROBE_GAUSSIAN
+    # Gaussian probes are dense columns: k <= 32, and the workspace holds them
+    assert _hutch(_fake_layer(), k=33, probe=G, ws_bytes=1 << 30) == 2
+    assert L.dprc_norm_hutch_workspace(arr, 1, 33, G, 0) == 0
+    assert L.dprc_norm_hutch_workspace(arr, 1, 4, 9, 0) == 0
+    for dt in (dprc.BF16, dprc.F32):
+        a1 = (dprc.Layer * 1)(_fake_layer(dtype=dt))
+        g = L.dprc_norm_hutch_workspace(a1, 1, 32, G, 0)
+        r = L.dprc_norm_hutch_workspace(a1, 1, 32, dprc.PROBE_RADEMACHER, 0)
+        assert g > r > 0
+        assert _hutch(_fake_layer(dtype=dt), k=32, probe=G, ws_bytes=g - 1) == 3
+    # values export
+    assert L.dprc_probe_gaussian(1, 0, 100, 4, None, None) == 1
+    assert L.dprc_probe_gaussian(1, 0, 0, 4, 0x40000, None) == 1
+    assert L.dprc_probe_gaussian(1, 0, 100, 0, 0x40000, None) == 1
+    assert L.dprc_probe_gaussian(1, 0, 100, 257, 0x40000, None) == 1
+    assert L.dprc_probe_gaussian(1, 0, 100, 4, 0x40002, None) == 1
 
 
 def test_hutchpp_and_accumulate_validation():

@@ -131,7 +131,8 @@ def describe(cfg):
             "layers": [f"{n}:{d}x{p}" for (n, d, p) in cfg["layers"]][:8]
             + ([f"... {len(cfg['layers'])} layers"] if len(cfg["layers"]) > 8 else []),
             "dtype": cfg["dtype"], "estimator": cfg["estimator"],
-            "probes": cfg.get("k", None) if cfg["estimator"] == "hutch" else f"s={cfg['s']},r={cfg['r']}"}
+            "probes": cfg.get("k", None) if cfg["estimator"] == "hutch" else f"s={cfg['s']},r={cfg['r']}"} \
+        | ({"probe_family": cfg.get("probe", "rademacher")} if cfg["estimator"] == "hutch" else {})
 
 
 def ceil_div(a, b):
