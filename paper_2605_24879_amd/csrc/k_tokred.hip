@@ -240,36 +240,59 @@ __global__ __launch_bounds__(kBlock) void tokred_kernel(TokredArgs a) {
 
 // Sum of the token splits of one tile, in split order: its squared norm (mode 0)
 // or the stored tile (mode 1).
+// Sum of the S split partials of one (sample, tile), in split order.  Each thread
+// takes G = 16 / U float4 groups at a time and U splits of each, so 16 loads are
+// in flight whatever S is (split indices past S are clamped to S-1 and not added).
+template <int U>
 __global__ __launch_bounds__(kBlock) void tokred_splits_kernel(TokredArgs a) {
+  constexpr int G = 16 / U;
   __shared__ double dred[4];
   const int tid = threadIdx.x, tile = blockIdx.x, i = blockIdx.y;
   const int64_t tslot = (int64_t)i * a.ntiles + tile;
   const float* tp = a.part + tslot * a.S * (int64_t)a.ncols_pad * kTile;
+  const int64_t sstride = (int64_t)a.ncols_pad * kTile;
+  const int ng = a.ncols_pad * (kTile / 4);
   double sq = 0.0;
-  for (int gi = tid; gi < a.ncols_pad * (kTile / 4); gi += kBlock) {
-    const int c = gi / (kTile / 4), j4 = (gi - c * (kTile / 4)) * 4;
-    float v[4] = {0.f, 0.f, 0.f, 0.f};
-    const float* src = tp + (int64_t)c * kTile + j4;
-    const int64_t sstride = (int64_t)a.ncols_pad * kTile;
-    int s2 = 0;
-    for (; s2 + 8 <= a.S; s2 += 8) {                 // eight loads in flight, summed in split order
-      float4 pv[8];
+  for (int g0 = tid; g0 < ng; g0 += G * kBlock) {
+    float v[G][4];
+    const float* src[G];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) pv[u] = *reinterpret_cast<const float4*>(src + (s2 + u) * sstride);
+    for (int q = 0; q < G; ++q) {
+      const int gi = g0 + q * kBlock < ng ? g0 + q * kBlock : g0;
+      const int c = gi / (kTile / 4), j4 = (gi - c * (kTile / 4)) * 4;
+      src[q] = tp + (int64_t)c * kTile + j4;
+      v[q][0] = v[q][1] = v[q][2] = v[q][3] = 0.f;
+    }
+    for (int s0 = 0; s0 < a.S; s0 += U) {
+      float4 pv[G][U];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        v[0] += pv[u].x; v[1] += pv[u].y; v[2] += pv[u].z; v[3] += pv[u].w;
+      for (int q = 0; q < G; ++q)
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int s2 = s0 + u < a.S ? s0 + u : a.S - 1;
+          pv[q][u] = *reinterpret_cast<const float4*>(src[q] + s2 * sstride);
+        }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const bool use = s0 + u < a.S;          // adding 0 to a sum leaves it unchanged
+#pragma unroll
+        for (int q = 0; q < G; ++q) {
+          v[q][0] += use ? pv[q][u].x : 0.f; v[q][1] += use ? pv[q][u].y : 0.f;
+          v[q][2] += use ? pv[q][u].z : 0.f; v[q][3] += use ? pv[q][u].w : 0.f;
+        }
       }
     }
-    for (; s2 < a.S; ++s2) {
-      const float4 pv = *reinterpret_cast<const float4*>(src + s2 * sstride);
-      v[0] += pv.x; v[1] += pv.y; v[2] += pv.z; v[3] += pv.w;
-    }
-    if (a.mode == 0) {
-      if (c < a.ncols)
-        for (int q = 0; q < 4; ++q) sq += (double)(v[q] * v[q]);
-    } else {
-      store4(a, i, c, tile * kTile + j4, v);
+#pragma unroll
+    for (int q = 0; q < G; ++q) {
+      const int gi = g0 + q * kBlock;
+      if (gi >= ng) break;
+      const int c = gi / (kTile / 4), j4 = (gi - c * (kTile / 4)) * 4;
+      if (a.mode == 0) {
+        if (c < a.ncols)
+          for (int e = 0; e < 4; ++e) sq += (double)(v[q][e] * v[q][e]);
+      } else {
+        store4(a, i, c, tile * kTile + j4, v[q]);
+      }
     }
   }
   if (a.mode == 0) {
@@ -293,7 +316,10 @@ __global__ __launch_bounds__(kBlock) void tokred_sample_kernel(TokredArgs a) {
 }
 
 hipError_t launch_tokred_splits(const TokredArgs& a, hipStream_t st) {
-  DPRC_LAUNCH(tokred_splits_kernel, dim3((unsigned)a.ntiles, (unsigned)a.B), dim3(kBlock), 0, st, a);
+  const dim3 grid((unsigned)a.ntiles, (unsigned)a.B);
+  if (a.S <= 2) DPRC_LAUNCH(tokred_splits_kernel<2>, grid, dim3(kBlock), 0, st, a);
+  else if (a.S <= 4) DPRC_LAUNCH(tokred_splits_kernel<4>, grid, dim3(kBlock), 0, st, a);
+  else DPRC_LAUNCH(tokred_splits_kernel<8>, grid, dim3(kBlock), 0, st, a);
   return hipGetLastError();
 }
 
