@@ -138,10 +138,10 @@ struct TokBufs {
   double* tilesq;
 };
 
-TokBufs take_tok(Arena& ar, int64_t B, const TokPlan& tp, int ncols_pad) {
+TokBufs take_tok(Arena& ar, int64_t B, const TokPlan& tp, int ncols_pad, int nseg = 1) {
   TokBufs b;
   b.part = tp.S > 1 ? ar.take<float>((size_t)B * tp.ntiles * tp.S * ncols_pad * kTile) : nullptr;
-  b.tilesq = ar.take<double>((size_t)B * tp.ntiles);
+  b.tilesq = ar.take<double>((size_t)nseg * B * tp.ntiles);
   return b;
 }
 
@@ -184,10 +184,10 @@ struct PassSpec {
 };
 
 size_t pass_ws(Arena& ar, int64_t B, int64_t T, int64_t n, int ncols_pad, uint16_t** Yt, TokBufs* tb,
-               TokPlan* tpo) {
+               TokPlan* tpo, int nseg = 1) {
   const TokPlan tp = tok_plan(B, T, n);
   uint16_t* y = ar.take<uint16_t>((size_t)2 * ncols_pad * B * tp.T_pad);
-  TokBufs t = take_tok(ar, B, tp, ncols_pad);
+  TokBufs t = take_tok(ar, B, tp, ncols_pad, nseg);
   if (Yt) *Yt = y;
   if (tb) *tb = t;
   if (tpo) *tpo = tp;
@@ -212,6 +212,7 @@ dprc_status run_pass(const PassSpec& ps, int64_t B, int64_t T, uint32_t k0, uint
   pa.probe_kind = ps.probe_kind; pa.key0 = k0; pa.key1 = k1; pa.layer_id = layer; pa.stream_id = ps.stream_id;
   pa.words_per_chunk = words_per_chunk(ps.m, ps.nz);
   pa.Yt = Yt; pa.yt_ld = B * tp.T_pad;
+  pa.ylo_off = (int64_t)ncols_pad * pa.yt_ld; pa.ncols_write = ncols_pad;
   pa.zero_ptr = nullptr; pa.zero_count = 0;
   pa.vec = rows16(ps.X, ps.ldx);
   hipError_t e = traced(DPRC_KERNEL_PROJECT, st, [&] { return launch_project(pa, rows_per_wg(B * tp.T_pad, ncols_pad), st); });
@@ -222,7 +223,7 @@ dprc_status run_pass(const PassSpec& ps, int64_t B, int64_t T, uint32_t k0, uint
   ta.B = (int32_t)B; ta.T = (int32_t)T; ta.n = (int32_t)ps.n;
   ta.Yt = Yt; ta.yt_ld = B * tp.T_pad; ta.T_pad = tp.T_pad; ta.ncols = ncols; ta.ncols_pad = ncols_pad;
   ta.ntiles = tp.ntiles; ta.S = tp.S; ta.stages_per_split = tp.sps;
-  ta.mode = ps.mode;
+  ta.mode = ps.mode; ta.seg = ncols; ta.nseg = 1;
   ta.part = tb.part; ta.tilesq = tb.tilesq;
   ta.scale = ps.scale; ta.n2 = ps.n2; ta.n2_layer = ps.n2_layer; ta.accumulate = ps.accumulate;
   ta.M = ps.M; ta.m_ld = ps.m_ld; ta.m_ss = (int64_t)ncols * ps.m_ld;
@@ -264,43 +265,60 @@ GaussBufs take_gauss(Arena& ar, const View& v, int32_t k) {
   return g;
 }
 
-size_t hutch_layer_ws(const View& v, int32_t k, int probe) {
+// Consecutive bf16 layers that read the same activations (same A, shape and row
+// stride) and sketch the output side share one token reduction over A: each
+// layer's Y = E Z fills k columns of one Y, and the reduction squares each
+// layer's columns separately (q, k, v of an attention block; gate and up).
+int32_t group_end(const dprc_layer* layers, int32_t l0, int32_t num_layers, int32_t k, dprc_side side) {
+  const dprc_layer& L = layers[l0];
+  if (L.dtype != DPRC_BF16 || resolve(L, side) != DPRC_SIDE_OUT) return l0 + 1;
+  int32_t l = l0 + 1;
+  while (l < num_layers && l - l0 < kMaxGroup && (int64_t)(l - l0 + 1) * k <= 256) {
+    const dprc_layer& M = layers[l];
+    if (M.A != L.A || M.lda != L.lda || M.d != L.d || M.B != L.B || M.T != L.T || M.dtype != L.dtype ||
+        resolve(M, side) != DPRC_SIDE_OUT)
+      break;
+    ++l;
+  }
+  return l;
+}
+
+int64_t max_m(const View* v, int G) {
+  int64_t m = 0;
+  for (int l = 0; l < G; ++l) m = std::max(m, v[l].m);
+  return m;
+}
+
+size_t hutch_group_ws(const View* v, int G, int32_t k, int probe) {
   Arena ar(nullptr);
-  if (probe == DPRC_PROBE_GAUSSIAN) take_gauss(ar, v, k);
-  if (v.dtype == DPRC_BF16) return round_up((int64_t)ar.off, kAlign) + pass_ws_bytes(v.B, v.T, v.n, k);
-  if (probe != DPRC_PROBE_GAUSSIAN) ar.take<uint32_t>((size_t)k * ceil_div(v.m, 32));
-  ar.take<float>((size_t)v.B * v.T * k);
-  ar.take<float>((size_t)v.B * k * v.n);
+  View vm = v[0];
+  vm.m = max_m(v, G);
+  if (probe == DPRC_PROBE_GAUSSIAN) take_gauss(ar, vm, k);
+  if (v[0].dtype == DPRC_BF16) {
+    pass_ws(ar, v[0].B, v[0].T, v[0].n, pad_cols(G * k), nullptr, nullptr, nullptr, G);
+    return ar.off;
+  }
+  if (probe != DPRC_PROBE_GAUSSIAN) ar.take<uint32_t>((size_t)k * ceil_div(v[0].m, 32));
+  ar.take<float>((size_t)v[0].B * v[0].T * k);
+  ar.take<float>((size_t)v[0].B * k * v[0].n);
   return ar.off;
 }
 
-dprc_status hutch_layer(const View& v, int32_t k, int probe, uint32_t k0, uint32_t k1, float* n2,
-                        float* n2_layer, int accumulate, void* ws, hipStream_t st) {
+dprc_status hutch_f32(const View& v, int32_t k, int probe, uint32_t k0, uint32_t k1, float* n2,
+                      float* n2_layer, int accumulate, void* ws, hipStream_t st) {
   const bool gauss = probe == DPRC_PROBE_GAUSSIAN;
   Arena ar(ws);
   GaussBufs g{};
+  hipError_t e = hipSuccess;
   if (gauss) {
     g = take_gauss(ar, v, k);
-    hipError_t e = traced(DPRC_KERNEL_PROBE_GAUSS, st, [&] {
-      return launch_gauss_probe(k0, k1, v.layer_id, v.m, k, g.ld, g.hi, g.lo, g.f32, st); });
-    if (e != hipSuccess) return DPRC_ERROR_HIP;
-  }
-  if (v.dtype == DPRC_BF16) {
-    PassSpec ps{};
-    ps.X = (const uint16_t*)v.X; ps.ldx = v.ldx; ps.m = v.m;
-    ps.Xo = (const uint16_t*)v.Xo; ps.ldo = v.ldo; ps.n = v.n;
-    if (gauss) {
-      ps.nd = k; ps.Rhi = g.hi; ps.Rlo = g.lo; ps.ld_r = g.ld; ps.shared_r = true; ps.nz = 0;
-    } else {
-      ps.nd = 0; ps.nz = k; ps.stream_id = 0; ps.probe_kind = probe;
-    }
-    ps.mode = 0; ps.scale = 1.0f / (float)k; ps.n2 = n2; ps.n2_layer = n2_layer; ps.accumulate = accumulate;
-    return run_pass(ps, v.B, v.T, k0, k1, v.layer_id, ar.take<char>(0), st);
+    if ((e = traced(DPRC_KERNEL_PROBE_GAUSS, st, [&] {
+           return launch_gauss_probe(k0, k1, v.layer_id, v.m, k, g.ld, nullptr, nullptr, g.f32, st); })) != hipSuccess)
+      return DPRC_ERROR_HIP;
   }
   uint32_t* zb = gauss ? nullptr : ar.take<uint32_t>((size_t)k * ceil_div(v.m, 32));
   float* Y = ar.take<float>((size_t)v.B * v.T * k);
   float* M = ar.take<float>((size_t)v.B * k * v.n);
-  hipError_t e = hipSuccess;
   if (!gauss && (e = traced(DPRC_KERNEL_PROBE_BITS, st, [&] { return launch_probe_bits(probe, k0, k1, v.layer_id, 0, v.m, k, zb, st); })) != hipSuccess)
     return DPRC_ERROR_HIP;
   ProjectF32Args pa = gauss
@@ -314,6 +332,60 @@ dprc_status hutch_layer(const View& v, int32_t k, int probe, uint32_t k0, uint32
   if ((e = traced(DPRC_KERNEL_TOKEN_REDUCE_F32, st, [&] { return launch_tokred_f32(ta, st); })) != hipSuccess) return DPRC_ERROR_HIP;
   return hip_status(traced(DPRC_KERNEL_SAMPLE_SQ, st, [&] { return launch_sample_sq(M, v.n, (int64_t)k * v.n, (int32_t)v.B, k, (int32_t)v.n,
                                      1.0f / (float)k, n2, n2_layer, accumulate, st); }));
+}
+
+// G layers (G = 1, or a shared-activation group of bf16 OUT layers): one projection
+// per layer into its columns of a shared Y, then one token reduction.
+dprc_status hutch_group(const View* v, int G, int32_t k, int probe, uint32_t k0, uint32_t k1, float* n2,
+                        float* n2_layers, int accumulate, void* ws, hipStream_t st) {
+  if (v[0].dtype != DPRC_BF16) return hutch_f32(v[0], k, probe, k0, k1, n2, n2_layers, accumulate, ws, st);
+  const bool gauss = probe == DPRC_PROBE_GAUSSIAN;
+  const int64_t B = v[0].B, T = v[0].T;
+  Arena ar(ws);
+  View vm = v[0];
+  vm.m = max_m(v, G);
+  GaussBufs gz = gauss ? take_gauss(ar, vm, k) : GaussBufs{};
+  const int ncols = G * k, ncols_pad = pad_cols(ncols);
+  uint16_t* Yt;
+  TokBufs tb;
+  TokPlan tp;
+  pass_ws(ar, B, T, v[0].n, ncols_pad, &Yt, &tb, &tp, G);
+  const int64_t yt_ld = B * tp.T_pad;
+  hipError_t e = hipSuccess;
+  for (int l = 0; l < G; ++l) {
+    const View& w = v[l];
+    const int64_t ldz = round_up(w.m, kTile);
+    if (gauss && (e = traced(DPRC_KERNEL_PROBE_GAUSS, st, [&] {
+                    return launch_gauss_probe(k0, k1, w.layer_id, w.m, k, ldz, gz.hi, gz.lo, nullptr, st); })) != hipSuccess)
+      return DPRC_ERROR_HIP;
+    ProjectArgs pa;
+    pa.X = (const uint16_t*)w.X; pa.ldx = w.ldx; pa.x_ss = T * w.ldx;
+    pa.B = (int32_t)B; pa.T = (int32_t)T; pa.m = (int32_t)w.m; pa.T_pad = tp.T_pad;
+    pa.nd = gauss ? k : 0; pa.nz = gauss ? 0 : k; pa.ncols_pad = pad_cols(k);
+    pa.Rhi = gz.hi; pa.Rlo = gz.lo; pa.ld_r = gauss ? ldz : 0; pa.r_ss = 0;
+    pa.probe_kind = probe; pa.key0 = k0; pa.key1 = k1; pa.layer_id = w.layer_id; pa.stream_id = 0;
+    pa.words_per_chunk = words_per_chunk(w.m, pa.nz);
+    pa.Yt = Yt + (int64_t)l * k * yt_ld; pa.yt_ld = yt_ld;
+    pa.ylo_off = (int64_t)ncols_pad * yt_ld;
+    pa.ncols_write = G == 1 ? pa.ncols_pad : k;   // inside a shared Y only the layer's own columns
+    pa.zero_ptr = nullptr; pa.zero_count = 0;
+    pa.vec = rows16(w.X, w.ldx);
+    if ((e = traced(DPRC_KERNEL_PROJECT, st, [&] { return launch_project(pa, rows_per_wg(B * tp.T_pad, pa.ncols_pad), st); })) != hipSuccess)
+      return DPRC_ERROR_HIP;
+  }
+  TokredArgs ta{};
+  ta.X = (const uint16_t*)v[0].Xo; ta.ldx = v[0].ldo; ta.x_ss = T * v[0].ldo;
+  ta.B = (int32_t)B; ta.T = (int32_t)T; ta.n = (int32_t)v[0].n;
+  ta.Yt = Yt; ta.yt_ld = yt_ld; ta.T_pad = tp.T_pad; ta.ncols = ncols; ta.ncols_pad = ncols_pad;
+  ta.ntiles = tp.ntiles; ta.S = tp.S; ta.stages_per_split = tp.sps;
+  ta.mode = 0; ta.seg = k; ta.nseg = G;
+  ta.part = tb.part; ta.tilesq = tb.tilesq;
+  ta.scale = 1.0f / (float)k; ta.n2 = n2; ta.n2_layer = n2_layers; ta.accumulate = accumulate;
+  ta.vec = rows16(v[0].Xo, v[0].ldo);
+  if ((e = traced(DPRC_KERNEL_TOKEN_REDUCE, st, [&] { return launch_tokred(ta, st); })) != hipSuccess) return DPRC_ERROR_HIP;
+  if (tp.S > 1 && (e = traced(DPRC_KERNEL_TOKEN_SPLITS, st, [&] { return launch_tokred_splits(ta, st); })) != hipSuccess)
+    return DPRC_ERROR_HIP;
+  return hip_status(traced(DPRC_KERNEL_SAMPLE_SUM, st, [&] { return launch_tokred_sample(ta, st); }));
 }
 
 // ---- Hutch++ -------------------------------------------------------------------------------------
@@ -518,7 +590,13 @@ size_t dprc_norm_hutch_workspace(const dprc_layer* layers, int32_t num_layers, i
   if (probe != DPRC_PROBE_RADEMACHER && probe != DPRC_PROBE_HADAMARD && probe != DPRC_PROBE_GAUSSIAN) return 0;
   if (probe == DPRC_PROBE_GAUSSIAN && k > kMaxGaussK) return 0;
   size_t need = 0;
-  for (int32_t l = 0; l < num_layers; ++l) need = std::max(need, hutch_layer_ws(view_of(layers[l], side), k, (int)probe));
+  View v[kMaxGroup];
+  for (int32_t l = 0; l < num_layers;) {
+    const int32_t le = group_end(layers, l, num_layers, k, side);
+    for (int32_t j = l; j < le; ++j) v[j - l] = view_of(layers[j], side);
+    need = std::max(need, hutch_group_ws(v, le - l, k, (int)probe));
+    l = le;
+  }
   return need;
 }
 
@@ -537,10 +615,14 @@ dprc_status dprc_norm_hutch(const dprc_layer* layers, int32_t num_layers, int32_
   uint32_t k0, k1;
   key_of(seed, k0, k1);
   const int64_t B = layers[0].B;
-  for (int32_t l = 0; l < num_layers; ++l) {
-    s = hutch_layer(view_of(layers[l], side), k, (int)probe, k0, k1, n2,
-                    n2_layers ? n2_layers + (int64_t)l * B : nullptr, (accumulate || l > 0) ? 1 : 0, ws, stream);
+  View v[kMaxGroup];
+  for (int32_t l = 0; l < num_layers;) {
+    const int32_t le = group_end(layers, l, num_layers, k, side);
+    for (int32_t j = l; j < le; ++j) v[j - l] = view_of(layers[j], side);
+    s = hutch_group(v, le - l, k, (int)probe, k0, k1, n2, n2_layers ? n2_layers + (int64_t)l * B : nullptr,
+                    (accumulate || l > 0) ? 1 : 0, ws, stream);
     if (s != DPRC_SUCCESS) return s;
+    l = le;
   }
   return DPRC_SUCCESS;
 }

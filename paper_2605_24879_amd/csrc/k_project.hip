@@ -246,10 +246,10 @@ __global__ __launch_bounds__(kBlock) void project_kernel(ProjectArgs a) {
   __syncthreads();
   const int rows = 16 * RB;
   uint16_t* yhi = a.Yt + (int64_t)i * a.T_pad + t0;
-  uint16_t* ylo = yhi + (int64_t)a.ncols_pad * a.yt_ld;
+  uint16_t* ylo = yhi + a.ylo_off;
   for (int idx = tid; idx < rows * 16 * NB; idx += kBlock) {
     const int c = idx / rows, r = idx - c * rows;
-    if (c >= a.ncols_pad) continue;
+    if (c >= a.ncols_write) continue;
     float y = 0.f;
 #pragma unroll
     for (int s = 0; s < 4; ++s) y += red[s * rows * RS + r * RS + c];

@@ -56,6 +56,26 @@ __device__ __forceinline__ void store4(const TokredArgs& a, int i, int c, int j,
   }
 }
 
+// mode 0: adds a squared entry of column c to its layer's sum (columns past
+// ncols, which may hold anything, are left out)
+__device__ __forceinline__ void seg_add(const TokredArgs& a, int c, double v, double (&sq)[kMaxGroup]) {
+  if (c >= a.ncols) return;
+#pragma unroll
+  for (int g = 0; g < kMaxGroup; ++g)
+    if (c >= g * a.seg && c < (g + 1) * a.seg) sq[g] += v;
+}
+
+__device__ __forceinline__ void seg_publish(const TokredArgs& a, int64_t tslot, double (&sq)[kMaxGroup],
+                                            double* dred) {
+  const int64_t lstride = (int64_t)a.B * a.ntiles;
+#pragma unroll
+  for (int g = 0; g < kMaxGroup; ++g) {
+    if (g >= a.nseg) break;
+    const double t = block_sum_d(sq[g], dred);
+    if (threadIdx.x == 0) a.tilesq[g * lstride + tslot] = t;
+  }
+}
+
 template <int V>
 struct Int {
   static constexpr int value = V;
@@ -210,15 +230,16 @@ __global__ __launch_bounds__(kBlock) void tokred_kernel(TokredArgs a) {
   const int64_t tslot = (int64_t)i * a.ntiles + tile;
   if (a.S == 1) {
     if (a.mode == 0) {
-      double sq = 0.0;
+      double sq[kMaxGroup] = {};
 #pragma unroll
       for (int x = 0; x < 2; ++x)
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
+        for (int nb = 0; nb < NB; ++nb) {
+          const int c = 16 * nb + l16;
 #pragma unroll
-          for (int q = 0; q < 4; ++q) sq += (double)(w[x][nb][q] * w[x][nb][q]);
-      sq = block_sum_d(sq, dred);
-      if (tid == 0) a.tilesq[tslot] = sq;
+          for (int q = 0; q < 4; ++q) seg_add(a, c, (double)(w[x][nb][q] * w[x][nb][q]), sq);
+        }
+      seg_publish(a, tslot, sq, dred);
     } else {
 #pragma unroll
       for (int x = 0; x < 2; ++x)
@@ -252,7 +273,7 @@ __global__ __launch_bounds__(kBlock) void tokred_splits_kernel(TokredArgs a) {
   const float* tp = a.part + tslot * a.S * (int64_t)a.ncols_pad * kTile;
   const int64_t sstride = (int64_t)a.ncols_pad * kTile;
   const int ng = a.ncols_pad * (kTile / 4);
-  double sq = 0.0;
+  double sq[kMaxGroup] = {};
   for (int g0 = tid; g0 < ng; g0 += G * kBlock) {
     float v[G][4];
     const float* src[G];
@@ -288,31 +309,31 @@ __global__ __launch_bounds__(kBlock) void tokred_splits_kernel(TokredArgs a) {
       if (gi >= ng) break;
       const int c = gi / (kTile / 4), j4 = (gi - c * (kTile / 4)) * 4;
       if (a.mode == 0) {
-        if (c < a.ncols)
-          for (int e = 0; e < 4; ++e) sq += (double)(v[q][e] * v[q][e]);
+        for (int e = 0; e < 4; ++e) seg_add(a, c, (double)(v[q][e] * v[q][e]), sq);
       } else {
         store4(a, i, c, tile * kTile + j4, v[q]);
       }
     }
   }
-  if (a.mode == 0) {
-    sq = block_sum_d(sq, dred);
-    if (tid == 0) a.tilesq[tslot] = sq;
-  }
+  if (a.mode == 0) seg_publish(a, tslot, sq, dred);
 }
 
-// estimate_i = scale * sum over tiles (in tile order), into n2 and the per-layer copy
+// estimate of layer g for sample i = scale * sum over tiles (in tile order);
+// n2 gets the layers' estimates added one after another, as separate calls would
 __global__ __launch_bounds__(kBlock) void tokred_sample_kernel(TokredArgs a) {
   __shared__ double dred[4];
   const int i = blockIdx.x;
-  double t = 0.0;
-  for (int k = threadIdx.x; k < a.ntiles; k += kBlock) t += a.tilesq[(int64_t)i * a.ntiles + k];
-  t = block_sum_d(t, dred);
-  if (threadIdx.x == 0) {
+  float n2 = a.accumulate ? a.n2[i] : 0.f;
+  for (int g = 0; g < a.nseg; ++g) {
+    const double* ts = a.tilesq + ((int64_t)g * a.B + i) * a.ntiles;
+    double t = 0.0;
+    for (int k = threadIdx.x; k < a.ntiles; k += kBlock) t += ts[k];
+    t = block_sum_d(t, dred);
     const float est = (float)(t * (double)a.scale);
-    a.n2[i] = (a.accumulate ? a.n2[i] : 0.f) + est;
-    if (a.n2_layer) a.n2_layer[i] = est;
+    n2 += est;
+    if (threadIdx.x == 0 && a.n2_layer) a.n2_layer[(int64_t)g * a.B + i] = est;
   }
+  if (threadIdx.x == 0) a.n2[i] = n2;
 }
 
 hipError_t launch_tokred_splits(const TokredArgs& a, hipStream_t st) {

@@ -29,6 +29,7 @@ LaunchEvents& next_launch_events();
 constexpr int kWave = 64;
 constexpr int kBlock = 256;        // threads per workgroup of the streaming kernels
 constexpr int kStage = 64;         // tokens per pipeline stage of the token reduction
+constexpr int kMaxGroup = 4;       // layers sharing one token reduction (same activations)
 constexpr int kTile = 128;         // result rows per token-reduction workgroup
 // Padded LDS row (elements) of a staged 64 x 128 bf16 tile: 288 bytes, so the four
 // rows of one 16-lane transpose read start 32 bytes apart; rows with bit 3 set are
@@ -56,8 +57,10 @@ struct ProjectArgs {
   int32_t probe_kind;
   uint32_t key0, key1, layer_id, stream_id;
   int32_t words_per_chunk;  // probe words per column staged in LDS at a time
-  uint16_t* Yt;
+  uint16_t* Yt;             // hi plane: Yt[c*yt_ld + i*T_pad + t]; lo plane at Yt + ylo_off
   int64_t yt_ld;            // B * T_pad
+  int64_t ylo_off;
+  int32_t ncols_write;      // columns written (ncols_pad, or only the real ones inside a shared Y)
   uint32_t* zero_ptr;       // counters cleared by workgroup (0,0) (may be null)
   int32_t zero_count;
   int32_t vec;              // token rows of X are 16-byte aligned: 16-byte loads
@@ -75,11 +78,12 @@ struct TokredArgs {
   int32_t T_pad, ncols, ncols_pad;
   int32_t ntiles, S, stages_per_split;
   int32_t mode;
+  int32_t seg, nseg;      // mode 0: columns [g*seg, (g+1)*seg) are layer g of nseg (<= kMaxGroup)
   float* part;            // [B][ntiles][S][ncols_pad][kTile] (S > 1)
-  double* tilesq;         // [B][ntiles] (mode 0)
+  double* tilesq;         // [nseg][B][ntiles] (mode 0)
   float scale;            // estimate = scale * ||M_i||^2
   float* n2;
-  float* n2_layer;
+  float* n2_layer;        // [nseg][B] (may be null)
   int32_t accumulate;
   float* M;               // M[i*m_ss + c*m_ld + j]
   int64_t m_ld, m_ss;

@@ -129,6 +129,54 @@ def test_hutch_gaussian_multilayer_accumulate(D):
     assert np.all(_rel(n2.cpu().numpy(), np.array([0.5, 1.0]) + r1 + r2) < NORM_RTOL)
 
 
+# ---- layers sharing their activations (one token reduction over A) -------------------------
+
+def _shared_a(B, T, d, ps, layer0=0):
+    """Layers that read the same A (as q, k, v do), each with its own E."""
+    A, _ = _draw(B, T, d, 8, layer=layer0)
+    Es = [_draw(B, T, 8, p, layer=layer0 + 1 + j)[1] for j, p in enumerate(ps)]
+    return A, Es
+
+
+@pytest.mark.parametrize("B,T,d,ps,k,probe", [
+    (2, 200, 300, (260, 72, 72), 16, "rademacher"),     # q, k, v-like widths (ragged)
+    (3, 130, 136, (520, 520), 5, "rademacher"),         # gate/up-like pair, k not a multiple of 16
+    (2, 700, 256, (200, 100, 64, 48, 30), 16, "rademacher"),   # five sharing layers -> groups of 4 and 1
+    (2, 96, 64, (128, 40, 72), 100, "rademacher"),      # 3k > 256 columns -> groups of 2 and 1
+    (2, 150, 520, (96, 260), 7, "gaussian"),
+])
+def test_hutch_shared_activations(D, B, T, d, ps, k, probe):
+    A, Es = _shared_a(B, T, d, ps)
+    pairs = [(A, E, 30 + j) for j, E in enumerate(Es)]
+    pid = D.PROBE_GAUSSIAN if probe == "gaussian" else D.PROBE_RADEMACHER
+    n2l = torch.zeros(len(Es), B, device="cuda")
+    n2 = D.dprc_norm_hutch(pairs, k, 8, probe=pid, n2_layers=n2l)
+    refs = [est.hutch_layer(_np(A), _np(E), k, 8, 30 + j, probe=probe) for j, E in enumerate(Es)]
+    got = n2l.cpu().numpy()
+    for j in range(len(Es)):
+        assert np.all(_rel(got[j], refs[j]) < NORM_RTOL), j
+    assert np.all(_rel(n2.cpu().numpy(), np.sum(refs, axis=0)) < NORM_RTOL)
+    # same estimates as with a private copy of A per layer (no shared reduction)
+    n2l_sep = torch.zeros_like(n2l)
+    n2_sep = D.dprc_norm_hutch([(A.clone(), E, 30 + j) for j, E in enumerate(Es)], k, 8, probe=pid,
+                               n2_layers=n2l_sep)
+    assert np.all(_rel(got, n2l_sep.cpu().numpy()) < 1e-6)
+    assert np.all(_rel(n2.cpu().numpy(), n2_sep.cpu().numpy()) < 1e-6)
+    if k % 16 == 0:
+        assert torch.equal(n2l, n2l_sep)
+
+
+def test_hutch_shared_activations_mixed_sides(D):
+    # AUTO: q (d == p) sketches OUT, k/v (d > p) sketch IN; only OUT layers share a reduction
+    A, Es = _shared_a(2, 160, 256, (256, 64, 64))
+    pairs = [(A, E, 40 + j) for j, E in enumerate(Es)]
+    n2l = torch.zeros(3, 2, device="cuda")
+    D.dprc_norm_hutch(pairs, 16, 2, side=2, n2_layers=n2l)
+    for j, E in enumerate(Es):
+        ref = est.hutch_layer(_np(A), _np(E), 16, 2, 40 + j, side=2)
+        assert np.all(_rel(n2l[j].cpu().numpy(), ref) < NORM_RTOL), j
+
+
 def test_hutch_tiny_workload_fp32(D):
     cfg = workloads.BY_NAME["tiny"]
     A, E = workloads.layer_inputs(cfg, 0, device="cuda")
