@@ -230,6 +230,34 @@ def add_noise(grad, sigma, C, seed, tensor_id, start=0):
     return g + sigma * C * xi
 
 
+def private_gradient(A, E, c, sigma, C, seed, tensor_id, batch):
+    """The private gradient of one layer as the optimizer sees it (Algorithm 1):
+    (sum_i c_i G_i + sigma C xi) / batch, the division by the batch size being
+    the optimizer's normalisation."""
+    g = clip_accumulate(A, E, c)
+    if sigma > 0:
+        g = add_noise(g, sigma, C, seed, tensor_id)
+    return g / batch
+
+
+def adamw(theta, grad, m, v, t, lr, beta1, beta2, eps, weight_decay):
+    """One AdamW update (Algorithm 1's optimizer step; AdamW = Adam with decoupled
+    weight decay, Loshchilov and Hutter, which the paper's experiments use).
+
+    theta <- theta (1 - lr wd); m <- beta1 m + (1 - beta1) g;
+    v <- beta2 v + (1 - beta2) g^2; theta <- theta - lr m_hat / (sqrt(v_hat) + eps)
+    with m_hat = m / (1 - beta1^t), v_hat = v / (1 - beta2^t), t the 1-based step.
+    Returns (theta, m, v) in fp64.
+    """
+    theta, g = np.asarray(theta, dtype=np.float64), np.asarray(grad, dtype=np.float64)
+    theta = theta * (1.0 - lr * weight_decay)
+    m = beta1 * m + (1.0 - beta1) * g
+    v = beta2 * v + (1.0 - beta2) * g * g
+    m_hat = m / (1.0 - beta1 ** t)
+    v_hat = v / (1.0 - beta2 ** t)
+    return theta - lr * m_hat / (np.sqrt(v_hat) + eps), m, v
+
+
 # ---- FLOP model of the appendix table (tab:flops_analysis) -----------------
 
 def flops_fgc(B, T, d, p):

@@ -342,3 +342,32 @@ def test_projected_order_matches_explicit(side):
         assert abs(est.hutchpp_sample_projected(A[i], E[i], ZS, ZP, side) - refpp[i]) <= 1e-10 * refpp[i]
     c = np.array([0.5, 0.25])
     assert np.allclose(est.clip_accumulate_rows(A, E, c, [1, 4]), est.clip_accumulate(A, E, c)[[1, 4]])
+
+
+def test_adamw_matches_torch_and_first_step_closed_form():
+    # torch's AdamW (decoupled weight decay) on fp64 CPU tensors, three steps
+    r = np.random.default_rng(5)
+    theta0 = r.standard_normal((7, 5))
+    grads = [r.standard_normal((7, 5)) * s for s in (1.0, 0.1, 3.0)]
+    lr, b1, b2, eps, wd = 1e-2, 0.9, 0.99, 1e-8, 0.1
+    p = torch.tensor(theta0, dtype=torch.float64, requires_grad=True)
+    opt = torch.optim.AdamW([p], lr=lr, betas=(b1, b2), eps=eps, weight_decay=wd)
+    th, m, v = theta0, np.zeros_like(theta0), np.zeros_like(theta0)
+    for t, g in enumerate(grads, start=1):
+        p.grad = torch.tensor(g)
+        opt.step()
+        th, m, v = est.adamw(th, g, m, v, t, lr, b1, b2, eps, wd)
+        assert np.allclose(th, p.detach().numpy(), rtol=1e-12, atol=1e-14)
+    # first step without decay: theta - lr g / (|g| + eps)
+    g = grads[0]
+    th1, _, _ = est.adamw(theta0, g, 0.0, 0.0, 1, lr, b1, b2, eps, 0.0)
+    assert np.allclose(th1, theta0 - lr * g / (np.abs(g) + eps), rtol=1e-13, atol=1e-15)
+
+
+def test_private_gradient_composition():
+    A, E = _rng_inputs(3, 6, 4, 5, seed=8)
+    c = np.array([1.0, 0.5, 0.0])
+    g = est.private_gradient(A, E, c, 0.0, 1.0, 0, 0, 3)
+    assert np.allclose(g, est.clip_accumulate(A, E, c) / 3, rtol=1e-15)
+    g = est.private_gradient(A, E, c, 0.7, 2.0, 9, 4, 3)
+    assert np.allclose(g, est.add_noise(est.clip_accumulate(A, E, c), 0.7, 2.0, 9, 4) / 3, rtol=1e-15)
