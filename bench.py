@@ -272,6 +272,8 @@ def main():
         print(json.dumps({"copy_calibration_bytes": n, "copies": 5}))
         return
     D.lib()
+    if args.workload == "llama_step":
+        return run_llama_step(args, torch, D)
     cfg = dict(workloads.BY_NAME[args.workload])
     if args.probe != "rademacher":
         if cfg["estimator"] != "hutch":
@@ -392,6 +394,156 @@ def main():
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
         rec["cpu_baseline"] = cpu_baseline(cfg, sets, args.cpu_seconds)
     print(json.dumps(rec), flush=True)
+
+
+LLAMA_STEP = dict(B=2, T=2048, k=16, C=1.0, sigma=0.8, lr=1e-4)
+
+
+def run_llama_step(args, torch, D):
+    """The whole DP-SGD-RC training step on the Llama-3.2-1B-shaped stack (16 blocks, untied
+    lm_head, random weights, synthetic tokens): forward, capture of every linear layer's (A, E),
+    norms, clip factors, clipped gradients, noise and AdamW.  Context lines: a plain non-private
+    step (loss.backward-style weight gradients + AdamW) and the same private step with the
+    algorithm's second backward pass instead of the direct clipped GEMM."""
+    from paper_2605_24879_amd import dpsgd
+    from workloads import llama
+    cfg = LLAMA_STEP
+    B, T, k, C, sigma = cfg["B"], cfg["T"], cfg["k"], cfg["C"], cfg["sigma"]
+    steps, warmup = min(args.steps, 10), max(1, min(args.warmup, 3))
+    print(f"[bench] workload=llama_step B={B} T={T}: building the model", file=sys.stderr, flush=True)
+    model = llama.build(seed=0, device="cuda")
+    tok = llama.tokens(B, T, llama.LLAMA_3_2_1B["vocab"], device="cuda")
+    drv = dpsgd.DPSGDRC(model.linears(), C=C, sigma=sigma, k=k, lr=cfg["lr"])
+    loss_fn = lambda: llama.per_sample_loss(model(tok[:, :-1]), tok[:, 1:])
+    layer_shapes = [(lin.in_features, lin.out_features) for lin in drv.linears]
+    Ev = lambda: torch.cuda.Event(enable_timing=True)
+
+    def private_step(ev=None):
+        mark = (lambda j: ev[j].record()) if ev else (lambda j: None)
+        mark(0)
+        losses, pairs = drv.capture(loss_fn)
+        mark(1)
+        key = dpsgd.step_seed(0, drv.steps)
+        n2 = D.dprc_norm_hutch(pairs, k, key)
+        c = D.dprc_clip_scale(n2, C)
+        mark(2)
+        grads = []
+        for (A, E, j) in pairs:
+            g = D.dprc_clip_accumulate(A, E, c, ws=drv._ws_acc)
+            D.dprc_add_noise(g, sigma, C, key, j)
+            grads.append(g)
+        mark(3)
+        del pairs
+        drv.apply(grads, B)
+        mark(4)
+
+    need = max(D.dprc_clip_accumulate_workspace(torch.empty(B, T, d, dtype=torch.bfloat16, device="cuda"),
+                                                torch.empty(B, T, p, dtype=torch.bfloat16, device="cuda"))
+               for (d, p) in set(layer_shapes))
+    drv._ws_acc = torch.empty(max(need, 1), dtype=torch.uint8, device="cuda")
+    for _ in range(warmup):
+        private_step()
+    torch.cuda.synchronize()
+    print(f"[bench] llama_step: warm, timing {steps} steps", file=sys.stderr, flush=True)
+    stage = [0.0] * 4
+    t0, t1 = Ev(), Ev()
+    t0.record()
+    evs = []
+    for _ in range(steps):
+        ev = [Ev() for _ in range(5)]
+        private_step(ev)
+        evs.append(ev)
+    t1.record()
+    torch.cuda.synchronize()
+    ms_per_step = t0.elapsed_time(t1) / steps
+    for ev in evs:
+        for j in range(4):
+            stage[j] += ev[j].elapsed_time(ev[j + 1]) / steps
+    print(f"[bench] llama_step: {ms_per_step:.2f} ms/step", file=sys.stderr, flush=True)
+
+    # library kernels of one step, each launch timed with HIP events on its stream
+    hip = Hip()
+    recs = trace_kernels(hip, D, lambda: private_step(), 1, capacity=2048)
+    per_kind = {}
+    for name, ms in recs:
+        t, n = per_kind.get(name, (0.0, 0))
+        per_kind[name] = (t + ms, n + 1)
+    acc_ms, acc_n = per_kind.get("accumulate", (0.0, 0))
+    flops = sum(2 * B * T * d * p for (d, p) in layer_shapes)
+    acc_tf = flops / (acc_ms * 1e-3) / 1e12 if acc_ms else None
+    roof = {"bound": "mfma", "achieved": round(acc_tf, 1) if acc_tf else None, "peak": BF16_PEAK_TFLOPS,
+            "unit": "TFLOP/s", "frac": round(acc_tf / BF16_PEAK_TFLOPS, 4) if acc_tf else None, "traffic": None,
+            "kernel": "accumulate", "flops_per_step": int(flops), "launches_per_step": acc_n,
+            "avg_launch_us": round(acc_ms / max(acc_n, 1) * 1e3, 2)}
+    kernels = {kk: {"launches_per_step": v[1], "us_per_step": round(v[0] * 1e3, 1)} for kk, v in sorted(per_kind.items())}
+
+    extra = {"stages_ms": {"forward_and_capture": round(stage[0], 3), "norms_and_clip": round(stage[1], 3),
+                           "clipped_gemm_and_noise": round(stage[2], 3), "adamw": round(stage[3], 3)},
+             "library_kernels": kernels}
+    if not args.no_extra:
+        extra.update(llama_context_steps(torch, D, dpsgd, drv, loss_fn, model, B, T, k, C, sigma, steps))
+    rec = {"metric": "DP-SGD-RC training-step tokens/s, Llama-3.2-1B-shaped stack",
+           "value": round(B * T / (ms_per_step * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1,
+           "steps": steps, "warmup": warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+           "data": "synthetic (seeded tokens; random-init Llama-3.2-1B-shaped weights)",
+           "config": {"workload": "llama_step", "B": B, "T": T, "blocks": 16, "hidden": 2048, "mlp": 8192,
+                      "heads": "32q/8kv", "vocab": 128256, "trained": "all 113 linear layers",
+                      "estimator": "hutch", "probes": k, "C": C, "sigma": sigma, "optimizer": "AdamW",
+                      "steps_include": ["forward", "capture E (autograd to layer outputs)", "norm-hutch",
+                                        "clip_scale", "clip_accumulate", "add_noise", "AdamW"]},
+           "roofline": roof, "extra": extra}
+    print(json.dumps(rec), flush=True)
+
+
+def llama_context_steps(torch, D, dpsgd, drv, loss_fn, model, B, T, k, C, sigma, steps):
+    """Times of a plain non-private step and of the private step with the second backward pass."""
+    weights = [lin.weight for lin in drv.linears]
+    masters = [w.detach().t().float().contiguous() for w in weights]
+    opt = torch.optim.AdamW(masters, lr=1e-4)
+
+    def plain():
+        gw = torch.autograd.grad(loss_fn().mean(), weights)
+        for m, g in zip(masters, gw):
+            m.grad = g.t().float().contiguous()
+        opt.step()
+        opt.zero_grad(set_to_none=True)
+
+    def second_backward():
+        drv.remove_hooks()
+        hooks = [lin.register_forward_hook(drv._tap(j)) for j, lin in enumerate(drv.linears)]
+        losses = loss_fn()
+        E = torch.autograd.grad(losses.sum(), drv._S, retain_graph=True)
+        pairs = [(dpsgd._rows(drv._A[j].detach()), dpsgd._rows(E[j]), j) for j in range(len(weights))]
+        drv._A = [None] * len(weights)
+        drv._S = [None] * len(weights)
+        for h in hooks:
+            h.remove()
+        key = dpsgd.step_seed(0, drv.steps)
+        n2 = D.dprc_norm_hutch(pairs, k, key)
+        c = D.dprc_clip_scale(n2, C)
+        del pairs, E
+        gw = torch.autograd.grad((losses * c).sum(), weights)
+        for j, (m, g) in enumerate(zip(masters, gw)):
+            gt = g.t().float().contiguous()
+            D.dprc_add_noise(gt, sigma, C, key, j)
+            m.grad = gt.div_(B)
+        opt.step()
+        opt.zero_grad(set_to_none=True)
+
+    out = {}
+    for name, fn in (("plain_nonprivate_step_ms", plain), ("second_backward_private_step_ms", second_backward)):
+        fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        n = max(2, steps // 2)
+        a.record()
+        for _ in range(n):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        out[name] = round(a.elapsed_time(b) / n, 3)
+    return out
 
 
 def step_parts(cfg):
