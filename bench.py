@@ -427,14 +427,10 @@ def run_llama_step(args, torch, D):
         n2 = D.dprc_norm_hutch(pairs, k, key)
         c = D.dprc_clip_scale(n2, C)
         mark(2)
-        grads = []
-        for (A, E, j) in pairs:
-            g = D.dprc_clip_accumulate(A, E, c, ws=drv._ws_acc)
-            D.dprc_add_noise(g, sigma, C, key, j)
-            grads.append(g)
+        grads = [D.dprc_clip_accumulate(A, E, c, ws=drv._ws_acc) for (A, E, _) in pairs]
         mark(3)
         del pairs
-        drv.apply(grads, B)
+        drv.update(grads, B, key)            # noise + 1/B + AdamW + bf16 weights, one pass per layer
         mark(4)
 
     need = max(D.dprc_clip_accumulate_workspace(torch.empty(B, T, d, dtype=torch.bfloat16, device="cuda"),
@@ -478,7 +474,7 @@ def run_llama_step(args, torch, D):
     kernels = {kk: {"launches_per_step": v[1], "us_per_step": round(v[0] * 1e3, 1)} for kk, v in sorted(per_kind.items())}
 
     extra = {"stages_ms": {"forward_and_capture": round(stage[0], 3), "norms_and_clip": round(stage[1], 3),
-                           "clipped_gemm_and_noise": round(stage[2], 3), "adamw": round(stage[3], 3)},
+                           "clipped_gemm": round(stage[2], 3), "noise_and_adamw_fused": round(stage[3], 3)},
              "library_kernels": kernels}
     if not args.no_extra:
         extra.update(llama_context_steps(torch, D, dpsgd, drv, loss_fn, model, B, T, k, C, sigma, steps))
@@ -491,7 +487,7 @@ def run_llama_step(args, torch, D):
                       "heads": "32q/8kv", "vocab": 128256, "trained": "all 113 linear layers",
                       "estimator": "hutch", "probes": k, "C": C, "sigma": sigma, "optimizer": "AdamW",
                       "steps_include": ["forward", "capture E (autograd to layer outputs)", "norm-hutch",
-                                        "clip_scale", "clip_accumulate", "add_noise", "AdamW"]},
+                                        "clip_scale", "clip_accumulate", "private_adamw (noise + AdamW)"]},
            "roofline": roof, "extra": extra}
     print(json.dumps(rec), flush=True)
 
@@ -531,8 +527,25 @@ def llama_context_steps(torch, D, dpsgd, drv, loss_fn, model, B, T, k, C, sigma,
         opt.step()
         opt.zero_grad(set_to_none=True)
 
+    def unfused():
+        losses, pairs = drv.capture(loss_fn)
+        key = dpsgd.step_seed(0, drv.steps)
+        n2 = D.dprc_norm_hutch(pairs, k, key)
+        c = D.dprc_clip_scale(n2, C)
+        for (A, E, j), m in zip(pairs, masters):
+            g = D.dprc_clip_accumulate(A, E, c, ws=drv._ws_acc)
+            D.dprc_add_noise(g, sigma, C, key, j)
+            m.grad = g.div_(B)
+        del pairs
+        opt.step()
+        opt.zero_grad(set_to_none=True)
+        with torch.no_grad():
+            for lin, m in zip(drv.linears, masters):
+                lin.weight.copy_(m.t())
+
     out = {}
-    for name, fn in (("plain_nonprivate_step_ms", plain), ("second_backward_private_step_ms", second_backward)):
+    for name, fn in (("plain_nonprivate_step_ms", plain), ("private_step_torch_adamw_ms", unfused),
+                     ("second_backward_private_step_ms", second_backward)):
         fn()
         torch.cuda.synchronize()
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)

@@ -149,6 +149,33 @@ dprc_status dprc_clip_accumulate(const dprc_layer* layer, const float* c, float*
 dprc_status dprc_add_noise(float* grad, int64_t numel, float sigma, float C, uint64_t seed,
                            uint32_t tensor_id, hipStream_t stream);
 
+/* ---- Private AdamW step (Algorithm 1: noise addition and optimizer step) --------
+ * One AdamW step (Adam with decoupled weight decay, the optimizer of the
+ * paper's private runs) on one layer's fp32 master weights, fed the private
+ * gradient
+ *   g[r][c] = (G[r][c] + sigma * C * xi_e) * inv_batch,   e = r * p + c,
+ * where G [d, p] (row stride ldg) is the clipped gradient sum from
+ * dprc_clip_accumulate and xi_e is the value dprc_add_noise(seed, tensor_id)
+ * would add to element e of a contiguous [d, p] buffer (sigma = 0: none).
+ * With t = hp->step (1-based), for every element:
+ *   theta *= 1 - lr * weight_decay;
+ *   m = beta1 m + (1 - beta1) g;   v = beta2 v + (1 - beta2) g^2;
+ *   theta -= lr / (1 - beta1^t) * m / (sqrt(v) / sqrt(1 - beta2^t) + eps).
+ * theta, m, v: fp32 [d, p] with row stride ldt >= p, updated in place; G is
+ * read only.  w (may be NULL) receives bf16(theta) transposed, w[c][r] with
+ * row stride ldw >= d (the [p, d] weight of a linear layer), rounded to
+ * nearest even.  Device pointers, fp32 ones 4-byte aligned, w 2-byte aligned;
+ * 16-byte aligned rows with p a multiple of 4 take vector accesses.
+ * hp: host pointer; lr >= 0, 0 <= beta1, beta2 < 1, eps > 0, step >= 1. */
+typedef struct {
+  float lr, beta1, beta2, eps, weight_decay;
+  int32_t step;
+} dprc_adamw_params;
+dprc_status dprc_private_adamw(float* theta, float* m, float* v, int64_t ldt, const float* G, int64_t ldg,
+                               int64_t d, int64_t p, float sigma, float C, uint64_t seed,
+                               uint32_t tensor_id, float inv_batch, const dprc_adamw_params* hp,
+                               uint16_t* w, int64_t ldw, hipStream_t stream);
+
 /* ---- probe bits (verification) -------------------------------------------------
  * out[j*ceil(m/32) + w] = packed probe word w of column j (k columns), bits of
  * rows >= m cleared.  probe selects the family; for HADAMARD, seed, layer_id
@@ -192,7 +219,8 @@ typedef enum {
   DPRC_KERNEL_QR_COMBINE = 16,        /* QR of stacked block R factors (upper tree levels) */
   DPRC_KERNEL_QR_EXPAND = 17,         /* rows of Q per tree level; Q^T P at the first */
   DPRC_KERNEL_HUTCHPP_SUM = 18,       /* per-sample Hutch++ estimate            */
-  DPRC_KERNEL_PROBE_GAUSS = 19        /* Gaussian probe columns                  */
+  DPRC_KERNEL_PROBE_GAUSS = 19,       /* Gaussian probe columns                  */
+  DPRC_KERNEL_ADAMW = 20              /* private AdamW step                      */
 } dprc_kernel_kind;
 dprc_status dprc_trace_launches(hipEvent_t* events, int32_t* kinds, int32_t capacity,
                                 int32_t* count);

@@ -728,6 +728,41 @@ dprc_status dprc_probe_bits(dprc_probe probe, uint64_t seed, uint32_t layer_id, 
   return hip_status(traced(DPRC_KERNEL_PROBE_BITS, stream, [&] { return launch_probe_bits((int)probe, k0, k1, layer_id, stream_id, m, k, out, stream); }));
 }
 
+dprc_status dprc_private_adamw(float* theta, float* m, float* v, int64_t ldt, const float* G, int64_t ldg,
+                               int64_t d, int64_t p, float sigma, float C, uint64_t seed, uint32_t tensor_id,
+                               float inv_batch, const dprc_adamw_params* hp, uint16_t* w, int64_t ldw,
+                               hipStream_t stream) {
+  if (!theta || !m || !v || !G || !hp || d < 0 || p < 0 || ldt < p || ldg < p) return DPRC_ERROR_INVALID_VALUE;
+  if (w && ldw < d) return DPRC_ERROR_INVALID_VALUE;
+  if (!(sigma >= 0.f) || !std::isfinite(sigma) || !(C > 0.f) || !std::isfinite(C) || !std::isfinite(inv_batch))
+    return DPRC_ERROR_INVALID_VALUE;
+  const dprc_adamw_params& h = *hp;
+  if (!(h.lr >= 0.f) || !std::isfinite(h.lr) || !(h.beta1 >= 0.f && h.beta1 < 1.f) ||
+      !(h.beta2 >= 0.f && h.beta2 < 1.f) || !(h.eps > 0.f) || !std::isfinite(h.eps) ||
+      !std::isfinite(h.weight_decay) || h.step < 1)
+    return DPRC_ERROR_INVALID_VALUE;
+  if (!aligned(theta, 4) || !aligned(m, 4) || !aligned(v, 4) || !aligned(G, 4) || (w && !aligned(w, 2)))
+    return DPRC_ERROR_INVALID_VALUE;
+  if (d == 0 || p == 0) return DPRC_SUCCESS;
+  AdamArgs a;
+  a.theta = theta; a.m = m; a.v = v; a.ldt = ldt; a.G = G; a.ldg = ldg; a.d = d; a.p = p;
+  a.noise_scale = sigma * C;
+  key_of(seed, a.key0, a.key1);
+  a.tensor = tensor_id; a.inv_batch = inv_batch;
+  a.decay = (float)(1.0 - (double)h.lr * h.weight_decay);
+  a.beta1 = h.beta1; a.beta2 = h.beta2;
+  a.one_minus_beta1 = (float)(1.0 - (double)h.beta1); a.one_minus_beta2 = (float)(1.0 - (double)h.beta2);
+  const double bc1 = 1.0 - std::pow((double)h.beta1, h.step), bc2 = 1.0 - std::pow((double)h.beta2, h.step);
+  a.step_size = (float)(h.lr / bc1);
+  a.inv_sqrt_bc2 = (float)(1.0 / std::sqrt(bc2));
+  a.eps = h.eps;
+  a.w = w; a.ldw = ldw;
+  a.vec = p % 4 == 0 && ldt % 4 == 0 && ldg % 4 == 0 && aligned(theta, 16) && aligned(m, 16) && aligned(v, 16) &&
+          aligned(G, 16);
+  a.wvec = w && ldw % 8 == 0 && aligned(w, 16);
+  return hip_status(traced(DPRC_KERNEL_ADAMW, stream, [&] { return launch_private_adamw(a, stream); }));
+}
+
 dprc_status dprc_probe_gaussian(uint64_t seed, uint32_t layer_id, int64_t m, int32_t k, float* out,
                                 hipStream_t stream) {
   if (!out || m < 1 || k < 1 || k > 256 || m > (1LL << 36)) return DPRC_ERROR_INVALID_VALUE;

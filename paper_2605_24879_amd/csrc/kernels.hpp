@@ -183,6 +183,29 @@ int32_t final_chunks(int64_t n);
 hipError_t launch_probe_bits(int probe_kind, uint32_t key0, uint32_t key1, uint32_t layer,
                              uint32_t stream_id, int64_t m, int32_t k, uint32_t* out,
                              hipStream_t st);
+// One private AdamW step on a [d, p] fp32 master (see dprc_private_adamw).
+struct AdamArgs {
+  float* theta;
+  float* m;
+  float* v;
+  int64_t ldt;
+  const float* G;
+  int64_t ldg;
+  int64_t d, p;
+  float noise_scale;       // sigma * C (0: no noise)
+  uint32_t key0, key1, tensor;
+  float inv_batch;
+  float decay;             // 1 - lr * weight_decay
+  float beta1, beta2, one_minus_beta1, one_minus_beta2;
+  float step_size;         // lr / (1 - beta1^t)
+  float inv_sqrt_bc2;      // 1 / sqrt(1 - beta2^t)
+  float eps;
+  uint16_t* w;             // bf16 [p, d] copy (may be null)
+  int64_t ldw;
+  int32_t vec, wvec;
+};
+hipError_t launch_private_adamw(const AdamArgs& a, hipStream_t st);
+
 // Gaussian probe columns, column j at [j*ld .. j*ld + ld) (rows >= m zero);
 // any of hi/lo (both or neither) and f32 may be null.
 hipError_t launch_gauss_probe(uint32_t key0, uint32_t key1, uint32_t layer, int64_t m, int32_t k, int64_t ld,

@@ -24,7 +24,7 @@ STREAM_PROBE, STREAM_SKETCH, STREAM_NOISE = 0, 1, 2
 
 EXPORTS = ["dprc_norm_hutch_workspace", "dprc_norm_hutch", "dprc_norm_hutchpp_workspace",
            "dprc_norm_hutchpp", "dprc_clip_scale", "dprc_clip_accumulate_workspace",
-           "dprc_clip_accumulate", "dprc_add_noise", "dprc_probe_bits", "dprc_probe_gaussian", "dprc_status_string",
+           "dprc_clip_accumulate", "dprc_add_noise", "dprc_probe_bits", "dprc_probe_gaussian", "dprc_private_adamw", "dprc_status_string",
            "dprc_version", "dprc_trace_launches"]
 
 
@@ -34,6 +34,12 @@ class Layer(ctypes.Structure):
                 ("B", ctypes.c_int64), ("T", ctypes.c_int64), ("d", ctypes.c_int64), ("p", ctypes.c_int64),
                 ("lda", ctypes.c_int64), ("lde", ctypes.c_int64),
                 ("dtype", ctypes.c_int), ("layer_id", ctypes.c_uint32)]
+
+
+class AdamWParams(ctypes.Structure):
+    """Mirror of dprc_adamw_params."""
+    _fields_ = [("lr", ctypes.c_float), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float),
+                ("eps", ctypes.c_float), ("weight_decay", ctypes.c_float), ("step", ctypes.c_int32)]
 
 
 _lib = None
@@ -60,6 +66,8 @@ def lib():
             "dprc_add_noise": (ctypes.c_int, [P, I64, F, F, U64, U32, P]),
             "dprc_probe_bits": (ctypes.c_int, [ctypes.c_int, U64, U32, U32, I64, I32, P, P]),
             "dprc_probe_gaussian": (ctypes.c_int, [U64, U32, I64, I32, P, P]),
+            "dprc_private_adamw": (ctypes.c_int, [P, P, P, I64, P, I64, I64, I64, F, F, U64, U32, F,
+                                                  ctypes.POINTER(AdamWParams), P, I64, P]),
             "dprc_status_string": (ctypes.c_char_p, [ctypes.c_int]),
             "dprc_version": (ctypes.c_char_p, []),
             "dprc_trace_launches": (ctypes.c_int, [P, P, I32, P]),
@@ -193,6 +201,26 @@ def dprc_add_noise(grad, sigma, C, seed, tensor_id):
     return grad
 
 
+def dprc_private_adamw(theta, m, v, G, sigma, C, seed, tensor_id, inv_batch, lr, beta1, beta2, eps,
+                       weight_decay, step, w=None):
+    """One private AdamW step: theta, m, v ([d, p] fp32, updated in place) from the clipped
+    gradient G [d, p]; w (optional, [p, d] bf16) receives bf16(theta) transposed."""
+    d, p = G.shape
+    for X in (theta, m, v):
+        if X.shape != (d, p) or X.dtype != torch.float32 or X.stride(1) != 1 or X.stride(0) != theta.stride(0):
+            raise ValueError("theta, m, v must be fp32 [d, p] with one row stride")
+    if G.dtype != torch.float32 or G.stride(1) != 1:
+        raise ValueError("G must be fp32 [d, p] with contiguous rows")
+    if w is not None and (w.shape != (p, d) or w.dtype != torch.bfloat16 or w.stride(1) != 1):
+        raise ValueError("w must be bf16 [p, d] with contiguous rows")
+    hp = AdamWParams(lr, beta1, beta2, eps, weight_decay, int(step))
+    _check(lib().dprc_private_adamw(theta.data_ptr(), m.data_ptr(), v.data_ptr(), theta.stride(0), G.data_ptr(),
+                                    G.stride(0), d, p, sigma, C, seed, tensor_id, inv_batch, ctypes.byref(hp),
+                                    w.data_ptr() if w is not None else None, w.stride(0) if w is not None else 0,
+                                    _stream(G.device)))
+    return theta
+
+
 def dprc_probe_bits(probe, seed, layer_id, stream_id, m, k, device="cuda", out=None):
     """Packed probe words [k, ceil(m/32)] (int32 view of the uint32 words)."""
     nw = (m + 31) // 32
@@ -218,7 +246,7 @@ KERNEL_NAMES = {1: "project", 2: "token_reduce", 3: "qr", 4: "hutchpp_final", 5:
                 6: "accumulate", 7: "splitk_reduce", 8: "noise", 9: "probe_bits", 10: "project_f32",
                 11: "token_reduce_f32", 12: "sample_sq", 13: "accumulate_f32",
                 14: "token_splits", 15: "sample_sum", 16: "qr_combine", 17: "qr_expand", 18: "hutchpp_sum",
-                19: "probe_gauss"}
+                19: "probe_gauss", 20: "adamw"}
 
 
 def dprc_trace_launches(events_ptr, kinds_ptr, capacity, count_ptr):

@@ -19,7 +19,10 @@ Per step:
 6. ``dprc_add_noise``: + sigma C N(0, I) per element of the summed gradient;
 7. AdamW on fp32 master weights (kept in the [d, p] layout of the clipped
    gradient) with the private gradient divided by the batch size, then the
-   bf16 weights are refreshed from the masters.
+   bf16 weights are refreshed from the masters.  By default steps 6 and 7
+   run as one ``dprc_private_adamw`` pass per layer (noise, division, AdamW
+   and the transposed bf16 weight write); ``fused_adamw=False`` runs
+   ``dprc_add_noise`` and ``torch.optim.AdamW`` instead.
 
 Only the listed linear layers are trained; every other parameter (embedding,
 norms) is held fixed.  Probes and noise are keyed by a per-step seed derived
@@ -54,7 +57,8 @@ class DPSGDRC:
     """
 
     def __init__(self, linears, C, sigma, estimator="hutch", k=16, probe="rademacher", s=16, r=32,
-                 side=D.SIDE_OUT, seed=0, lr=1e-4, betas=(0.9, 0.999), eps=1e-8, weight_decay=0.0):
+                 side=D.SIDE_OUT, seed=0, lr=1e-4, betas=(0.9, 0.999), eps=1e-8, weight_decay=0.0,
+                 fused_adamw=True):
         self.linears = list(linears)
         for lin in self.linears:
             if lin.bias is not None:
@@ -67,7 +71,13 @@ class DPSGDRC:
         self.master = [lin.weight.detach().t().float().contiguous() for lin in self.linears]
         for lin in self.linears:
             lin.weight.requires_grad_(True)
-        self.opt = torch.optim.AdamW(self.master, lr=lr, betas=betas, eps=eps, weight_decay=weight_decay)
+        self.hp = dict(lr=lr, beta1=betas[0], beta2=betas[1], eps=eps, weight_decay=weight_decay)
+        self.fused = bool(fused_adamw)
+        if self.fused:
+            self.m = [torch.zeros_like(x) for x in self.master]
+            self.v = [torch.zeros_like(x) for x in self.master]
+        else:
+            self.opt = torch.optim.AdamW(self.master, lr=lr, betas=betas, eps=eps, weight_decay=weight_decay)
         self.steps = 0
         self._A = [None] * len(self.linears)
         self._S = [None] * len(self.linears)
@@ -98,8 +108,9 @@ class DPSGDRC:
         self._S = [None] * len(self.linears)
         return losses.detach(), pairs
 
-    def private_grads(self, pairs, key):
-        """Steps 3-6: n2 [B], c [B] and the noisy clipped gradients ([d, p] fp32 per layer)."""
+    def private_grads(self, pairs, key, noise=True):
+        """Steps 3-6: n2 [B], c [B] and the clipped gradients ([d, p] fp32 per layer), with
+        the noise added unless ``noise`` is false."""
         if self.estimator == "hutch":
             n2 = D.dprc_norm_hutch(pairs, self.k, key, side=self.side, probe=self.probe)
         else:
@@ -111,13 +122,22 @@ class DPSGDRC:
         grads = []
         for (A, E, j) in pairs:
             g = D.dprc_clip_accumulate(A, E, c, ws=self._ws_acc)
-            if self.sigma > 0:
+            if noise and self.sigma > 0:
                 D.dprc_add_noise(g, self.sigma, self.C, key, j)
             grads.append(g)
         return n2, c, grads
 
+    def update(self, clipped, batch, key):
+        """Steps 6-7 fused: per layer, noise + 1/batch + AdamW + bf16 weight write in one pass."""
+        t = self.steps + 1
+        for j, (lin, th, G) in enumerate(zip(self.linears, self.master, clipped)):
+            D.dprc_private_adamw(th, self.m[j], self.v[j], G, self.sigma, self.C, key, j, 1.0 / batch,
+                                 step=t, w=lin.weight.detach(), **self.hp)
+            lin.weight.grad = None
+        self.steps = t
+
     def apply(self, grads, batch):
-        """Step 7: AdamW on the masters with grads / batch, then refresh the model weights."""
+        """Step 7 with torch's AdamW (noisy grads / batch), then refresh the model weights."""
         for m, g in zip(self.master, grads):
             m.grad = g.div_(batch)
         self.opt.step()
@@ -132,8 +152,11 @@ class DPSGDRC:
         """One full step; returns the per-sample losses (before the update)."""
         losses, pairs = self.capture(loss_fn)
         key = step_seed(self.seed, self.steps)
-        n2, c, grads = self.private_grads(pairs, key)
+        n2, c, grads = self.private_grads(pairs, key, noise=not self.fused)
         del pairs
-        self.apply(grads, losses.numel())
+        if self.fused:
+            self.update(grads, losses.numel(), key)
+        else:
+            self.apply(grads, losses.numel())
         self.last = {"n2": n2, "c": c}
         return losses

@@ -334,3 +334,44 @@ def test_add_noise_moments(D):
     n = x.numel()
     assert abs(x.mean().item()) < 5 / math.sqrt(n)
     assert abs(x.var().item() - 1.0) < 5 * math.sqrt(2.0 / n)
+
+
+# ---- private AdamW step (noise + 1/B + AdamW + transposed bf16 weights) ---------------------
+
+@pytest.mark.parametrize("d,p,ld_pad,sigma,steps,wout", [
+    (128, 256, 0, 0.7, 3, True),      # vector path, three steps
+    (67, 130, 3, 0.5, 2, True),       # p not a multiple of 4, padded rows: element path, ragged tiles
+    (64, 64, 4, 0.0, 1, False),       # no noise, no weight copy, padded rows
+    (1, 5, 0, 1.0, 1, True),
+])
+def test_private_adamw_parity(D, d, p, ld_pad, sigma, steps, wout):
+    r = np.random.default_rng(1000 * d + p)
+    ld = p + ld_pad
+    C, Bsz, lr, b1, b2, eps, wd, seed, tid = 1.5, 4, 1e-2, 0.9, 0.99, 1e-8, 0.05, 21, 5
+
+    def dev(x):
+        buf = torch.zeros(d, ld, dtype=torch.float32, device="cuda")
+        buf[:, :p] = torch.tensor(x, dtype=torch.float32)
+        return buf[:, :p]
+    th0 = (r.standard_normal((d, p)) * 0.02).astype(np.float32)
+    theta, m, v = dev(th0), dev(np.zeros((d, p))), dev(np.zeros((d, p)))
+    w = torch.empty(p, d, dtype=torch.bfloat16, device="cuda") if wout else None
+    th, mr, vr = th0.astype(np.float64), 0.0, 0.0
+    firm = None
+    for t in range(1, steps + 1):
+        G = dev((r.standard_normal((d, p)) * 0.3).astype(np.float32))
+        D.dprc_private_adamw(theta, m, v, G, sigma, C, seed, tid, 1.0 / Bsz, lr, b1, b2, eps, wd, t, w=w)
+        G64 = est.as_f64(G.cpu())
+        g = (est.add_noise(G64, sigma, C, seed, tid) if sigma > 0 else G64) / Bsz
+        if firm is None:
+            firm = np.abs(g) > 1e-4               # first update lr g/(|g|+eps) is steep near g = 0
+        th, mr, vr = est.adamw(th, g, mr, vr, t, lr, b1, b2, eps, wd)
+    torch.cuda.synchronize()
+    got = theta.cpu().double().numpy()
+    assert firm.mean() > 0.99
+    assert np.max(np.abs(got - th)[firm]) <= 2e-6
+    assert np.max(np.abs(got - th)) <= 2 * lr * steps
+    assert np.allclose(m.cpu().double().numpy(), mr, rtol=1e-5, atol=1e-8)
+    assert np.allclose(v.cpu().double().numpy(), vr, rtol=1e-5, atol=1e-10)
+    if wout:
+        assert torch.equal(w, theta.t().to(torch.bfloat16))

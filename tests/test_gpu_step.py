@@ -47,7 +47,8 @@ def _rel_fro(a, b):
 def test_step_stages_match_oracle(mods):
     D, dpsgd = mods
     C, sigma, k = 0.05, 0.6, 16
-    model, drv, loss_fn = _setup(dpsgd, C=C, sigma=sigma, k=k, seed=11, lr=1e-3, weight_decay=0.01)
+    model, drv, loss_fn = _setup(dpsgd, C=C, sigma=sigma, k=k, seed=11, lr=1e-3, weight_decay=0.01,
+                                 fused_adamw=False)
     losses, pairs = drv.capture(loss_fn)
     assert pairs[0][0].data_ptr() == pairs[1][0].data_ptr() == pairs[2][0].data_ptr()   # q, k, v
     key = dpsgd.step_seed(11, 0)
@@ -80,6 +81,39 @@ def test_step_stages_match_oracle(mods):
         assert firm.mean() > 0.99
         assert np.max(np.abs(got - th)[firm]) <= 1e-6, j
         assert np.max(np.abs(got - th)) <= 2.1e-3, j
+        assert torch.equal(lin.weight.detach(), drv.master[j].t().to(torch.bfloat16))
+    drv.remove_hooks()
+
+
+def test_fused_update_matches_oracle(mods):
+    # steps 6-7 in one kernel per layer: noise + 1/B + AdamW + transposed bf16 weights
+    D, dpsgd = mods
+    C, sigma, k, lr, wd = 0.05, 0.6, 16, 1e-3, 0.01
+    model, drv, loss_fn = _setup(dpsgd, C=C, sigma=sigma, k=k, seed=12, lr=lr, weight_decay=wd)
+    assert drv.fused
+    losses, pairs = drv.capture(loss_fn)
+    key = dpsgd.step_seed(12, 0)
+    n2, c, clipped = drv.private_grads(pairs, key, noise=False)
+    torch.cuda.synchronize()
+    B = losses.numel()
+    masters0 = [m.detach().cpu().double().numpy() for m in drv.master]
+    c_ref = est.clip_scale(n2.cpu().numpy().astype(np.float64), C)
+    refs = []
+    for (A, E, j) in pairs:
+        A64, E64 = est.as_f64(A), est.as_f64(E)
+        clip = est.clip_accumulate(A64, E64, c_ref)
+        assert np.linalg.norm(clipped[j].cpu().double().numpy() - clip) <= GRAD_RTOL * np.linalg.norm(clip), j
+        refs.append(est.private_gradient(A64, E64, c_ref, sigma, C, key, j, B))
+    drv.update(clipped, B, key)
+    torch.cuda.synchronize()
+    for j, lin in enumerate(drv.linears):
+        th, m, v = est.adamw(masters0[j], refs[j], 0.0, 0.0, 1, lr, 0.9, 0.999, 1e-8, wd)
+        got = drv.master[j].detach().cpu().double().numpy()
+        firm = np.abs(refs[j]) > 1e-5
+        assert firm.mean() > 0.99
+        assert np.max(np.abs(got - th)[firm]) <= 1e-6, j
+        assert np.max(np.abs(got - th)) <= 2.1e-3, j
+        assert np.allclose(drv.m[j].cpu().double().numpy(), m, rtol=1e-3, atol=1e-7)
         assert torch.equal(lin.weight.detach(), drv.master[j].t().to(torch.bfloat16))
     drv.remove_hooks()
 

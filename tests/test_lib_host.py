@@ -131,3 +131,26 @@ def test_clip_noise_bits_validation():
     assert L.dprc_probe_bits(0, 0, 0, 0, 0, 4, 0x1000, None) == 1
     assert L.dprc_probe_bits(0, 0, 0, 0, 32, 0, 0x1000, None) == 1
     assert L.dprc_probe_bits(3, 0, 0, 0, 32, 4, 0x1000, None) == 1
+
+
+def test_private_adamw_validation():
+    L = dprc.lib()
+    hp = dprc.AdamWParams(1e-3, 0.9, 0.999, 1e-8, 0.0, 1)
+    T, M, V, G = 0x10000, 0x20000, 0x30000, 0x40000
+
+    def call(ldt=8, ldg=8, d=4, p=8, sigma=1.0, C=1.0, inv=0.25, h=hp, w=None, ldw=0, theta=T):
+        return L.dprc_private_adamw(theta, M, V, ldt, G, ldg, d, p, sigma, C, 0, 0, inv, ctypes.byref(h) if h else None,
+                                    w, ldw, None)
+    assert call(theta=0) == 1
+    assert call(ldt=7) == 1
+    assert call(ldg=7) == 1
+    assert call(sigma=-1.0) == 1
+    assert call(C=0.0) == 1
+    assert call(inv=float("inf")) == 1
+    assert call(h=None) == 1
+    assert call(w=0x50000, ldw=3) == 1
+    assert call(theta=T + 2) == 1                 # fp32 pointers 4-byte aligned
+    for bad in (dprc.AdamWParams(-1.0, 0.9, 0.999, 1e-8, 0.0, 1), dprc.AdamWParams(1e-3, 1.0, 0.999, 1e-8, 0.0, 1),
+                dprc.AdamWParams(1e-3, 0.9, 0.999, 0.0, 0.0, 1), dprc.AdamWParams(1e-3, 0.9, 0.999, 1e-8, 0.0, 0)):
+        assert call(h=bad) == 1
+    assert call(d=0) == 0                         # nothing to do, nothing enqueued
