@@ -176,6 +176,30 @@ dprc_status dprc_private_adamw(float* theta, float* m, float* v, int64_t ldt, co
                                uint32_t tensor_id, float inv_batch, const dprc_adamw_params* hp,
                                uint16_t* w, int64_t ldw, hipStream_t stream);
 
+/* ---- Envelope CDF of the Hutchinson estimate (privacy accounting) ------------------
+ * Proposition on the extremal envelope and the appendix algorithms cdf-grid and
+ * binary-search-xplus.  dprc_envelope_middle evaluates MiddleRegionCDF at nx
+ * points: best[e] = the largest P(S <= x[e]) over the two-level forms
+ *   S(i, j, lam) = lam/(ik) chi^2(ik) + (1-lam)/(jk) chi^2(jk),
+ *   i, j >= 1, i + j <= d, lam = l / (2 (n_lambda - 1)), l = 0 .. n_lambda - 1
+ * (lam = 0 only when n_lambda = 1), in fp64.  arg (may be NULL) receives
+ * (i, j, l) of the maximiser, the first in (i, j, l) order among equal values.
+ * Each form's CDF is a convolution integral evaluated by composite
+ * Gauss-Legendre quadrature (16 panels of 16 nodes) with regularised incomplete
+ * gamma functions; about 1e-12 absolute.  x, best, arg: device.  Limits:
+ * 1 <= nx <= 65535, k >= 1, 2 <= d, k * d < 2^31, 1 <= n_lambda <= 4096.
+ * Workspace: dprc_envelope_middle_workspace() bytes. */
+size_t dprc_envelope_middle_workspace(int32_t nx, int32_t d, int32_t n_lambda);
+dprc_status dprc_envelope_middle(const double* x, int32_t nx, int32_t k, int32_t d, int32_t n_lambda,
+                                 double* best, int32_t* arg, void* ws, size_t ws_bytes,
+                                 hipStream_t stream);
+
+/* out[e] = P(chi^2(dof) <= x[e] * scale) for e < n (the extremal parts of the
+ * envelope: dof = k, scale = k for the single coordinate; dof = scale = k d for
+ * uniform weights).  dof > 0, scale > 0; x, out: device, fp64. */
+dprc_status dprc_chi2_cdf(const double* x, int64_t n, double dof, double scale, double* out,
+                          hipStream_t stream);
+
 /* ---- probe bits (verification) -------------------------------------------------
  * out[j*ceil(m/32) + w] = packed probe word w of column j (k columns), bits of
  * rows >= m cleared.  probe selects the family; for HADAMARD, seed, layer_id
@@ -220,7 +244,9 @@ typedef enum {
   DPRC_KERNEL_QR_EXPAND = 17,         /* rows of Q per tree level; Q^T P at the first */
   DPRC_KERNEL_HUTCHPP_SUM = 18,       /* per-sample Hutch++ estimate            */
   DPRC_KERNEL_PROBE_GAUSS = 19,       /* Gaussian probe columns                  */
-  DPRC_KERNEL_ADAMW = 20              /* private AdamW step                      */
+  DPRC_KERNEL_ADAMW = 20,             /* private AdamW step                      */
+  DPRC_KERNEL_ENVELOPE = 21,          /* MiddleRegionCDF candidates and reduction */
+  DPRC_KERNEL_CHI2_CDF = 22           /* chi-squared CDF values                  */
 } dprc_kernel_kind;
 dprc_status dprc_trace_launches(hipEvent_t* events, int32_t* kinds, int32_t capacity,
                                 int32_t* count);

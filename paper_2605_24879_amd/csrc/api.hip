@@ -553,6 +553,30 @@ dprc_status hutchpp_layer(const View& v, int32_t s, int32_t r, uint32_t k0, uint
 // ---- clipped accumulation ----------------------------------------------------------------------------
 GemmPlan gemm_plan(const dprc_layer& L) { return gemm_plan_v2(L.B, L.T, L.d, L.p); }
 
+// n-point Gauss-Legendre nodes and weights on [-1, 1]: Newton iteration on the
+// roots of P_n, started from the Chebyshev-like guesses cos(pi (q + 3/4) / (n + 1/2)),
+// with P_n and P_n' from the three-term recurrence; w = 2 / ((1 - x^2) P_n'(x)^2).
+void gauss_legendre(int n, double* x, double* w) {
+  for (int q = 0; q < (n + 1) / 2; ++q) {
+    double z = std::cos(M_PI * (q + 0.75) / (n + 0.5)), dp = 1.0;
+    for (int it = 0; it < 100; ++it) {
+      double p0 = 1.0, p1 = 0.0;
+      for (int j = 1; j <= n; ++j) {
+        const double p2 = p1;
+        p1 = p0;
+        p0 = ((2.0 * j - 1.0) * z * p1 - (j - 1.0) * p2) / j;
+      }
+      dp = n * (z * p0 - p1) / (z * z - 1.0);
+      const double dz = p0 / dp;
+      z -= dz;
+      if (std::fabs(dz) < 1e-15) break;
+    }
+    x[q] = -z;
+    x[n - 1 - q] = z;
+    w[q] = w[n - 1 - q] = 2.0 / ((1.0 - z * z) * dp * dp);
+  }
+}
+
 }  // namespace
 
 namespace dprc {
@@ -761,6 +785,44 @@ dprc_status dprc_private_adamw(float* theta, float* m, float* v, int64_t ldt, co
           aligned(G, 16);
   a.wvec = w && ldw % 8 == 0 && aligned(w, 16);
   return hip_status(traced(DPRC_KERNEL_ADAMW, stream, [&] { return launch_private_adamw(a, stream); }));
+}
+
+size_t dprc_envelope_middle_workspace(int32_t nx, int32_t d, int32_t n_lambda) {
+  if (nx < 1 || nx > 65535 || d < 2 || n_lambda < 1 || n_lambda > 4096) return 0;
+  const int64_t ncand = (int64_t)d * (d - 1) / 2 * n_lambda;
+  Arena ar(nullptr);
+  ar.take<double>((size_t)nx * env_blocks(ncand));
+  ar.take<int64_t>((size_t)nx * env_blocks(ncand));
+  return ar.off;
+}
+
+dprc_status dprc_envelope_middle(const double* x, int32_t nx, int32_t k, int32_t d, int32_t n_lambda,
+                                 double* best, int32_t* arg, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!x || !best || nx < 1 || nx > 65535 || k < 1 || d < 2 || (int64_t)k * d >= ((int64_t)1 << 31) ||
+      n_lambda < 1 || n_lambda > 4096)
+    return DPRC_ERROR_INVALID_VALUE;
+  const size_t need = dprc_envelope_middle_workspace(nx, d, n_lambda);
+  if (ws_bytes < need) return DPRC_ERROR_WORKSPACE_TOO_SMALL;
+  if (!ws || !aligned(ws, kAlign) || !aligned(x, 8) || !aligned(best, 8) || (arg && !aligned(arg, 4)))
+    return DPRC_ERROR_INVALID_VALUE;
+  EnvArgs a;
+  a.x = x; a.nx = nx; a.k = k; a.d = d; a.n_lambda = n_lambda;
+  a.ncand = (int64_t)d * (d - 1) / 2 * n_lambda;
+  a.panels = 16;
+  gauss_legendre(kEnvNodes, a.gx, a.gw);
+  Arena ar(ws);
+  const int nblk = env_blocks(a.ncand);
+  a.part_v = ar.take<double>((size_t)nx * nblk);
+  a.part_c = ar.take<int64_t>((size_t)nx * nblk);
+  a.best = best; a.arg = arg;
+  return hip_status(traced(DPRC_KERNEL_ENVELOPE, stream, [&] { return launch_env_middle(a, stream); }));
+}
+
+dprc_status dprc_chi2_cdf(const double* x, int64_t n, double dof, double scale, double* out, hipStream_t stream) {
+  if (!x || !out || n < 0 || !(dof > 0.0) || !std::isfinite(dof) || !(scale > 0.0) || !std::isfinite(scale))
+    return DPRC_ERROR_INVALID_VALUE;
+  if (!aligned(x, 8) || !aligned(out, 8)) return DPRC_ERROR_INVALID_VALUE;
+  return hip_status(traced(DPRC_KERNEL_CHI2_CDF, stream, [&] { return launch_chi2_cdf(x, n, dof, scale, out, stream); }));
 }
 
 dprc_status dprc_probe_gaussian(uint64_t seed, uint32_t layer_id, int64_t m, int32_t k, float* out,

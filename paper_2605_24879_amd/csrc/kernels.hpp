@@ -183,6 +183,23 @@ int32_t final_chunks(int64_t n);
 hipError_t launch_probe_bits(int probe_kind, uint32_t key0, uint32_t key1, uint32_t layer,
                              uint32_t stream_id, int64_t m, int32_t k, uint32_t* out,
                              hipStream_t st);
+// MiddleRegionCDF over a batch of points (see dprc_envelope_middle).
+constexpr int kEnvNodes = 16;
+struct EnvArgs {
+  const double* x;
+  int32_t nx, k, d, n_lambda;
+  int64_t ncand;          // d (d - 1) / 2 * n_lambda
+  int32_t panels;
+  double gx[kEnvNodes], gw[kEnvNodes];   // Gauss-Legendre nodes and weights on [-1, 1]
+  double* part_v;         // [nx][blocks]
+  int64_t* part_c;
+  double* best;           // [nx]
+  int32_t* arg;           // [nx][3] or null
+};
+int env_blocks(int64_t ncand);
+hipError_t launch_env_middle(const EnvArgs& a, hipStream_t st);
+hipError_t launch_chi2_cdf(const double* x, int64_t n, double dof, double scale, double* out, hipStream_t st);
+
 // One private AdamW step on a [d, p] fp32 master (see dprc_private_adamw).
 struct AdamArgs {
   float* theta;

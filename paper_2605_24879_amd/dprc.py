@@ -24,7 +24,8 @@ STREAM_PROBE, STREAM_SKETCH, STREAM_NOISE = 0, 1, 2
 
 EXPORTS = ["dprc_norm_hutch_workspace", "dprc_norm_hutch", "dprc_norm_hutchpp_workspace",
            "dprc_norm_hutchpp", "dprc_clip_scale", "dprc_clip_accumulate_workspace",
-           "dprc_clip_accumulate", "dprc_add_noise", "dprc_probe_bits", "dprc_probe_gaussian", "dprc_private_adamw", "dprc_status_string",
+           "dprc_clip_accumulate", "dprc_add_noise", "dprc_probe_bits", "dprc_probe_gaussian", "dprc_private_adamw", "dprc_envelope_middle_workspace",
+           "dprc_envelope_middle", "dprc_chi2_cdf", "dprc_status_string",
            "dprc_version", "dprc_trace_launches"]
 
 
@@ -66,6 +67,9 @@ def lib():
             "dprc_add_noise": (ctypes.c_int, [P, I64, F, F, U64, U32, P]),
             "dprc_probe_bits": (ctypes.c_int, [ctypes.c_int, U64, U32, U32, I64, I32, P, P]),
             "dprc_probe_gaussian": (ctypes.c_int, [U64, U32, I64, I32, P, P]),
+            "dprc_envelope_middle_workspace": (SZ, [I32, I32, I32]),
+            "dprc_envelope_middle": (ctypes.c_int, [P, I32, I32, I32, I32, P, P, P, SZ, P]),
+            "dprc_chi2_cdf": (ctypes.c_int, [P, I64, ctypes.c_double, ctypes.c_double, P, P]),
             "dprc_private_adamw": (ctypes.c_int, [P, P, P, I64, P, I64, I64, I64, F, F, U64, U32, F,
                                                   ctypes.POINTER(AdamWParams), P, I64, P]),
             "dprc_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -221,6 +225,28 @@ def dprc_private_adamw(theta, m, v, G, sigma, C, seed, tensor_id, inv_batch, lr,
     return theta
 
 
+def dprc_envelope_middle(x, k, d, n_lambda):
+    """MiddleRegionCDF at the points x (fp64 device tensor): (best [nx], arg [nx, 3] = i, j, l)."""
+    x = x.contiguous()
+    nx = x.numel()
+    best = torch.empty(nx, dtype=torch.float64, device=x.device)
+    arg = torch.empty(nx, 3, dtype=torch.int32, device=x.device)
+    need = lib().dprc_envelope_middle_workspace(nx, d, n_lambda)
+    ws = _workspace(need, x.device, None)
+    _check(lib().dprc_envelope_middle(x.data_ptr(), nx, k, d, n_lambda, best.data_ptr(), arg.data_ptr(),
+                                      ws.data_ptr(), need, _stream(x.device)))
+    return best, arg
+
+
+def dprc_chi2_cdf(x, dof, scale=1.0):
+    """P(chi^2(dof) <= x * scale) elementwise (fp64 device tensor)."""
+    x = x.contiguous()
+    out = torch.empty_like(x)
+    _check(lib().dprc_chi2_cdf(x.data_ptr(), x.numel(), float(dof), float(scale), out.data_ptr(),
+                               _stream(x.device)))
+    return out
+
+
 def dprc_probe_bits(probe, seed, layer_id, stream_id, m, k, device="cuda", out=None):
     """Packed probe words [k, ceil(m/32)] (int32 view of the uint32 words)."""
     nw = (m + 31) // 32
@@ -246,7 +272,7 @@ KERNEL_NAMES = {1: "project", 2: "token_reduce", 3: "qr", 4: "hutchpp_final", 5:
                 6: "accumulate", 7: "splitk_reduce", 8: "noise", 9: "probe_bits", 10: "project_f32",
                 11: "token_reduce_f32", 12: "sample_sq", 13: "accumulate_f32",
                 14: "token_splits", 15: "sample_sum", 16: "qr_combine", 17: "qr_expand", 18: "hutchpp_sum",
-                19: "probe_gauss", 20: "adamw"}
+                19: "probe_gauss", 20: "adamw", 21: "envelope", 22: "chi2_cdf"}
 
 
 def dprc_trace_launches(events_ptr, kinds_ptr, capacity, count_ptr):

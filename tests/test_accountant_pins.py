@@ -88,6 +88,13 @@ def test_x_plus_asymptotic_d2(k):
     assert abs((xp - 1.0) / (2.0 / (2 * k)) - 1.0) < 2e-3
 
 
+@pytest.mark.parametrize("k,d", [(16, 3), (64, 3), (16, 4)])
+def test_x_plus_remainder_is_order_inverse_k_squared(k, d):
+    # x_+ = 1 + 2/(dk) + O(1/k^2); the remainder times k^2 stays bounded (about 1 to 2.5 here)
+    xp = ac.x_plus(k, d, tol=1e-8, n_lambda=51)
+    assert 0.0 < (xp - 1.0 - 2.0 / (d * k)) * k * k < 4.0
+
+
 def _gauss_eps(mu, delta):
     return optimize.brentq(lambda e: ac.gaussian_delta(e, mu) - delta, 0.0, 100.0)
 
