@@ -187,23 +187,26 @@ def cpu_baseline(cfg, sets, budget_s):
     done_tokens = 0
     pairs = []
     t0 = time.perf_counter()
-    for (A, E, li) in layers:
-        _, d, p = cfg["layers"][li]
-        for i in range(B):
-            Ai = A[i].float().cpu().numpy().astype(np.float64)
-            Ei = E[i].float().cpu().numpy().astype(np.float64)
-            if cfg["estimator"] == "hutch":
-                kind = cfg.get("probe", "rademacher")
-                Z = est.probe_matrix(kind, 0, li, 0, p, cfg["k"])
-                est.hutch_layer(Ai[None], Ei[None], cfg["k"], 0, li, probe=kind, Z=Z)
-            else:
-                est.hutchpp_layer(Ai[None], Ei[None], cfg["s"], cfg["r"], 0, li)
-            done_tokens += T
-            pairs.append(f"{cfg['layers'][li][0]}[{i}]")
+    # (layer, sample) pairs in order, cycled until the budget is spent (small workloads finish a
+    # pass in well under a second)
+    while time.perf_counter() - t0 <= budget_s:
+        for (A, E, li) in layers:
+            _, d, p = cfg["layers"][li]
+            for i in range(B):
+                Ai = A[i].float().cpu().numpy().astype(np.float64)
+                Ei = E[i].float().cpu().numpy().astype(np.float64)
+                if cfg["estimator"] == "hutch":
+                    kind = cfg.get("probe", "rademacher")
+                    Z = est.probe_matrix(kind, 0, li, 0, p, cfg["k"])
+                    est.hutch_layer(Ai[None], Ei[None], cfg["k"], 0, li, probe=kind, Z=Z)
+                else:
+                    est.hutchpp_layer(Ai[None], Ei[None], cfg["s"], cfg["r"], 0, li)
+                done_tokens += T
+                pairs.append(f"{cfg['layers'][li][0]}[{i}]")
+                if time.perf_counter() - t0 > budget_s:
+                    break
             if time.perf_counter() - t0 > budget_s:
                 break
-        if time.perf_counter() - t0 > budget_s:
-            break
     dt = time.perf_counter() - t0
     info = threadpool_info()
     threads = max([x.get("num_threads", 1) for x in info] or [1])
@@ -211,8 +214,9 @@ def cpu_baseline(cfg, sets, budget_s):
     layer_tokens = B * T * len(cfg["layers"])
     return {"value": done_tokens / dt * (B * T) / layer_tokens, "unit": "tokens/s", "cores": threads,
             "kind": "oracle",
-            "sample": f"fp64 explicit per-sample gradients + Hutchinson for {len(pairs)} (layer, sample) pairs "
-                      f"({', '.join(pairs[:6])}{'...' if len(pairs) > 6 else ''}) in {dt:.1f} s; "
+            "sample": f"fp64 explicit per-sample gradients + Hutchinson for {len(pairs)} (layer, sample) pair "
+                      f"evaluations ({', '.join(pairs[:6])}{'...' if len(pairs) > 6 else ''}; pairs cycled in "
+                      f"order until the budget was spent) in {dt:.1f} s; "
                       f"blas={','.join(sorted(set(x.get('internal_api', '?') for x in info))) or 'unknown'}, "
                       f"os.cpu_count={os.cpu_count()}, affinity={len(os.sched_getaffinity(0))}"}
 

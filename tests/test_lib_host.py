@@ -19,7 +19,7 @@ pytestmark = pytest.mark.skipif(not os.path.exists(dprc.LIB_PATH), reason="libdp
 def declared_functions():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(dprc_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(dprc_[a-z0-9_]+)\s*\(", text)))
 
 
 def test_every_declared_symbol_is_exported():
