@@ -143,6 +143,7 @@ def _shared_a(B, T, d, ps, layer0=0):
     (3, 130, 136, (520, 520), 5, "rademacher"),         # gate/up-like pair, k not a multiple of 16
     (2, 700, 256, (200, 100, 64, 48, 30), 16, "rademacher"),   # five sharing layers -> groups of 4 and 1
     (2, 96, 64, (128, 40, 72), 100, "rademacher"),      # 3k > 256 columns -> groups of 2 and 1
+    (2, 100, 64, (1100, 600), 16, "rademacher"),        # wide, unequal sketched sides in one group
     (2, 150, 520, (96, 260), 7, "gaussian"),
 ])
 def test_hutch_shared_activations(D, B, T, d, ps, k, probe):
@@ -175,6 +176,15 @@ def test_hutch_shared_activations_mixed_sides(D):
     for j, E in enumerate(Es):
         ref = est.hutch_layer(_np(A), _np(E), 16, 2, 40 + j, side=2)
         assert np.all(_rel(n2l[j].cpu().numpy(), ref) < NORM_RTOL), j
+
+
+@pytest.mark.parametrize("B,T,p,k", [(1, 64, 4100, 16), (2, 40, 2600, 5), (1, 200, 4096, 32)])
+def test_hutch_few_rows_wide_sketch(D, B, T, p, k):
+    # few token rows and a wide sketched side (many 512-column stages per workgroup, ragged end)
+    A, E = _draw(B, T, 72, p, layer=9)
+    n2 = D.dprc_norm_hutch([(A, E, 3)], k, 5)
+    ref = est.hutch_layer(_np(A), _np(E), k, 5, 3)
+    assert np.all(_rel(n2.cpu().numpy(), ref) < NORM_RTOL)
 
 
 def test_hutch_tiny_workload_fp32(D):
