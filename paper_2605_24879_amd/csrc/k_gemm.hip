@@ -1,13 +1,16 @@
 // Clipped accumulation grad = sum_i c_i A_i^T E_i (Algorithm 1, second backward
 // pass of a bias-free linear layer) on bf16 matrix cores, fp32 accumulation.
 //
-// Workgroup tile 256 (d) x 256 (p), eight waves of 128 x 64, each a 4 x 2 grid of
-// v_mfma_f32_32x32x16_bf16 (128 fp32 accumulators per lane).  The contraction
-// runs over tokens and both operands are token-major, so 32-token slabs of A and E
-// (256 columns each, 512-byte rows) are loaded with coalesced 16-byte reads,
-// double-buffered through LDS and read back token-contiguous with the LDS
-// transpose read.  A 128 x 64 wave tile reads 24 bytes of LDS per 1024 MFMA flops
-// (a 64 x 64 tile needs 32), and two waves per SIMD overlap loads with MFMAs.
+// Workgroup tile 256 (d) x 256 (p), four waves of 128 x 128, each a 4 x 4 grid of
+// v_mfma_f32_32x32x16_bf16 (256 fp32 accumulators per lane).  The contraction runs
+// over tokens and both operands are token-major, so 32-token slabs of A and E (256
+// columns each, 512-byte rows) are loaded with coalesced 16-byte buffer reads, two
+// slabs ahead in registers, double-buffered through LDS and read back
+// token-contiguous with the LDS transpose read.  A 128 x 128 wave tile reads 16
+// bytes of LDS per 1024 MFMA flops.  With one wave per SIMD the matrix cores idle
+// whenever the wave waits, so each step is software-pipelined over the two
+// 16-token halves of a slab and its LDS reads, LDS writes and global loads are
+// interleaved with the MFMAs.
 //
 // Per-sample factors scale the fp32 accumulator at sample boundaries
 // (acc <- acc * c_prev / c_i, and * c_last at the end), so the result is
@@ -37,6 +40,19 @@ template <int V>
 struct GInt {
   static constexpr int value = V;
 };
+
+// Instruction order of one phase of a step: NM MFMAs, each followed by one LDS read
+// (NR of them) and, after every second MFMA, one instruction of the phase's other
+// kind (MASK: 0x200 LDS writes, 0x020 global loads; OTH of them).
+template <int NM, int NR, int MASK, int OTH>
+__device__ __forceinline__ void sched_phase() {
+#pragma unroll
+  for (int q = 0; q < NM; ++q) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    if (q < NR) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    if (q % 2 == 1 && q / 2 < OTH) __builtin_amdgcn_sched_group_barrier(MASK, 1, 0);
+  }
+}
 
 template <int NW, int NS, bool FAST>
 __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmArgs a) {
@@ -117,25 +133,29 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmArgs a) {
 
   // the lane's transpose-read offsets: rows 8*(g/2) + r4 (+4), columns 16*(g%2) + 4*c4
   const int tr_row = 8 * (g >> 1) + r4, tr_col = 16 * (g & 1) + 4 * c4;
-  auto slab = [&](int buf) __attribute__((always_inline)) {
+  // The two 16-token halves of a slab are separate register fragment sets (f0, f1):
+  // a step multiplies half 0 while reading half 1 and writing the next slab to the
+  // other LDS buffer, then (after the step's one barrier) multiplies half 1 while
+  // reading half 0 of the next slab.  LDS reads, LDS writes and global loads are
+  // placed between the MFMAs (sched_phase), so the matrix cores rarely wait.
+  uint4 f0a[4], f0b[YB], f1a[4], f1b[YB];
+  auto frag = [&](uint4 (&av)[4], uint4 (&bv)[YB], int buf, int ks) __attribute__((always_inline)) {
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      uint4 av[4], bv[YB];
-#pragma unroll
-      for (int x = 0; x < 4; ++x) {
-        const uint16_t* pa = &la[buf][(16 * ks + tr_row) * kGLd + wm * 128 + 32 * x + tr_col];
-        av[x] = make_u4(lds_read_tr16(pa), lds_read_tr16(pa + 4 * kGLd));
-      }
-#pragma unroll
-      for (int y = 0; y < YB; ++y) {
-        const uint16_t* pe = &le[buf][(16 * ks + tr_row) * kGLd + wn * WN + 32 * y + tr_col];
-        bv[y] = make_u4(lds_read_tr16(pe), lds_read_tr16(pe + 4 * kGLd));
-      }
-#pragma unroll
-      for (int x = 0; x < 4; ++x)
-#pragma unroll
-        for (int y = 0; y < YB; ++y) acc[x][y] = mfma32x32x16(av[x], bv[y], acc[x][y]);
+    for (int x = 0; x < 4; ++x) {
+      const uint16_t* pa = &la[buf][(16 * ks + tr_row) * kGLd + wm * 128 + 32 * x + tr_col];
+      av[x] = make_u4(lds_read_tr16(pa), lds_read_tr16(pa + 4 * kGLd));
     }
+#pragma unroll
+    for (int y = 0; y < YB; ++y) {
+      const uint16_t* pe = &le[buf][(16 * ks + tr_row) * kGLd + wn * WN + 32 * y + tr_col];
+      bv[y] = make_u4(lds_read_tr16(pe), lds_read_tr16(pe + 4 * kGLd));
+    }
+  };
+  auto mm = [&](const uint4 (&av)[4], const uint4 (&bv)[YB]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+      for (int y = 0; y < YB; ++y) acc[x][y] = mfma32x32x16(av[x], bv[y], acc[x][y]);
   };
 
   // samples of this split in order; the accumulator is rescaled between samples
@@ -165,13 +185,23 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmArgs a) {
     for (int q = 0; q < NS; ++q) gload(q, i, st_lo + q, st_hi);
     swrite(0, 0);
     __syncthreads();
+    frag(f0a, f0b, 0, 0);
     auto step = [&](int st, auto u) __attribute__((always_inline)) {
       constexpr int k = decltype(u)::value;      // step index modulo 2 NS
+      // phase A: loads of slab k + NS (register slot k % NS, free since slab k went to
+      // LDS); MFMAs of half 0 of slab k while reading its half 1 and writing slab k + 1
+      // (slot (k + 1) % NS) to the other buffer
       gload(k % NS, i, st + NS, st_hi);
-      __builtin_amdgcn_sched_barrier(0);           // keep the loads ahead of the step's MFMAs
-      slab(k % 2);
+      frag(f1a, f1b, k % 2, 1);
+      mm(f0a, f0b);
       swrite((k + 1) % NS, (k + 1) % 2);
+      sched_phase<4 * YB, 2 * (4 + YB), 0x200, 2 * RQ>();
       __syncthreads();
+      // phase B: MFMAs of half 1 of slab k while reading half 0 of slab k + 1; the next
+      // step's loads fall into this phase's MFMAs
+      frag(f0a, f0b, (k + 1) % 2, 0);
+      mm(f1a, f1b);
+      sched_phase<4 * YB, 2 * (4 + YB), 0x020, 2 * RQ>();
     };
     // whole groups of 2 NS steps in the loop (no early exit reaches its back edge,
     // so the compiler's wait counting stays exact), the remainder after it
@@ -185,10 +215,6 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmArgs a) {
         step(st + 4, GInt<4>{});
         step(st + 5, GInt<5>{});
       }
-      if constexpr (NS > 3) {
-        step(st + 6, GInt<6>{});
-        step(st + 7, GInt<7>{});
-      }
     }
     if (st < st_hi) step(st, GInt<0>{});
     if (st + 1 < st_hi) step(st + 1, GInt<1>{});
@@ -197,10 +223,7 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmArgs a) {
       if (st + 3 < st_hi) step(st + 3, GInt<3>{});
       if (st + 4 < st_hi) step(st + 4, GInt<4>{});
     }
-    if constexpr (NS > 3) {
-      if (st + 5 < st_hi) step(st + 5, GInt<5>{});
-      if (st + 6 < st_hi) step(st + 6, GInt<6>{});
-    }
+    __syncthreads();                               // the last reads of both buffers are done
   }
 
   // epilogue: lane holds rows 8*(q/4) + 4*(lane/32) + q%4 and column lane%32 of each 32 x 32 block
