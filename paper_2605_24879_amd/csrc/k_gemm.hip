@@ -1,16 +1,16 @@
 // Clipped accumulation grad = sum_i c_i A_i^T E_i (Algorithm 1, second backward
 // pass of a bias-free linear layer) on bf16 matrix cores, fp32 accumulation.
 //
-// Workgroup tile 256 (d) x 256 (p), four waves of 128 x 128, each a 4 x 4 grid of
-// v_mfma_f32_32x32x16_bf16 (256 fp32 accumulators per lane).  The contraction runs
-// over tokens and both operands are token-major, so 32-token slabs of A and E (256
-// columns each, 512-byte rows) are loaded with coalesced 16-byte buffer reads, two
-// slabs ahead in registers, double-buffered through LDS and read back
-// token-contiguous with the LDS transpose read.  A 128 x 128 wave tile reads 16
-// bytes of LDS per 1024 MFMA flops.  With one wave per SIMD the matrix cores idle
-// whenever the wave waits, so each step is software-pipelined over the two
-// 16-token halves of a slab and its LDS reads, LDS writes and global loads are
-// interleaved with the MFMAs.
+// Workgroup tile 256 (d) x 256 (p), eight waves of 128 x 64 (two per SIMD), each a
+// 4 x 2 grid of v_mfma_f32_32x32x16_bf16 (128 fp32 accumulators per lane).  The
+// contraction runs over tokens and both operands are token-major, so 32-token
+// slabs of A and E (256 columns each, 512-byte rows) are loaded with coalesced
+// 16-byte buffer reads, two slabs ahead in registers, double-buffered through LDS
+// and read back token-contiguous with the LDS transpose read.  Each step is
+// software-pipelined over the two 16-token halves of a slab, and the two waves of
+// a SIMD cover each other's waits (one wave of 128 x 128 per SIMD with the same
+// pipeline, or with LDS reads, writes and loads placed between the MFMAs by
+// scheduling barriers, was 7 to 10 percent slower).
 //
 // Per-sample factors scale the fp32 accumulator at sample boundaries
 // (acc <- acc * c_prev / c_i, and * c_last at the end), so the result is
@@ -40,19 +40,6 @@ template <int V>
 struct GInt {
   static constexpr int value = V;
 };
-
-// Instruction order of one phase of a step: NM MFMAs, each followed by one LDS read
-// (NR of them) and, after every second MFMA, one instruction of the phase's other
-// kind (MASK: 0x200 LDS writes, 0x020 global loads; OTH of them).
-template <int NM, int NR, int MASK, int OTH>
-__device__ __forceinline__ void sched_phase() {
-#pragma unroll
-  for (int q = 0; q < NM; ++q) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    if (q < NR) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    if (q % 2 == 1 && q / 2 < OTH) __builtin_amdgcn_sched_group_barrier(MASK, 1, 0);
-  }
-}
 
 template <int NW, int NS, bool FAST>
 __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmArgs a) {
@@ -136,8 +123,8 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmArgs a) {
   // The two 16-token halves of a slab are separate register fragment sets (f0, f1):
   // a step multiplies half 0 while reading half 1 and writing the next slab to the
   // other LDS buffer, then (after the step's one barrier) multiplies half 1 while
-  // reading half 0 of the next slab.  LDS reads, LDS writes and global loads are
-  // placed between the MFMAs (sched_phase), so the matrix cores rarely wait.
+  // reading half 0 of the next slab, so a wave always has MFMAs whose operands are
+  // already in registers.
   uint4 f0a[4], f0b[YB], f1a[4], f1b[YB];
   auto frag = [&](uint4 (&av)[4], uint4 (&bv)[YB], int buf, int ks) __attribute__((always_inline)) {
 #pragma unroll
@@ -195,13 +182,10 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmArgs a) {
       frag(f1a, f1b, k % 2, 1);
       mm(f0a, f0b);
       swrite((k + 1) % NS, (k + 1) % 2);
-      sched_phase<4 * YB, 2 * (4 + YB), 0x200, 2 * RQ>();
       __syncthreads();
-      // phase B: MFMAs of half 1 of slab k while reading half 0 of slab k + 1; the next
-      // step's loads fall into this phase's MFMAs
+      // phase B: MFMAs of half 1 of slab k while reading half 0 of slab k + 1
       frag(f0a, f0b, (k + 1) % 2, 0);
       mm(f1a, f1b);
-      sched_phase<4 * YB, 2 * (4 + YB), 0x020, 2 * RQ>();
     };
     // whole groups of 2 NS steps in the loop (no early exit reaches its back edge,
     // so the compiler's wait counting stays exact), the remainder after it
@@ -271,7 +255,7 @@ GemmPlan gemm_plan_v2(int64_t B, int64_t T, int64_t d, int64_t p) {
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t st) {
   const int tiles = (int)(ceil_div(a.d, kGM) * ceil_div(a.p, kGM));
   dim3 grid((unsigned)tiles, (unsigned)a.S);
-  constexpr int NW = 4, NS = 2;
+  constexpr int NW = 8, NS = 2;
   // buffer offsets within one 32-row slab stay below 2^31
   if (a.vec_a && a.vec_e && a.d % 8 == 0 && a.p % 8 == 0 &&
       (int64_t)kGK * std::max(a.lda, a.lde) * 2 < ((int64_t)1 << 31))
