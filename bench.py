@@ -103,11 +103,11 @@ def step_fn(cfg, D, torch, ws_norm, grads, ws_acc):
     probe = probe_id(D, cfg)
 
     def step(layers, n2, c):
-        if cfg["estimator"] == "hutch":
-            D.dprc_norm_hutch(layers, cfg["k"], 0, n2=n2, ws=ws_norm, probe=probe)
+        if cfg["estimator"] == "hutch":       # norms and clip factors in the same launches
+            D.dprc_norm_hutch_clip(layers, cfg["k"], 0, C, n2=n2, c=c, ws=ws_norm, probe=probe)
         else:
             D.dprc_norm_hutchpp(layers, cfg["s"], cfg["r"], 0, n2=n2, ws=ws_norm)
-        D.dprc_clip_scale(n2, C, c=c)
+            D.dprc_clip_scale(n2, C, c=c)
         if cfg["accumulate"]:
             for (A, E, li), g in zip(layers, grads):
                 D.dprc_clip_accumulate(A, E, c, grad=g, ws=ws_acc)
@@ -430,8 +430,7 @@ def run_llama_step(args, torch, D):
         losses, pairs = drv.capture(loss_fn)
         mark(1)
         key = dpsgd.step_seed(0, drv.steps)
-        n2 = D.dprc_norm_hutch(pairs, k, key)
-        c = D.dprc_clip_scale(n2, C)
+        n2, c = D.dprc_norm_hutch_clip(pairs, k, key, C)
         mark(2)
         grads = [D.dprc_clip_accumulate(A, E, c, ws=drv._ws_acc) for (A, E, _) in pairs]
         mark(3)

@@ -110,6 +110,15 @@ dprc_status dprc_norm_hutch(const dprc_layer* layers, int32_t num_layers, int32_
                             float* n2_layers, int32_t accumulate, void* ws, size_t ws_bytes,
                             hipStream_t stream);
 
+/* Hutchinson estimates followed by the clip factors of Algorithm 1 in the same
+ * launches: as dprc_norm_hutch, then c[i] = the dprc_clip_scale factor of the
+ * final n2[i] (bitwise the same as calling dprc_clip_scale on n2).  C > 0 and
+ * finite; c [B] device.  Workspace: dprc_norm_hutch_workspace(). */
+dprc_status dprc_norm_hutch_clip(const dprc_layer* layers, int32_t num_layers, int32_t k,
+                                 dprc_probe probe, uint64_t seed, dprc_side side, float C, float* n2,
+                                 float* c, float* n2_layers, int32_t accumulate, void* ws,
+                                 size_t ws_bytes, hipStream_t stream);
+
 /* ---- Hutch++ (Algorithm 2, Hutch++ branch; estimator section) --------------
  * With M_i = X'_i^T X_i (m probed columns): sketch O S = M_i^T (M_i S) with s
  * sketch probes (stream 1), Q = orthonormal basis of its columns (Householder

@@ -224,6 +224,7 @@ dprc_status run_pass(const PassSpec& ps, int64_t B, int64_t T, uint32_t k0, uint
   ta.Yt = Yt; ta.yt_ld = B * tp.T_pad; ta.T_pad = tp.T_pad; ta.ncols = ncols; ta.ncols_pad = ncols_pad;
   ta.ntiles = tp.ntiles; ta.S = tp.S; ta.stages_per_split = tp.sps;
   ta.mode = ps.mode; ta.seg = ncols; ta.nseg = 1;
+  ta.clip_C = 0.f; ta.clip_c = nullptr;
   ta.part = tb.part; ta.tilesq = tb.tilesq;
   ta.scale = ps.scale; ta.n2 = ps.n2; ta.n2_layer = ps.n2_layer; ta.accumulate = ps.accumulate;
   ta.M = ps.M; ta.m_ld = ps.m_ld; ta.m_ss = (int64_t)ncols * ps.m_ld;
@@ -337,8 +338,13 @@ dprc_status hutch_f32(const View& v, int32_t k, int probe, uint32_t k0, uint32_t
 // G layers (G = 1, or a shared-activation group of bf16 OUT layers): one projection
 // per layer into its columns of a shared Y, then one token reduction.
 dprc_status hutch_group(const View* v, int G, int32_t k, int probe, uint32_t k0, uint32_t k1, float* n2,
-                        float* n2_layers, int accumulate, void* ws, hipStream_t st) {
-  if (v[0].dtype != DPRC_BF16) return hutch_f32(v[0], k, probe, k0, k1, n2, n2_layers, accumulate, ws, st);
+                        float* n2_layers, int accumulate, void* ws, hipStream_t st, float clipC = 0.f,
+                        float* clip_c = nullptr) {
+  if (v[0].dtype != DPRC_BF16) {
+    dprc_status s = hutch_f32(v[0], k, probe, k0, k1, n2, n2_layers, accumulate, ws, st);
+    if (s != DPRC_SUCCESS || !clip_c) return s;
+    return hip_status(traced(DPRC_KERNEL_CLIP_SCALE, st, [&] { return launch_clip_scale(n2, v[0].B, clipC, clip_c, st); }));
+  }
   const bool gauss = probe == DPRC_PROBE_GAUSSIAN;
   const int64_t B = v[0].B, T = v[0].T;
   Arena ar(ws);
@@ -381,6 +387,7 @@ dprc_status hutch_group(const View* v, int G, int32_t k, int probe, uint32_t k0,
   ta.mode = 0; ta.seg = k; ta.nseg = G;
   ta.part = tb.part; ta.tilesq = tb.tilesq;
   ta.scale = 1.0f / (float)k; ta.n2 = n2; ta.n2_layer = n2_layers; ta.accumulate = accumulate;
+  ta.clip_C = clipC; ta.clip_c = clip_c;
   ta.vec = rows16(v[0].Xo, v[0].ldo);
   if ((e = traced(DPRC_KERNEL_TOKEN_REDUCE, st, [&] { return launch_tokred(ta, st); })) != hipSuccess) return DPRC_ERROR_HIP;
   if (tp.S > 1 && (e = traced(DPRC_KERNEL_TOKEN_SPLITS, st, [&] { return launch_tokred_splits(ta, st); })) != hipSuccess)
@@ -624,9 +631,9 @@ size_t dprc_norm_hutch_workspace(const dprc_layer* layers, int32_t num_layers, i
   return need;
 }
 
-dprc_status dprc_norm_hutch(const dprc_layer* layers, int32_t num_layers, int32_t k, dprc_probe probe,
-                            uint64_t seed, dprc_side side, float* n2, float* n2_layers, int32_t accumulate,
-                            void* ws, size_t ws_bytes, hipStream_t stream) {
+static dprc_status norm_hutch(const dprc_layer* layers, int32_t num_layers, int32_t k, dprc_probe probe,
+                              uint64_t seed, dprc_side side, float* n2, float* n2_layers, int32_t accumulate,
+                              void* ws, size_t ws_bytes, hipStream_t stream, float clipC, float* clip_c) {
   dprc_status s = check_layers(layers, num_layers, side);
   if (s != DPRC_SUCCESS) return s;
   if (k < 1 || k > 256 || !n2) return DPRC_ERROR_INVALID_VALUE;
@@ -643,12 +650,27 @@ dprc_status dprc_norm_hutch(const dprc_layer* layers, int32_t num_layers, int32_
   for (int32_t l = 0; l < num_layers;) {
     const int32_t le = group_end(layers, l, num_layers, k, side);
     for (int32_t j = l; j < le; ++j) v[j - l] = view_of(layers[j], side);
+    const bool last = le == num_layers;
     s = hutch_group(v, le - l, k, (int)probe, k0, k1, n2, n2_layers ? n2_layers + (int64_t)l * B : nullptr,
-                    (accumulate || l > 0) ? 1 : 0, ws, stream);
+                    (accumulate || l > 0) ? 1 : 0, ws, stream, clipC, last ? clip_c : nullptr);
     if (s != DPRC_SUCCESS) return s;
     l = le;
   }
   return DPRC_SUCCESS;
+}
+
+dprc_status dprc_norm_hutch(const dprc_layer* layers, int32_t num_layers, int32_t k, dprc_probe probe,
+                            uint64_t seed, dprc_side side, float* n2, float* n2_layers, int32_t accumulate,
+                            void* ws, size_t ws_bytes, hipStream_t stream) {
+  return norm_hutch(layers, num_layers, k, probe, seed, side, n2, n2_layers, accumulate, ws, ws_bytes, stream, 0.f,
+                    nullptr);
+}
+
+dprc_status dprc_norm_hutch_clip(const dprc_layer* layers, int32_t num_layers, int32_t k, dprc_probe probe,
+                                 uint64_t seed, dprc_side side, float C, float* n2, float* c, float* n2_layers,
+                                 int32_t accumulate, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!c || !(C > 0.f) || std::isinf(C)) return DPRC_ERROR_INVALID_VALUE;
+  return norm_hutch(layers, num_layers, k, probe, seed, side, n2, n2_layers, accumulate, ws, ws_bytes, stream, C, c);
 }
 
 size_t dprc_norm_hutchpp_workspace(const dprc_layer* layers, int32_t num_layers, int32_t s, int32_t r,

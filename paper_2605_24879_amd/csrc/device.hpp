@@ -184,6 +184,14 @@ __device__ __forceinline__ void box_muller(uint32_t x0, uint32_t x1, float& n0, 
   n1 = r * sn;
 }
 
+// c = min(1, C / sqrt(n)) for a summed squared-norm estimate n (Algorithm 1);
+// n = 0 gives 1, a NaN, negative or infinite n gives 0.
+__device__ __forceinline__ float clip_factor(float n, float C) {
+  if (!(n >= 0.f) || isinf(n)) return 0.f;
+  if (n <= C * C) return 1.f;
+  return C / sqrtf(n);
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);

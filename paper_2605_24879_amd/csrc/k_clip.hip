@@ -10,12 +10,7 @@ namespace dprc {
 __global__ void clip_scale_kernel(const float* n2, int64_t B, float C, float* c) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= B) return;
-  const float v = n2[i];
-  float r;
-  if (!(v >= 0.f) || isinf(v)) r = 0.f;       // NaN, negative, +inf
-  else if (v <= C * C) r = 1.f;
-  else r = C / sqrtf(v);
-  c[i] = r;
+  c[i] = clip_factor(n2[i], C);
 }
 
 hipError_t launch_clip_scale(const float* n2, int64_t B, float C, float* c, hipStream_t st) {

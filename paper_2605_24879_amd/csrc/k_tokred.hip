@@ -333,7 +333,10 @@ __global__ __launch_bounds__(kBlock) void tokred_sample_kernel(TokredArgs a) {
     n2 += est;
     if (threadIdx.x == 0 && a.n2_layer) a.n2_layer[(int64_t)g * a.B + i] = est;
   }
-  if (threadIdx.x == 0) a.n2[i] = n2;
+  if (threadIdx.x == 0) {
+    a.n2[i] = n2;
+    if (a.clip_c) a.clip_c[i] = clip_factor(n2, a.clip_C);
+  }
 }
 
 hipError_t launch_tokred_splits(const TokredArgs& a, hipStream_t st) {

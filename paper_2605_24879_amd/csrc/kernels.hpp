@@ -85,6 +85,8 @@ struct TokredArgs {
   float* n2;
   float* n2_layer;        // [nseg][B] (may be null)
   int32_t accumulate;
+  float clip_C;           // with clip_c: clip_c[i] = clip factor of the final n2[i]
+  float* clip_c;
   float* M;               // M[i*m_ss + c*m_ld + j]
   int64_t m_ld, m_ss;
   uint16_t* Mhi;          // Mhi/Mlo[i*mh_ss + c*mh_ld + j]

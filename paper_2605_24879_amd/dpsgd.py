@@ -112,10 +112,10 @@ class DPSGDRC:
         """Steps 3-6: n2 [B], c [B] and the clipped gradients ([d, p] fp32 per layer), with
         the noise added unless ``noise`` is false."""
         if self.estimator == "hutch":
-            n2 = D.dprc_norm_hutch(pairs, self.k, key, side=self.side, probe=self.probe)
+            n2, c = D.dprc_norm_hutch_clip(pairs, self.k, key, self.C, side=self.side, probe=self.probe)
         else:
             n2 = D.dprc_norm_hutchpp(pairs, self.s, self.r, key, side=self.side)
-        c = D.dprc_clip_scale(n2, self.C)
+            c = D.dprc_clip_scale(n2, self.C)
         need = max(D.dprc_clip_accumulate_workspace(A, E) for (A, E, _) in pairs)
         if self._ws_acc is None or self._ws_acc.numel() < need:
             self._ws_acc = torch.empty(max(need, 1), dtype=torch.uint8, device=n2.device)

@@ -187,6 +187,28 @@ def test_hutch_few_rows_wide_sketch(D, B, T, p, k):
     assert np.all(_rel(n2.cpu().numpy(), ref) < NORM_RTOL)
 
 
+@pytest.mark.parametrize("case", ["bf16", "shared", "gaussian", "fp32", "accumulate"])
+def test_hutch_clip_fused_matches_separate_calls(D, case):
+    C = 0.3
+    if case == "shared":
+        A, Es = _shared_a(3, 150, 200, (200, 64, 64))
+        pairs = [(A, E, j) for j, E in enumerate(Es)]
+    elif case == "fp32":
+        A, E = _draw(2, 64, 64, 48, dtype="f32", layer=2)
+        pairs = [(A, E, 0)]
+    else:
+        A, E = _draw(3, 130, 96, 300, layer=2)
+        pairs = [(A, E, 0)]
+    probe = D.PROBE_GAUSSIAN if case == "gaussian" else D.PROBE_RADEMACHER
+    prior = torch.tensor([0.5, 0.01, 2.0][:pairs[0][0].shape[0]], device="cuda")
+    acc = case == "accumulate"
+    n2f, cf = D.dprc_norm_hutch_clip(pairs, 16, 4, C, probe=probe, n2=prior.clone() if acc else None, accumulate=acc)
+    n2 = D.dprc_norm_hutch(pairs, 16, 4, probe=probe, n2=prior.clone() if acc else None, accumulate=acc)
+    c = D.dprc_clip_scale(n2, C)
+    assert torch.equal(n2f, n2) and torch.equal(cf, c)
+    assert np.allclose(cf.cpu().numpy(), est.clip_scale(n2.cpu().numpy().astype(np.float64), C), rtol=1e-6)
+
+
 def test_hutch_tiny_workload_fp32(D):
     cfg = workloads.BY_NAME["tiny"]
     A, E = workloads.layer_inputs(cfg, 0, device="cuda")

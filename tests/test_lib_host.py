@@ -154,3 +154,16 @@ def test_private_adamw_validation():
                 dprc.AdamWParams(1e-3, 0.9, 0.999, 0.0, 0.0, 1), dprc.AdamWParams(1e-3, 0.9, 0.999, 1e-8, 0.0, 0)):
         assert call(h=bad) == 1
     assert call(d=0) == 0                         # nothing to do, nothing enqueued
+
+
+def test_hutch_clip_validation():
+    L = dprc.lib()
+    arr = (dprc.Layer * 1)(_fake_layer())
+
+    def call(C=1.0, c=0x50000, ws_bytes=1 << 30):
+        return L.dprc_norm_hutch_clip(arr, 1, 4, 0, 0, 0, C, 0x40000, c, None, 0, 0x30000, ws_bytes, None)
+    assert call(C=0.0) == 1
+    assert call(C=float("inf")) == 1
+    assert call(c=None) == 1
+    need = L.dprc_norm_hutch_workspace(arr, 1, 4, 0, 0)
+    assert call(ws_bytes=need - 1) == 3
