@@ -49,6 +49,27 @@ __device__ __forceinline__ double readlane_f64(double v, int l) {
   return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
 }
 
+// x[l] + x[l ^ 16] (R = 16) or x[l] + x[l ^ 32] (R = 32) with the lane swaps of
+// gfx950: the swap returns the pair's two values in the same order on both lanes
+// (lane with the bit clear first), so both lanes form the same sum.
+template <int R>
+__device__ __forceinline__ double add_across(double x) {
+  const uint64_t u = (uint64_t)__double_as_longlong(x);
+  const uint32_t lo = (uint32_t)u, hi = (uint32_t)(u >> 32);
+  uint32_t l0, l1, h0, h1;
+  if constexpr (R == 16) {
+    const auto pl = __builtin_amdgcn_permlane16_swap(lo, lo, false, false);
+    const auto ph = __builtin_amdgcn_permlane16_swap(hi, hi, false, false);
+    l0 = pl[0]; l1 = pl[1]; h0 = ph[0]; h1 = ph[1];
+  } else {
+    const auto pl = __builtin_amdgcn_permlane32_swap(lo, lo, false, false);
+    const auto ph = __builtin_amdgcn_permlane32_swap(hi, hi, false, false);
+    l0 = pl[0]; l1 = pl[1]; h0 = ph[0]; h1 = ph[1];
+  }
+  return __longlong_as_double((long long)(((uint64_t)h0 << 32) | l0)) +
+         __longlong_as_double((long long)(((uint64_t)h1 << 32) | l1));
+}
+
 // v[c] <- sum over the 64 lanes of v[c], for c >= c_lo (c_lo a constant after
 // unrolling).  Lane sums go to LDS column by column; lane (c, g) adds the g-th
 // run of SP of them, and shuffles over the run bits finish the sum.
@@ -66,11 +87,18 @@ __device__ __forceinline__ void wave_vec_sum(double (&v)[SP], int c_lo, double* 
 #pragma unroll
     for (int q = 0; q < SP; ++q) t[q] = red[c * kRedLd + g * SP + q];
 #pragma unroll
-    for (int q = 0; q < SP; ++q) x += t[q];
+    for (int w = SP / 2; w >= 1; w >>= 1)        // pairwise tree
+#pragma unroll
+      for (int q = 0; q < w; ++q) t[q] += t[q + w];
+    x = t[0];
   }
 #pragma unroll
-  for (int e = 0; e < 6; ++e)
-    if ((SP << e) < 64) x += __shfl_xor(x, SP << e, 64);
+  for (int e = 0; e < 6; ++e) {
+    const int m = SP << e;
+    if (m == 16) x = add_across<16>(x);
+    else if (m == 32) x = add_across<32>(x);
+    else if (m < 64) x += __shfl_xor(x, m, 64);
+  }
   if (g == 0) tot[c] = x;
   qr_wave_fence();
 #pragma unroll
@@ -125,6 +153,17 @@ __global__ __launch_bounds__(64) void qr_factor_kernel(QrArgs a, int level) {
   double* tb = L.tau + ((int64_t)i * L.nblk + b) * s;
   const bool has_next = level + 1 < a.nlev;
   const QrLevel N = a.lev[has_next ? level + 1 : level];
+  // outputs stay in registers until the loop ends (a store costs the wave tens of
+  // cycles even with one lane active): v_k and tau_k enter register column SP - 1
+  // and move down one place per step, so after s steps column k sits at SP - s + k;
+  // lane k keeps row k of R (offset e from the diagonal in register column e)
+  double Vs[2][SP], Ts[SP], Rr[SP];
+#pragma unroll
+  for (int e = 0; e < SP; ++e) {
+    Vs[0][e] = Vs[1][e] = 0.0;
+    Ts[e] = 0.0;
+    Rr[e] = 0.0;
+  }
   for (int k = 0; k < s; ++k) {
     double pv[SP];
 #pragma unroll
@@ -158,21 +197,22 @@ __global__ __launch_bounds__(64) void qr_factor_kernel(QrArgs a, int level) {
         }
       }
     }
-    // v_k (zero above the diagonal; for a zero column the column itself, which is zero)
+    // v_k (zero above the diagonal; for a zero column the column itself, which is zero),
+    // tau_k, and row k of R (R_kk = alpha_k, R_k,k+e = A[0][e]) in lane k
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
       const int j = lane + 64 * u;
-      V[(int64_t)k * kQrRows + j] = j >= k ? A[u][0] : 0.0;
-    }
-    if (lane == 0) tb[k] = t;
-    // row k of R into row b*s + k of the next level's input: R_kk = alpha_k, R_kc (c > k)
-    if (has_next && lane == k) {
-      double* nm = N.M + (int64_t)i * s * N.rows + (int64_t)b * s + k;
-      nm[(int64_t)k * N.rows] = al;
 #pragma unroll
-      for (int c = 1; c < SP; ++c)
-        if (k + c < s) nm[(int64_t)(k + c) * N.rows] = A[0][c];
-      for (int c = 0; c < k; ++c) nm[(int64_t)c * N.rows] = 0.0;
+      for (int e = 0; e + 1 < SP; ++e) Vs[u][e] = Vs[u][e + 1];
+      Vs[u][SP - 1] = j >= k ? A[u][0] : 0.0;
+    }
+#pragma unroll
+    for (int e = 0; e + 1 < SP; ++e) Ts[e] = Ts[e + 1];
+    Ts[SP - 1] = t;
+    if (lane == k) {
+      Rr[0] = al;
+#pragma unroll
+      for (int e = 1; e < SP; ++e) Rr[e] = A[0][e];
     }
     // the remaining columns move down one register column
 #pragma unroll
@@ -180,6 +220,25 @@ __global__ __launch_bounds__(64) void qr_factor_kernel(QrArgs a, int level) {
 #pragma unroll
       for (int c = 0; c + 1 < SP; ++c) A[u][c] = A[u][c + 1];
       A[u][SP - 1] = 0.0;
+    }
+  }
+  // V (column k of the block at register column SP - s + k), tau, and the rows of R
+  // into rows b*s + q of the next level's input (zero left of the diagonal)
+#pragma unroll
+  for (int e = 0; e < SP; ++e) {
+    const int k = e - (SP - s);
+    if (k >= 0) {
+#pragma unroll
+      for (int u = 0; u < 2; ++u) V[(int64_t)k * kQrRows + lane + 64 * u] = Vs[u][e];
+      if (lane == 0) tb[k] = Ts[e];
+    }
+  }
+  if (has_next && lane < s) {
+    double* nm = N.M + (int64_t)i * s * N.rows + (int64_t)b * s + lane;
+#pragma unroll
+    for (int e = 0; e < SP; ++e) {
+      if (lane + e < s) nm[(int64_t)(lane + e) * N.rows] = Rr[e];
+      if (e >= 1 && e <= lane) nm[(int64_t)(lane - e) * N.rows] = 0.0;
     }
   }
 }
