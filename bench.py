@@ -130,6 +130,9 @@ def trace_kernels(hip, D, fn, reps, capacity=4096):
         torch.cuda.synchronize()
     finally:
         D.dprc_trace_launches(None, None, 0, None)
+    if count.value >= capacity:
+        hip.destroy(events)
+        raise RuntimeError(f"launch trace full ({capacity} launches): per-kernel figures would be wrong")
     out = []
     for j in range(count.value):
         out.append((D.KERNEL_NAMES.get(kinds[j], str(kinds[j])), hip.elapsed_ms(events[2 * j], events[2 * j + 1])))
@@ -348,7 +351,10 @@ def main():
     # per-kernel durations over the same number of steps, with the launch hook on
     hip = Hip()
     it = iter(range(10 ** 9))
-    recs = trace_kernels(hip, D, lambda: step(sets[next(it) % copies], n2, c), args.steps)
+    # one traced step sizes the trace (the stack workload launches several hundred kernels per step)
+    per_step = len(trace_kernels(hip, D, lambda: step(sets[0], n2, c), 1, capacity=1 << 14))
+    recs = trace_kernels(hip, D, lambda: step(sets[next(it) % copies], n2, c), args.steps,
+                         capacity=per_step * args.steps + 16)
     per_kind = {}
     for k, ms in recs:
         tot, cnt = per_kind.get(k, (0.0, 0))
