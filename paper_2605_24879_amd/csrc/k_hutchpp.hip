@@ -423,13 +423,17 @@ hipError_t launch_qr_expand(const QrArgs& a, int level, hipStream_t st) {
 }
 
 // ---- finalize -----------------------------------------------------------------------------------------
-constexpr int kFinRows = 256;
+// A workgroup takes 32 rows j of U | W_P; its threads are (row, column group): group
+// g handles the residual columns q = g, g + 8, ..., so a wave reads whole 128-byte
+// runs of a column and every row's residuals advance in parallel.
+constexpr int kFinRows = 32;                 // rows per workgroup
+constexpr int kFinGroups = kQrThreads / kFinRows;
 
 // C = sum of the block partials C_b, in block order (one thread per entry).
-__global__ __launch_bounds__(kFinRows) void hpp_csum_kernel(FinalArgs a) {
+__global__ __launch_bounds__(kQrThreads) void hpp_csum_kernel(FinalArgs a) {
   const int i = blockIdx.y;
   const int sr = a.s * a.r;
-  const int e = blockIdx.x * kFinRows + threadIdx.x;
+  const int e = blockIdx.x * kQrThreads + threadIdx.x;
   if (e >= sr) return;
   const double* cp = a.Cpart + (int64_t)i * a.nblk * sr + e;
   double v = 0.0;
@@ -445,39 +449,44 @@ __global__ __launch_bounds__(kFinRows) void hpp_csum_kernel(FinalArgs a) {
   a.C[(int64_t)i * sr + e] = v;
 }
 
-// Rows j of one chunk: ||U_j||^2 and ||W_P,j - U_j C||^2 summed over the chunk.
+// Rows of one chunk: ||U_j||^2 and ||W_P,j - U_j C||^2 summed over the chunk.
 template <int SP>
-__global__ __launch_bounds__(kFinRows) void hpp_rows_kernel(FinalArgs a) {
+__global__ __launch_bounds__(kQrThreads) void hpp_rows_kernel(FinalArgs a) {
   extern __shared__ __attribute__((aligned(16))) float fs[];
   __shared__ double sh[4];
   const int ch = blockIdx.x, i = blockIdx.y, tid = threadIdx.x;
   const int s = a.s, r = a.r;
   float* C = fs;                           // [s][r]
-  for (int e = tid; e < s * r; e += kFinRows) C[e] = (float)a.C[(int64_t)i * s * r + e];
+  for (int e = tid; e < s * r; e += kQrThreads) C[e] = (float)a.C[(int64_t)i * s * r + e];
   __syncthreads();
-  const int64_t j = (int64_t)ch * kFinRows + tid;
+  const int grp = tid / kFinRows;
+  const int64_t j = (int64_t)ch * kFinRows + (tid % kFinRows);
   double su = 0.0, sv = 0.0;
   if (j < a.n) {
     const float* uw = a.UW + (int64_t)i * a.uw_ss + j;
-    double u[SP];                                  // row j of U, loaded once
+    double u[SP];                                  // row j of U
 #pragma unroll
     for (int c = 0; c < SP; ++c) {
       const float x = uw[(int64_t)(c < s ? c : 0) * a.uw_ld];
       u[c] = c < s ? (double)x : 0.0;
-      su += u[c] * u[c];
+      if (grp == 0) su += u[c] * u[c];
     }
-    // residual columns 16 at a time: their loads are in flight together
-    for (int b0 = 0; b0 < r; b0 += 16) {
-      float w[16];
+    // residual columns of this group, four at a time: their loads are in flight together
+    for (int q0 = grp; q0 < r; q0 += 4 * kFinGroups) {
+      float w[4];
 #pragma unroll
-      for (int q = 0; q < 16; ++q) w[q] = uw[(int64_t)(s + (b0 + q < r ? b0 + q : 0)) * a.uw_ld];
+      for (int t = 0; t < 4; ++t) {
+        const int q = q0 + t * kFinGroups;
+        w[t] = uw[(int64_t)(s + (q < r ? q : 0)) * a.uw_ld];
+      }
 #pragma unroll
-      for (int q = 0; q < 16; ++q) {
-        if (b0 + q < r) {
-          double v = (double)w[q];
+      for (int t = 0; t < 4; ++t) {
+        const int q = q0 + t * kFinGroups;
+        if (q < r) {
+          double v = (double)w[t];
 #pragma unroll
           for (int c = 0; c < SP; ++c)
-            if (c < s) v -= u[c] * (double)C[c * r + b0 + q];
+            if (c < s) v -= u[c] * (double)C[c * r + q];
           sv += v * v;
         }
       }
@@ -511,15 +520,15 @@ __global__ __launch_bounds__(kQrThreads) void hpp_sum_kernel(FinalArgs a) {
 hipError_t launch_hpp_rows(const FinalArgs& a, hipStream_t st) {
   const dim3 grid((unsigned)a.nchunk, (unsigned)a.B);
   const size_t lds = (size_t)a.s * a.r * 4;
-  if (a.s <= 8) DPRC_LAUNCH(hpp_rows_kernel<8>, grid, dim3(kFinRows), lds, st, a);
-  else if (a.s <= 16) DPRC_LAUNCH(hpp_rows_kernel<16>, grid, dim3(kFinRows), lds, st, a);
-  else DPRC_LAUNCH(hpp_rows_kernel<32>, grid, dim3(kFinRows), lds, st, a);
+  if (a.s <= 8) DPRC_LAUNCH(hpp_rows_kernel<8>, grid, dim3(kQrThreads), lds, st, a);
+  else if (a.s <= 16) DPRC_LAUNCH(hpp_rows_kernel<16>, grid, dim3(kQrThreads), lds, st, a);
+  else DPRC_LAUNCH(hpp_rows_kernel<32>, grid, dim3(kQrThreads), lds, st, a);
   return hipGetLastError();
 }
 
 hipError_t launch_hpp_csum(const FinalArgs& a, hipStream_t st) {
-  DPRC_LAUNCH(hpp_csum_kernel, dim3((unsigned)ceil_div((int64_t)a.s * a.r, kFinRows), (unsigned)a.B),
-              dim3(kFinRows), 0, st, a);
+  DPRC_LAUNCH(hpp_csum_kernel, dim3((unsigned)ceil_div((int64_t)a.s * a.r, kQrThreads), (unsigned)a.B),
+              dim3(kQrThreads), 0, st, a);
   return hipGetLastError();
 }
 
