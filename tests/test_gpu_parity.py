@@ -268,6 +268,7 @@ def test_hutch_deterministic(D):
     (1, 200, 600, 96, 32, 16, 1, "bf16"),      # m = 600: 5 blocks -> 160 rows -> 2 -> 1 (3 levels)
     (2, 150, 64, 1100, 5, 7, 0, "bf16"),       # m = 1100: 9 blocks -> 45 rows -> 1
     (2, 100, 50, 260, 1, 3, 0, "bf16"),        # s = 1
+    (1, 180, 72, 130, 6, 40, 0, "bf16"),       # r = 40: the finalize's residual columns take two passes
 ])
 def test_hutchpp_parity(D, B, T, d, p, s, r, side, dtype):
     A, E = _draw(B, T, d, p, dtype=dtype, law="student_t", layer=2)
