@@ -410,7 +410,15 @@ struct PPBufs {
   void* pass_ws;                           // bf16 path: scratch of one pass
 };
 
-size_t hutchpp_layout(const View& v, int32_t s, int32_t r, void* ws, PPBufs* out) {
+// Bytes of the bf16 pass scratch of one layer (the Y buffer and token-split partials).
+size_t hpp_pass_bytes(const View& v, int32_t s, int32_t r) {
+  size_t need = std::max(pass_ws_bytes(v.B, v.T, v.n, std::max(s, 1)), pass_ws_bytes(v.B, v.T, v.m, std::max(s, 1)));
+  return std::max(need, pass_ws_bytes(v.B, v.T, v.n, s + r));
+}
+
+// Buffers of one layer carved from ws.  With own_pass false the bf16 pass scratch is
+// not reserved (layers of one call then share one, given by the caller).
+size_t hutchpp_layout(const View& v, int32_t s, int32_t r, void* ws, PPBufs* out, bool own_pass = true) {
   Arena ar(ws);
   PPBufs b{};
   const int64_t B = v.B;
@@ -446,11 +454,11 @@ size_t hutchpp_layout(const View& v, int32_t s, int32_t r, void* ws, PPBufs* out
     b.fin.C = ar.take<double>((size_t)B * s * r);
   }
   if (v.dtype == DPRC_BF16) {
-    b.pass_ws = ar.base ? ar.base + ((ar.off + kAlign - 1) / kAlign) * kAlign : nullptr;
-    ar.off = (ar.off + kAlign - 1) / kAlign * kAlign;
-    size_t need = std::max(pass_ws_bytes(B, v.T, v.n, std::max(s, 1)), pass_ws_bytes(B, v.T, v.m, std::max(s, 1)));
-    need = std::max(need, pass_ws_bytes(B, v.T, v.n, s + r));
-    ar.off += need;
+    if (own_pass) {
+      b.pass_ws = ar.base ? ar.base + ((ar.off + kAlign - 1) / kAlign) * kAlign : nullptr;
+      ar.off = (ar.off + kAlign - 1) / kAlign * kAlign;
+      ar.off += hpp_pass_bytes(v, s, r);
+    }
   } else {
     b.zb = ar.take<uint32_t>((size_t)std::max(s, r) * ceil_div(std::max(v.m, v.n), 32));
     b.Y32 = ar.take<float>((size_t)B * v.T * (s + r));
@@ -460,32 +468,76 @@ size_t hutchpp_layout(const View& v, int32_t s, int32_t r, void* ws, PPBufs* out
   return ar.off;
 }
 
-// Q = orth(O S) (a TSQR tree: factor launches up, expansion launches down), with C = Q^T P
-// formed alongside by the last expansion.
-dprc_status run_qr(PPBufs& b, const View& v, uint32_t k0, uint32_t k1, bool bf16_out, hipStream_t st) {
-  QrArgs& q = b.qr;
-  q.OS = b.OS; q.os_ld = v.m; q.os_ss = (int64_t)q.s * v.m;
-  q.key0 = k0; q.key1 = k1; q.layer = v.layer_id;
-  q.Q = b.Q; q.q_ld = v.m; q.q_ss = (int64_t)q.s * v.m;
-  q.Qhi = bf16_out ? b.Qhi : nullptr; q.Qlo = bf16_out ? b.Qlo : nullptr;
-  q.qh_ld = bf16_out ? b.ld_q : 0; q.qh_ss = (int64_t)q.s * q.qh_ld;
-  if (q.nlev < 1) return DPRC_ERROR_NOT_SUPPORTED;
-  for (int l = 0; l < q.nlev; ++l)
-    if (traced(l == 0 ? DPRC_KERNEL_QR : DPRC_KERNEL_QR_COMBINE, st,
-               [&] { return launch_qr_factor(q, l, st); }) != hipSuccess)
-      return DPRC_ERROR_HIP;
-  for (int l = q.nlev - 1; l >= 0; --l)
-    if (traced(DPRC_KERNEL_QR_EXPAND, st, [&] { return launch_qr_expand(q, l, st); }) != hipSuccess)
-      return DPRC_ERROR_HIP;
+// The QR job of one layer at one tree level.
+QrJob qr_job(const PPBufs& b, const View& v, int level, uint32_t k0, uint32_t k1, bool bf16_out) {
+  const QrArgs& q = b.qr;
+  QrJob j{};
+  j.level = level; j.nlev = q.nlev;
+  j.B = q.B; j.m = q.m; j.s = q.s; j.r = q.r;
+  j.L = q.lev[level];
+  j.X = level + 1 < q.nlev ? q.lev[level + 1] : QrLevel{};
+  j.OS = b.OS; j.os_ld = v.m; j.os_ss = (int64_t)q.s * v.m;
+  j.Cpart = q.Cpart;
+  j.key0 = k0; j.key1 = k1; j.layer = v.layer_id;
+  j.Q = b.Q; j.q_ld = v.m; j.q_ss = (int64_t)q.s * v.m;
+  j.Qhi = bf16_out ? b.Qhi : nullptr; j.Qlo = bf16_out ? b.Qlo : nullptr;
+  j.qh_ld = bf16_out ? b.ld_q : 0; j.qh_ss = (int64_t)q.s * j.qh_ld;
+  return j;
+}
+
+// Q = orth(O S) of n layers (TSQR trees: factor launches up, expansion launches down),
+// with C = Q^T P formed alongside by each layer's last expansion.  The layers' trees are
+// independent, so one launch takes a level of up to kQrMaxJobs layers: the whole step
+// costs (levels of the tallest tree) x 2 launches instead of that many per layer.
+dprc_status run_qr(PPBufs* const* bs, const View* vs, int n, uint32_t k0, uint32_t k1, bool bf16_out,
+                   hipStream_t st) {
+  int maxlev = 0;
+  for (int l = 0; l < n; ++l) {
+    if (bs[l]->qr.nlev < 1) return DPRC_ERROR_NOT_SUPPORTED;
+    maxlev = std::max(maxlev, (int)bs[l]->qr.nlev);
+  }
+  for (int pass = 0; pass < 2; ++pass) {              // 0: factor levels bottom-up, 1: expansions top-down
+    for (int e = 0; e < maxlev; ++e) {
+      QrBatch bt{};
+      bt.s = bs[0]->qr.s; bt.r = bs[0]->qr.r;
+      auto flush = [&]() -> bool {
+        if (bt.njobs == 0) return true;
+        const int kind = pass == 1 ? DPRC_KERNEL_QR_EXPAND : (e == 0 ? DPRC_KERNEL_QR : DPRC_KERNEL_QR_COMBINE);
+        const hipError_t h = traced(kind, st, [&] {
+          return pass == 0 ? launch_qr_factor(bt, st) : launch_qr_expand(bt, st); });
+        bt.njobs = 0; bt.blocks = 0;
+        return h == hipSuccess;
+      };
+      for (int l = 0; l < n; ++l) {
+        const int nlev = bs[l]->qr.nlev;
+        if (e >= nlev) continue;
+        const int level = pass == 0 ? e : nlev - 1 - e;
+        QrJob j = qr_job(*bs[l], vs[l], level, k0, k1, bf16_out);
+        j.blk0 = bt.blocks;
+        bt.job[bt.njobs++] = j;
+        bt.blocks += j.L.nblk * j.B;
+        if (bt.njobs == kQrMaxJobs && !flush()) return DPRC_ERROR_HIP;
+      }
+      if (!flush()) return DPRC_ERROR_HIP;
+    }
+  }
   return DPRC_SUCCESS;
 }
 
+dprc_status hpp_passes12(const View& v, int32_t s, uint32_t k0, uint32_t k1, const PPBufs& b, hipStream_t st);
+dprc_status hpp_pass3_final(const View& v, int32_t s, int32_t r, uint32_t k0, uint32_t k1, const PPBufs& b,
+                            float* n2, float* n2_layer, int accumulate, hipStream_t st);
+dprc_status hutchpp_f32(const View& v, int32_t s, int32_t r, uint32_t k0, uint32_t k1, PPBufs& b, float* n2,
+                        float* n2_layer, int accumulate, hipStream_t st);
+dprc_status hpp_final(const View& v, int32_t s, int32_t r, const PPBufs& b, float* n2, float* n2_layer,
+                      int accumulate, hipStream_t st);
+
+// One layer on its own: passes 1 and 2, its QR, pass 3 and the estimate.
 dprc_status hutchpp_layer(const View& v, int32_t s, int32_t r, uint32_t k0, uint32_t k1, float* n2,
                           float* n2_layer, int accumulate, void* ws, hipStream_t st) {
   PPBufs b;
   hutchpp_layout(v, s, r, ws, &b);
   const int64_t B = v.B, T = v.T;
-  hipError_t e;
   if (v.dtype == DPRC_BF16) {
     const uint16_t* X = (const uint16_t*)v.X;
     const uint16_t* Xo = (const uint16_t*)v.Xo;
@@ -496,6 +548,22 @@ dprc_status hutchpp_layer(const View& v, int32_t s, int32_t r, uint32_t k0, uint
       ps.mode = 0; ps.scale = 1.0f / (float)r; ps.n2 = n2; ps.n2_layer = n2_layer; ps.accumulate = accumulate;
       return run_pass(ps, B, T, k0, k1, v.layer_id, b.pass_ws, st);
     }
+    dprc_status stt = hpp_passes12(v, s, k0, k1, b, st);
+    if (stt != DPRC_SUCCESS) return stt;
+    PPBufs* bp = &b;
+    if ((stt = run_qr(&bp, &v, 1, k0, k1, true, st)) != DPRC_SUCCESS) return stt;
+    return hpp_pass3_final(v, s, r, k0, k1, b, n2, n2_layer, accumulate, st);
+  } else {
+    return hutchpp_f32(v, s, r, k0, k1, b, n2, n2_layer, accumulate, st);
+  }
+}
+
+// Hutch++ passes 1 and 2 of a bf16 layer: W_S = Xo^T (X S), then O S = X^T (Xo W_S).
+dprc_status hpp_passes12(const View& v, int32_t s, uint32_t k0, uint32_t k1, const PPBufs& b, hipStream_t st) {
+  const int64_t B = v.B, T = v.T;
+  const uint16_t* X = (const uint16_t*)v.X;
+  const uint16_t* Xo = (const uint16_t*)v.Xo;
+  {
     // pass 1: W_S = Xo^T (X S)
     PassSpec p1{};
     p1.X = X; p1.ldx = v.ldx; p1.m = v.m; p1.Xo = Xo; p1.ldo = v.ldo; p1.n = v.n;
@@ -508,9 +576,18 @@ dprc_status hutchpp_layer(const View& v, int32_t s, int32_t r, uint32_t k0, uint
     p2.X = Xo; p2.ldx = v.ldo; p2.m = v.n; p2.Xo = X; p2.ldo = v.ldx; p2.n = v.m;
     p2.nd = s; p2.Rhi = b.WShi; p2.Rlo = b.WSlo; p2.ld_r = b.ld_ws;
     p2.mode = 1; p2.M = b.OS; p2.m_ld = v.m;
-    if ((stt = run_pass(p2, B, T, k0, k1, v.layer_id, b.pass_ws, st)) != DPRC_SUCCESS) return stt;
-    // Q = orth(O S) and C = Q^T P
-    if ((stt = run_qr(b, v, k0, k1, true, st)) != DPRC_SUCCESS) return stt;
+    return run_pass(p2, B, T, k0, k1, v.layer_id, b.pass_ws, st);
+  }
+}
+
+// Hutch++ pass 3 of a bf16 layer, [U | W_P] = Xo^T (X [Q | P]), and the estimate.
+dprc_status hpp_pass3_final(const View& v, int32_t s, int32_t r, uint32_t k0, uint32_t k1, const PPBufs& b,
+                            float* n2, float* n2_layer, int accumulate, hipStream_t st) {
+  const int64_t B = v.B, T = v.T;
+  const uint16_t* X = (const uint16_t*)v.X;
+  const uint16_t* Xo = (const uint16_t*)v.Xo;
+  dprc_status stt;
+  {
     // pass 3: [U | W_P] = Xo^T (X [Q | P])
     PassSpec p3{};
     p3.X = X; p3.ldx = v.ldx; p3.m = v.m; p3.Xo = Xo; p3.ldo = v.ldo; p3.n = v.n;
@@ -518,7 +595,16 @@ dprc_status hutchpp_layer(const View& v, int32_t s, int32_t r, uint32_t k0, uint
     p3.nz = r; p3.stream_id = 0; p3.probe_kind = 0;
     p3.mode = 1; p3.M = b.UW; p3.m_ld = v.n;
     if ((stt = run_pass(p3, B, T, k0, k1, v.layer_id, b.pass_ws, st)) != DPRC_SUCCESS) return stt;
-  } else {
+  }
+  return hpp_final(v, s, r, b, n2, n2_layer, accumulate, st);
+}
+
+// The fp32 Hutch++ path (the tiny workload): SIMT passes, the same QR and finalize.
+dprc_status hutchpp_f32(const View& v, int32_t s, int32_t r, uint32_t k0, uint32_t k1, PPBufs& b, float* n2,
+                        float* n2_layer, int accumulate, hipStream_t st) {
+  const int64_t B = v.B, T = v.T;
+  hipError_t e;
+  {
     const float* X = (const float*)v.X;
     const float* Xo = (const float*)v.Xo;
     if (s > 0) {
@@ -532,7 +618,8 @@ dprc_status hutchpp_layer(const View& v, int32_t s, int32_t r, uint32_t k0, uint
       if ((e = traced(DPRC_KERNEL_PROJECT_F32, st, [&] { return launch_project_f32(a2, st); })) != hipSuccess) return DPRC_ERROR_HIP;
       TokredF32Args t2{X, v.ldx, T * v.ldx, (int32_t)B, (int32_t)T, (int32_t)v.m, b.Y32, s, b.OS, v.m, (int64_t)s * v.m};
       if ((e = traced(DPRC_KERNEL_TOKEN_REDUCE_F32, st, [&] { return launch_tokred_f32(t2, st); })) != hipSuccess) return DPRC_ERROR_HIP;
-      const dprc_status sq = run_qr(b, v, k0, k1, false, st);
+      PPBufs* bp = &b;
+      const dprc_status sq = run_qr(&bp, &v, 1, k0, k1, false, st);
       if (sq != DPRC_SUCCESS) return sq;
     }
     if ((e = traced(DPRC_KERNEL_PROBE_BITS, st, [&] { return launch_probe_bits(0, k0, k1, v.layer_id, 0, v.m, r, b.zb, st); })) != hipSuccess) return DPRC_ERROR_HIP;
@@ -546,6 +633,14 @@ dprc_status hutchpp_layer(const View& v, int32_t s, int32_t r, uint32_t k0, uint
       return hip_status(traced(DPRC_KERNEL_SAMPLE_SQ, st, [&] { return launch_sample_sq(b.UW, v.n, (int64_t)r * v.n, (int32_t)B, r, (int32_t)v.n,
                                          1.0f / (float)r, n2, n2_layer, accumulate, st); }));
   }
+  return hpp_final(v, s, r, b, n2, n2_layer, accumulate, st);
+}
+
+// C = sum of the block partials of Q^T P, the row pass, and the per-sample estimate.
+dprc_status hpp_final(const View& v, int32_t s, int32_t r, const PPBufs& b, float* n2, float* n2_layer,
+                      int accumulate, hipStream_t st) {
+  const int64_t B = v.B;
+  hipError_t e;
   FinalArgs fa = b.fin;
   fa.UW = b.UW; fa.uw_ld = v.n; fa.uw_ss = (int64_t)(s + r) * v.n;
   fa.B = (int32_t)B; fa.n = (int32_t)v.n; fa.s = s; fa.r = r; fa.nblk = b.qr.nlev > 0 ? b.qr.lev[0].nblk : 0;
@@ -673,6 +768,33 @@ dprc_status dprc_norm_hutch_clip(const dprc_layer* layers, int32_t num_layers, i
   return norm_hutch(layers, num_layers, k, probe, seed, side, n2, n2_layers, accumulate, ws, ws_bytes, stream, C, c);
 }
 
+// Calls with several bf16 layers and a sketch run them in groups of up to kQrMaxJobs:
+// passes 1 and 2 of every layer of the group, one batched QR per tree level, then pass 3
+// and the estimate in layer order (so n2 adds the layers' estimates in the same order).
+// Each layer of a group keeps its own buffers; the pass scratch is shared.
+bool hpp_grouped(const dprc_layer* layers, int32_t n, int32_t s) {
+  if (s <= 0 || n < 2) return false;
+  for (int32_t l = 0; l < n; ++l)
+    if (layers[l].dtype != DPRC_BF16) return false;
+  return true;
+}
+
+// Buffers of layers [l0, l1) carved from ws (bufs may be null); returns the bytes used.
+size_t hpp_group_layout(const dprc_layer* layers, int32_t l0, int32_t l1, int32_t s, int32_t r, dprc_side side,
+                        void* ws, PPBufs* bufs) {
+  char* base = static_cast<char*>(ws);
+  size_t off = 0, pass = 0;
+  for (int32_t l = l0; l < l1; ++l) {
+    const View v = view_of(layers[l], side);
+    off += hutchpp_layout(v, s, r, base ? base + off : nullptr, bufs ? &bufs[l - l0] : nullptr, false);
+    off = (off + kAlign - 1) / kAlign * kAlign;
+    pass = std::max(pass, hpp_pass_bytes(v, s, r));
+  }
+  if (bufs)
+    for (int32_t l = l0; l < l1; ++l) bufs[l - l0].pass_ws = base ? base + off : nullptr;
+  return off + pass;
+}
+
 size_t dprc_norm_hutchpp_workspace(const dprc_layer* layers, int32_t num_layers, int32_t s, int32_t r,
                                    dprc_side side) {
   if (check_layers(layers, num_layers, side) != DPRC_SUCCESS) return 0;
@@ -683,6 +805,10 @@ size_t dprc_norm_hutchpp_workspace(const dprc_layer* layers, int32_t num_layers,
     if (s > v.m) return 0;
     need = std::max(need, hutchpp_layout(v, s, r, nullptr, nullptr));
   }
+  if (hpp_grouped(layers, num_layers, s))
+    for (int32_t g0 = 0; g0 < num_layers; g0 += kQrMaxJobs)
+      need = std::max(need, hpp_group_layout(layers, g0, std::min(num_layers, g0 + kQrMaxJobs), s, r, side,
+                                             nullptr, nullptr));
   return need;
 }
 
@@ -704,6 +830,29 @@ dprc_status dprc_norm_hutchpp(const dprc_layer* layers, int32_t num_layers, int3
   uint32_t k0, k1;
   key_of(seed, k0, k1);
   const int64_t B = layers[0].B;
+  if (hpp_grouped(layers, num_layers, s)) {
+    for (int32_t g0 = 0; g0 < num_layers; g0 += kQrMaxJobs) {
+      const int32_t g1 = std::min(num_layers, g0 + kQrMaxJobs), ng = g1 - g0;
+      PPBufs bufs[kQrMaxJobs];
+      View views[kQrMaxJobs];
+      PPBufs* bp[kQrMaxJobs];
+      hpp_group_layout(layers, g0, g1, s, r, side, ws, bufs);
+      for (int32_t q = 0; q < ng; ++q) {
+        views[q] = view_of(layers[g0 + q], side);
+        bp[q] = &bufs[q];
+        if ((st = hpp_passes12(views[q], s, k0, k1, bufs[q], stream)) != DPRC_SUCCESS) return st;
+      }
+      if ((st = run_qr(bp, views, ng, k0, k1, true, stream)) != DPRC_SUCCESS) return st;
+      for (int32_t q = 0; q < ng; ++q) {
+        const int32_t l = g0 + q;
+        if ((st = hpp_pass3_final(views[q], s, r, k0, k1, bufs[q], n2,
+                                  n2_layers ? n2_layers + (int64_t)l * B : nullptr, (accumulate || l > 0) ? 1 : 0,
+                                  stream)) != DPRC_SUCCESS)
+          return st;
+      }
+    }
+    return DPRC_SUCCESS;
+  }
   for (int32_t l = 0; l < num_layers; ++l) {
     st = hutchpp_layer(view_of(layers[l], side), s, r, k0, k1, n2, n2_layers ? n2_layers + (int64_t)l * B : nullptr,
                        (accumulate || l > 0) ? 1 : 0, ws, stream);

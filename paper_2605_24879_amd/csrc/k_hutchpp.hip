@@ -6,7 +6,9 @@
 //    stacked and factored the same way at the next level, until one block is
 //    left.  The expansion runs back down the tree: each block starts from its s
 //    rows of the level above's Q (the identity at the top) and applies its own
-//    reflectors.  Householder keeps Q orthonormal when O S is rank deficient (a
+//    reflectors.  One launch takes the same step of up to eight layers' trees
+//    (each block finds its layer from its block index), so the latency-bound tree
+//    costs a few launches per call rather than a few per layer.  Householder keeps Q orthonormal when O S is rank deficient (a
 //    Gram/Cholesky QR breaks down there).  Dot products over a block's rows are
 //    summed across the wave through LDS in a fixed order, so the result does not
 //    depend on scheduling.
@@ -107,6 +109,14 @@ __device__ __forceinline__ void wave_vec_sum(double (&v)[SP], int c_lo, double* 
   qr_wave_fence();
 }
 
+// The job of this block (jobs start at increasing blk0) and its (block, sample).
+__device__ __forceinline__ int qr_job_index(const QrBatch& bt) {
+  int jb = 0;
+#pragma unroll
+  for (int q = 1; q < kQrMaxJobs; ++q) jb += (q < bt.njobs && (int)blockIdx.x >= bt.job[q].blk0) ? 1 : 0;
+  return jb;
+}
+
 // ---- factor one 128-row block of a level ----------------------------------------------------------
 // Lane l holds rows l and l + 64 of the block.  Step k works on column k, held in
 // register column 0: the columns not yet factored shift down one place after each
@@ -115,12 +125,15 @@ __device__ __forceinline__ void wave_vec_sum(double (&v)[SP], int c_lo, double* 
 // R_kk; the dot products v_k . A_c come from one pass with the norm: x_k . A_c -
 // alpha_k A_kc.  v_k, tau_k and row k of R are written out as each step ends.
 template <int SP>
-__global__ __launch_bounds__(64) void qr_factor_kernel(QrArgs a, int level) {
+__global__ __launch_bounds__(64) void qr_factor_kernel(QrBatch bt) {
   __shared__ double red[SP * kRedLd];
   __shared__ double tot[SP];
-  const int b = blockIdx.x, i = blockIdx.y, lane = threadIdx.x;
+  const QrJob& a = bt.job[qr_job_index(bt)];
+  const int level = a.level;
+  const int rel = (int)blockIdx.x - a.blk0;
+  const int b = rel % a.L.nblk, i = rel / a.L.nblk, lane = threadIdx.x;
   const int s = a.s;
-  const QrLevel L = a.lev[level];
+  const QrLevel L = a.L;
   // all loads are issued before the first use: masked entries read a valid address
   // and are replaced by zero
   double A[2][SP];
@@ -152,7 +165,7 @@ __global__ __launch_bounds__(64) void qr_factor_kernel(QrArgs a, int level) {
   double* V = L.V + ((int64_t)i * L.nblk + b) * s * kQrRows;
   double* tb = L.tau + ((int64_t)i * L.nblk + b) * s;
   const bool has_next = level + 1 < a.nlev;
-  const QrLevel N = a.lev[has_next ? level + 1 : level];
+  const QrLevel N = has_next ? a.X : a.L;
   // outputs stay in registers until the loop ends (a store costs the wave tens of
   // cycles even with one lane active): v_k and tau_k enter register column SP - 1
   // and move down one place per step, so after s steps column k sits at SP - s + k;
@@ -245,16 +258,19 @@ __global__ __launch_bounds__(64) void qr_factor_kernel(QrArgs a, int level) {
 
 // ---- expand one block: W = H_0 ... H_{s-1} [Q_up rows; 0]; level 0 writes Q and C_b = Q_b^T P_b ----
 template <int SP>
-__global__ __launch_bounds__(64) void qr_expand_kernel(QrArgs a, int level) {
+__global__ __launch_bounds__(64) void qr_expand_kernel(QrBatch bt) {
   __shared__ double red[SP * kRedLd];
   __shared__ double tot[SP];
   __shared__ double qs[SP * (kQrRows + 1)];
   __shared__ uint32_t zw[256 * 4];
-  const int b = blockIdx.x, i = blockIdx.y, lane = threadIdx.x;
+  const QrJob& a = bt.job[qr_job_index(bt)];
+  const int level = a.level;
+  const int rel = (int)blockIdx.x - a.blk0;
+  const int b = rel % a.L.nblk, i = rel / a.L.nblk, lane = threadIdx.x;
   const int s = a.s;
-  const QrLevel L = a.lev[level];
+  const QrLevel L = a.L;
   const bool top = level + 1 == a.nlev;
-  const QrLevel U = a.lev[top ? level : level + 1];
+  const QrLevel U = top ? a.L : a.X;
   // all loads are issued before the first use (masked entries read a valid address)
   double W[2][SP];
   const double* uq = U.Q + (int64_t)i * s * U.rows + (int64_t)b * s;
@@ -396,11 +412,13 @@ int32_t qr_levels(int64_t m, int s, int32_t rows[kQrMaxLevels], int32_t nblk[kQr
 }
 
 template <template <int> class K>
-static hipError_t launch_qr_sp(const QrArgs& a, int level, hipStream_t st) {
-  const dim3 grid((unsigned)a.lev[level].nblk, (unsigned)a.B);
-  if (a.s <= 8) DPRC_LAUNCH(K<8>::fn, grid, dim3(64), 0, st, a, level);
-  else if (a.s <= 16) DPRC_LAUNCH(K<16>::fn, grid, dim3(64), 0, st, a, level);
-  else DPRC_LAUNCH(K<32>::fn, grid, dim3(64), 0, st, a, level);
+static hipError_t launch_qr_sp(const QrBatch& bt, hipStream_t st) {
+  if (bt.s < 1 || bt.s > 32 || bt.r > 256 || bt.njobs < 1 || bt.njobs > kQrMaxJobs || bt.blocks < 1)
+    return hipErrorInvalidValue;
+  const dim3 grid((unsigned)bt.blocks);
+  if (bt.s <= 8) DPRC_LAUNCH(K<8>::fn, grid, dim3(64), 0, st, bt);
+  else if (bt.s <= 16) DPRC_LAUNCH(K<16>::fn, grid, dim3(64), 0, st, bt);
+  else DPRC_LAUNCH(K<32>::fn, grid, dim3(64), 0, st, bt);
   return hipGetLastError();
 }
 template <int SP>
@@ -412,15 +430,8 @@ struct QrExpandK {
   static constexpr auto fn = qr_expand_kernel<SP>;
 };
 
-hipError_t launch_qr_factor(const QrArgs& a, int level, hipStream_t st) {
-  if (a.s < 1 || a.s > 32 || a.r > 256 || level < 0 || level >= a.nlev) return hipErrorInvalidValue;
-  return launch_qr_sp<QrFactorK>(a, level, st);
-}
-
-hipError_t launch_qr_expand(const QrArgs& a, int level, hipStream_t st) {
-  if (a.s < 1 || a.s > 32 || a.r > 256 || level < 0 || level >= a.nlev) return hipErrorInvalidValue;
-  return launch_qr_sp<QrExpandK>(a, level, st);
-}
+hipError_t launch_qr_factor(const QrBatch& bt, hipStream_t st) { return launch_qr_sp<QrFactorK>(bt, st); }
+hipError_t launch_qr_expand(const QrBatch& bt, hipStream_t st) { return launch_qr_sp<QrExpandK>(bt, st); }
 
 // ---- finalize -----------------------------------------------------------------------------------------
 // A workgroup takes 32 rows j of U | W_P; its threads are (row, column group): group

@@ -151,11 +151,26 @@ struct QrLevel {
   double* M;                     // [B][s][rows] fp64 input (levels >= 2); level 1 reads O S
   double* Q;                     // [B][s][rows] explicit Q of this level (levels >= 2)
 };
-struct QrArgs {
+struct QrArgs {                  // one layer's tree (host side): level geometry and scratch
   int32_t B, m, s, r;
   int32_t nlev;
   QrLevel lev[kQrMaxLevels];
-  const float* OS;               // OS[i*os_ss + c*os_ld + j]
+  double* Cpart;                 // [B][nblk1][s][r]
+};
+// Level geometry for m rows and s columns; doubles of workspace per sample in *dbl.
+int32_t qr_levels(int64_t m, int s, int32_t rows[kQrMaxLevels], int32_t nblk[kQrMaxLevels], int64_t* dbl);
+
+// One layer's share of a QR launch: one tree level of that layer.  Launches take up
+// to kQrMaxJobs layers at once (their trees are independent), so a whole level of
+// every layer's tree costs one launch.  Blocks blk0 .. blk0 + L.nblk * B - 1 of the
+// launch belong to the job (block b of sample i at blk0 + i * L.nblk + b).
+struct QrJob {
+  int32_t blk0;
+  int32_t level, nlev;           // tree level worked on; levels of the layer's tree
+  int32_t B, m, s, r;
+  QrLevel L;                     // level `level`
+  QrLevel X;                     // level `level` + 1 when it exists (factor: its input M; expand: its Q)
+  const float* OS;               // level 0 input: OS[i*os_ss + c*os_ld + j]
   int64_t os_ld, os_ss;
   double* Cpart;                 // [B][nblk1][s][r]
   uint32_t key0, key1, layer;
@@ -165,8 +180,12 @@ struct QrArgs {
   uint16_t* Qlo;
   int64_t qh_ld, qh_ss;
 };
-// Level geometry for m rows and s columns; doubles of workspace per sample in *dbl.
-int32_t qr_levels(int64_t m, int s, int32_t rows[kQrMaxLevels], int32_t nblk[kQrMaxLevels], int64_t* dbl);
+constexpr int kQrMaxJobs = 8;
+struct QrBatch {
+  int32_t njobs, blocks;         // jobs, total blocks of the launch
+  int32_t s, r;                  // shared by every job
+  QrJob job[kQrMaxJobs];
+};
 
 // Hutch++ estimate from U | W_P (UW[i*uw_ss + c*uw_ld + j], c < s + r) and C.
 struct FinalArgs {
@@ -240,8 +259,8 @@ hipError_t launch_tokred_f32(const TokredF32Args& a, hipStream_t st);
 hipError_t launch_sample_sq(const float* M, int64_t m_ld, int64_t m_ss, int32_t B, int32_t ncols,
                             int32_t n, float scale, float* n2, float* n2_layer, int accumulate,
                             hipStream_t st);
-hipError_t launch_qr_factor(const QrArgs& a, int level, hipStream_t st);   // level 0 reads O S
-hipError_t launch_qr_expand(const QrArgs& a, int level, hipStream_t st);   // level 0 writes Q and C
+hipError_t launch_qr_factor(const QrBatch& bt, hipStream_t st);   // a level-0 job reads O S
+hipError_t launch_qr_expand(const QrBatch& bt, hipStream_t st);   // a level-0 job writes Q and C
 hipError_t launch_hpp_csum(const FinalArgs& a, hipStream_t st);
 hipError_t launch_hpp_rows(const FinalArgs& a, hipStream_t st);
 hipError_t launch_hpp_sum(const FinalArgs& a, hipStream_t st);

@@ -294,6 +294,24 @@ def test_hutchpp_low_rank_is_exact_deep_tree(D, side):
     assert np.all(_rel(n2.cpu().numpy(), exact) < NORM_RTOL)
 
 
+def test_hutchpp_many_layers_grouped(D):
+    # 10 layers: two groups of the batched QR, sketched widths that take 1, 2 and 3 tree levels
+    B, T = 2, 160
+    shapes = [(64, 100), (96, 300), (48, 1500), (80, 130), (72, 640), (64, 90), (56, 2100), (40, 200),
+              (88, 120), (64, 700)]
+    pairs = []
+    for li, (d, p) in enumerate(shapes):
+        A, E = _draw(B, T, d, p, law="student_t", layer=20 + li)
+        pairs.append((A, E, li))
+    n2l = torch.zeros(len(pairs), B, device="cuda")
+    n2 = D.dprc_norm_hutchpp(pairs, 8, 12, 4, n2_layers=n2l)
+    ref_l = [est.hutchpp_layer(_np(A), _np(E), 8, 12, 4, li) for (A, E, li) in pairs]
+    got_l = n2l.cpu().numpy()
+    for li in range(len(pairs)):
+        assert np.all(_rel(got_l[li], ref_l[li]) < NORM_RTOL), li
+    assert np.all(_rel(n2.cpu().numpy(), sum(ref_l)) < NORM_RTOL)
+
+
 def test_hutchpp_without_sketch_equals_hutch(D):
     A, E = _draw(2, 300, 100, 180, layer=8)
     a = D.dprc_norm_hutchpp([(A, E, 4)], 0, 16, 5)
