@@ -1,6 +1,7 @@
 // C-ABI entry points of libdprc (declared in include/dprc.h): argument
 // validation, side resolution, workspace planning and the launch sequence of
 // each call.  Nothing here allocates device memory or synchronises the stream.
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 #include <vector>
@@ -194,8 +195,12 @@ size_t pass_ws(Arena& ar, int64_t B, int64_t T, int64_t n, int ncols_pad, uint16
   return ar.off;
 }
 
+// One projection + token-reduction pass.  With `part`, the token-split partials go there
+// instead of the pass scratch; with `defer` (store mode), the split sums are not launched
+// and the token-reduction arguments are returned for a batched launch (defer->S tells
+// whether one is needed).
 dprc_status run_pass(const PassSpec& ps, int64_t B, int64_t T, uint32_t k0, uint32_t k1, uint32_t layer,
-                     void* ws, hipStream_t st) {
+                     void* ws, hipStream_t st, float* part = nullptr, TokredArgs* defer = nullptr) {
   const int ncols = ps.nd + ps.nz;
   const int ncols_pad = pad_cols(ncols);
   Arena ar(ws);
@@ -203,6 +208,7 @@ dprc_status run_pass(const PassSpec& ps, int64_t B, int64_t T, uint32_t k0, uint
   TokBufs tb;
   TokPlan tp;
   pass_ws(ar, B, T, ps.n, ncols_pad, &Yt, &tb, &tp);
+  if (part && tp.S > 1) tb.part = part;
 
   ProjectArgs pa;
   pa.X = ps.X; pa.ldx = ps.ldx; pa.x_ss = T * ps.ldx;
@@ -232,12 +238,41 @@ dprc_status run_pass(const PassSpec& ps, int64_t B, int64_t T, uint32_t k0, uint
   ta.vec = rows16(ps.Xo, ps.ldo);
   e = traced(DPRC_KERNEL_TOKEN_REDUCE, st, [&] { return launch_tokred(ta, st); });
   if (e != hipSuccess) return DPRC_ERROR_HIP;
+  if (defer && ps.mode == 1) {
+    *defer = ta;
+    return DPRC_SUCCESS;
+  }
   if (tp.S > 1) {
     e = traced(DPRC_KERNEL_TOKEN_SPLITS, st, [&] { return launch_tokred_splits(ta, st); });
     if (e != hipSuccess) return DPRC_ERROR_HIP;
   }
   if (ps.mode == 0) return hip_status(traced(DPRC_KERNEL_SAMPLE_SUM, st, [&] { return launch_tokred_sample(ta, st); }));
   return DPRC_SUCCESS;
+}
+
+// Token-split partial floats of a pass (0 without splits).
+int64_t part_floats(int64_t B, int64_t T, int64_t n, int ncols) {
+  const TokPlan tp = tok_plan(B, T, n);
+  return tp.S > 1 ? B * tp.ntiles * tp.S * pad_cols(ncols) * kTile : 0;
+}
+
+// Split sums of deferred passes (those with token splits), up to kTokMaxJobs per launch.
+dprc_status run_splits_batch(const TokredArgs* ta, int n, hipStream_t st) {
+  TokredBatch bt{};
+  auto flush = [&]() -> bool {
+    if (bt.njobs == 0) return true;
+    const hipError_t e = traced(DPRC_KERNEL_TOKEN_SPLITS, st, [&] { return launch_tokred_splits_batch(bt, st); });
+    bt.njobs = 0; bt.blocks = 0;
+    return e == hipSuccess;
+  };
+  for (int j = 0; j < n; ++j) {
+    if (ta[j].S <= 1) continue;
+    bt.blk0[bt.njobs] = bt.blocks;
+    bt.job[bt.njobs++] = ta[j];
+    bt.blocks += ta[j].ntiles * ta[j].B;
+    if (bt.njobs == kTokMaxJobs && !flush()) return DPRC_ERROR_HIP;
+  }
+  return flush() ? DPRC_SUCCESS : DPRC_ERROR_HIP;
 }
 
 size_t pass_ws_bytes(int64_t B, int64_t T, int64_t n, int ncols) {
@@ -408,6 +443,7 @@ struct PPBufs {
   uint32_t* zb;                            // fp32 path: probe bits (s or r columns)
   float* Y32;                              // fp32 path
   void* pass_ws;                           // bf16 path: scratch of one pass
+  float* part;                             // grouped layers: the layer's own token-split partials
 };
 
 // Bytes of the bf16 pass scratch of one layer (the Y buffer and token-split partials).
@@ -524,9 +560,8 @@ dprc_status run_qr(PPBufs* const* bs, const View* vs, int n, uint32_t k0, uint32
   return DPRC_SUCCESS;
 }
 
-dprc_status hpp_passes12(const View& v, int32_t s, uint32_t k0, uint32_t k1, const PPBufs& b, hipStream_t st);
-dprc_status hpp_pass3_final(const View& v, int32_t s, int32_t r, uint32_t k0, uint32_t k1, const PPBufs& b,
-                            float* n2, float* n2_layer, int accumulate, hipStream_t st);
+dprc_status hpp_pass(int which, const View& v, int32_t s, int32_t r, uint32_t k0, uint32_t k1, const PPBufs& b,
+                     hipStream_t st, TokredArgs* defer);
 dprc_status hutchpp_f32(const View& v, int32_t s, int32_t r, uint32_t k0, uint32_t k1, PPBufs& b, float* n2,
                         float* n2_layer, int accumulate, hipStream_t st);
 dprc_status hpp_final(const View& v, int32_t s, int32_t r, const PPBufs& b, float* n2, float* n2_layer,
@@ -548,55 +583,42 @@ dprc_status hutchpp_layer(const View& v, int32_t s, int32_t r, uint32_t k0, uint
       ps.mode = 0; ps.scale = 1.0f / (float)r; ps.n2 = n2; ps.n2_layer = n2_layer; ps.accumulate = accumulate;
       return run_pass(ps, B, T, k0, k1, v.layer_id, b.pass_ws, st);
     }
-    dprc_status stt = hpp_passes12(v, s, k0, k1, b, st);
-    if (stt != DPRC_SUCCESS) return stt;
+    dprc_status stt;
+    if ((stt = hpp_pass(1, v, s, r, k0, k1, b, st, nullptr)) != DPRC_SUCCESS) return stt;
+    if ((stt = hpp_pass(2, v, s, r, k0, k1, b, st, nullptr)) != DPRC_SUCCESS) return stt;
     PPBufs* bp = &b;
     if ((stt = run_qr(&bp, &v, 1, k0, k1, true, st)) != DPRC_SUCCESS) return stt;
-    return hpp_pass3_final(v, s, r, k0, k1, b, n2, n2_layer, accumulate, st);
+    if ((stt = hpp_pass(3, v, s, r, k0, k1, b, st, nullptr)) != DPRC_SUCCESS) return stt;
+    return hpp_final(v, s, r, b, n2, n2_layer, accumulate, st);
   } else {
     return hutchpp_f32(v, s, r, k0, k1, b, n2, n2_layer, accumulate, st);
   }
 }
 
-// Hutch++ passes 1 and 2 of a bf16 layer: W_S = Xo^T (X S), then O S = X^T (Xo W_S).
-dprc_status hpp_passes12(const View& v, int32_t s, uint32_t k0, uint32_t k1, const PPBufs& b, hipStream_t st) {
-  const int64_t B = v.B, T = v.T;
+// Hutch++ pass `which` of a bf16 layer:
+//   1: W_S = Xo^T (X S);  2: O S = X^T (Xo W_S);  3: [U | W_P] = Xo^T (X [Q | P]).
+dprc_status hpp_pass(int which, const View& v, int32_t s, int32_t r, uint32_t k0, uint32_t k1, const PPBufs& b,
+                     hipStream_t st, TokredArgs* defer = nullptr) {
   const uint16_t* X = (const uint16_t*)v.X;
   const uint16_t* Xo = (const uint16_t*)v.Xo;
-  {
-    // pass 1: W_S = Xo^T (X S)
-    PassSpec p1{};
-    p1.X = X; p1.ldx = v.ldx; p1.m = v.m; p1.Xo = Xo; p1.ldo = v.ldo; p1.n = v.n;
-    p1.nz = s; p1.stream_id = 1; p1.probe_kind = 0;
-    p1.mode = 1; p1.Mhi = b.WShi; p1.Mlo = b.WSlo; p1.mh_ld = b.ld_ws;
-    dprc_status stt = run_pass(p1, B, T, k0, k1, v.layer_id, b.pass_ws, st);
-    if (stt != DPRC_SUCCESS) return stt;
-    // pass 2: O S = X^T (Xo W_S)
-    PassSpec p2{};
-    p2.X = Xo; p2.ldx = v.ldo; p2.m = v.n; p2.Xo = X; p2.ldo = v.ldx; p2.n = v.m;
-    p2.nd = s; p2.Rhi = b.WShi; p2.Rlo = b.WSlo; p2.ld_r = b.ld_ws;
-    p2.mode = 1; p2.M = b.OS; p2.m_ld = v.m;
-    return run_pass(p2, B, T, k0, k1, v.layer_id, b.pass_ws, st);
+  PassSpec p{};
+  if (which == 2) {
+    p.X = Xo; p.ldx = v.ldo; p.m = v.n; p.Xo = X; p.ldo = v.ldx; p.n = v.m;
+    p.nd = s; p.Rhi = b.WShi; p.Rlo = b.WSlo; p.ld_r = b.ld_ws;
+    p.mode = 1; p.M = b.OS; p.m_ld = v.m;
+  } else {
+    p.X = X; p.ldx = v.ldx; p.m = v.m; p.Xo = Xo; p.ldo = v.ldo; p.n = v.n;
+    p.mode = 1; p.probe_kind = 0;
+    if (which == 1) {
+      p.nz = s; p.stream_id = 1;
+      p.Mhi = b.WShi; p.Mlo = b.WSlo; p.mh_ld = b.ld_ws;
+    } else {
+      p.nd = s; p.Rhi = b.Qhi; p.Rlo = b.Qlo; p.ld_r = b.ld_q;
+      p.nz = r; p.stream_id = 0;
+      p.M = b.UW; p.m_ld = v.n;
+    }
   }
-}
-
-// Hutch++ pass 3 of a bf16 layer, [U | W_P] = Xo^T (X [Q | P]), and the estimate.
-dprc_status hpp_pass3_final(const View& v, int32_t s, int32_t r, uint32_t k0, uint32_t k1, const PPBufs& b,
-                            float* n2, float* n2_layer, int accumulate, hipStream_t st) {
-  const int64_t B = v.B, T = v.T;
-  const uint16_t* X = (const uint16_t*)v.X;
-  const uint16_t* Xo = (const uint16_t*)v.Xo;
-  dprc_status stt;
-  {
-    // pass 3: [U | W_P] = Xo^T (X [Q | P])
-    PassSpec p3{};
-    p3.X = X; p3.ldx = v.ldx; p3.m = v.m; p3.Xo = Xo; p3.ldo = v.ldo; p3.n = v.n;
-    p3.nd = s; p3.Rhi = b.Qhi; p3.Rlo = b.Qlo; p3.ld_r = b.ld_q;
-    p3.nz = r; p3.stream_id = 0; p3.probe_kind = 0;
-    p3.mode = 1; p3.M = b.UW; p3.m_ld = v.n;
-    if ((stt = run_pass(p3, B, T, k0, k1, v.layer_id, b.pass_ws, st)) != DPRC_SUCCESS) return stt;
-  }
-  return hpp_final(v, s, r, b, n2, n2_layer, accumulate, st);
+  return run_pass(p, v.B, v.T, k0, k1, v.layer_id, b.pass_ws, st, b.part, defer);
 }
 
 // The fp32 Hutch++ path (the tiny workload): SIMT passes, the same QR and finalize.
@@ -637,14 +659,19 @@ dprc_status hutchpp_f32(const View& v, int32_t s, int32_t r, uint32_t k0, uint32
 }
 
 // C = sum of the block partials of Q^T P, the row pass, and the per-sample estimate.
-dprc_status hpp_final(const View& v, int32_t s, int32_t r, const PPBufs& b, float* n2, float* n2_layer,
-                      int accumulate, hipStream_t st) {
-  const int64_t B = v.B;
-  hipError_t e;
+FinalArgs final_args(const View& v, int32_t s, int32_t r, const PPBufs& b, float* n2, float* n2_layer,
+                     int accumulate) {
   FinalArgs fa = b.fin;
   fa.UW = b.UW; fa.uw_ld = v.n; fa.uw_ss = (int64_t)(s + r) * v.n;
-  fa.B = (int32_t)B; fa.n = (int32_t)v.n; fa.s = s; fa.r = r; fa.nblk = b.qr.nlev > 0 ? b.qr.lev[0].nblk : 0;
+  fa.B = (int32_t)v.B; fa.n = (int32_t)v.n; fa.s = s; fa.r = r; fa.nblk = b.qr.nlev > 0 ? b.qr.lev[0].nblk : 0;
   fa.Cpart = b.qr.Cpart; fa.n2 = n2; fa.n2_layer = n2_layer; fa.accumulate = accumulate;
+  return fa;
+}
+
+dprc_status hpp_final(const View& v, int32_t s, int32_t r, const PPBufs& b, float* n2, float* n2_layer,
+                      int accumulate, hipStream_t st) {
+  hipError_t e;
+  const FinalArgs fa = final_args(v, s, r, b, n2, n2_layer, accumulate);
   if ((e = traced(DPRC_KERNEL_QR_EXPAND, st, [&] { return launch_hpp_csum(fa, st); })) != hipSuccess)
     return DPRC_ERROR_HIP;
   if ((e = traced(DPRC_KERNEL_HUTCHPP_FINAL, st, [&] { return launch_hpp_rows(fa, st); })) != hipSuccess)
@@ -788,6 +815,12 @@ size_t hpp_group_layout(const dprc_layer* layers, int32_t l0, int32_t l1, int32_
     const View v = view_of(layers[l], side);
     off += hutchpp_layout(v, s, r, base ? base + off : nullptr, bufs ? &bufs[l - l0] : nullptr, false);
     off = (off + kAlign - 1) / kAlign * kAlign;
+    // the layer's own token-split partials (its passes' split sums are launched for the group)
+    const int64_t pf = std::max({part_floats(v.B, v.T, v.n, s), part_floats(v.B, v.T, v.m, s),
+                                 part_floats(v.B, v.T, v.n, s + r)});
+    if (bufs) bufs[l - l0].part = base && pf > 0 ? reinterpret_cast<float*>(base + off) : nullptr;
+    off += (size_t)pf * sizeof(float);
+    off = (off + kAlign - 1) / kAlign * kAlign;
     pass = std::max(pass, hpp_pass_bytes(v, s, r));
   }
   if (bufs)
@@ -840,16 +873,29 @@ dprc_status dprc_norm_hutchpp(const dprc_layer* layers, int32_t num_layers, int3
       for (int32_t q = 0; q < ng; ++q) {
         views[q] = view_of(layers[g0 + q], side);
         bp[q] = &bufs[q];
-        if ((st = hpp_passes12(views[q], s, k0, k1, bufs[q], stream)) != DPRC_SUCCESS) return st;
+      }
+      TokredArgs def[kQrMaxJobs];
+      // passes 1 and 2 of every layer, each followed by one split-sum launch for the group
+      for (int which = 1; which <= 2; ++which) {
+        for (int32_t q = 0; q < ng; ++q)
+          if ((st = hpp_pass(which, views[q], s, r, k0, k1, bufs[q], stream, &def[q])) != DPRC_SUCCESS) return st;
+        if ((st = run_splits_batch(def, ng, stream)) != DPRC_SUCCESS) return st;
       }
       if ((st = run_qr(bp, views, ng, k0, k1, true, stream)) != DPRC_SUCCESS) return st;
+      for (int32_t q = 0; q < ng; ++q)
+        if ((st = hpp_pass(3, views[q], s, r, k0, k1, bufs[q], stream, &def[q])) != DPRC_SUCCESS) return st;
+      if ((st = run_splits_batch(def, ng, stream)) != DPRC_SUCCESS) return st;
+      // the estimates, added to n2 in layer order
+      FinalBatch fb{};
       for (int32_t q = 0; q < ng; ++q) {
         const int32_t l = g0 + q;
-        if ((st = hpp_pass3_final(views[q], s, r, k0, k1, bufs[q], n2,
-                                  n2_layers ? n2_layers + (int64_t)l * B : nullptr, (accumulate || l > 0) ? 1 : 0,
-                                  stream)) != DPRC_SUCCESS)
-          return st;
+        fb.job[fb.njobs++] = final_args(views[q], s, r, bufs[q], n2, n2_layers ? n2_layers + (int64_t)l * B : nullptr,
+                                        (accumulate || l > 0) ? 1 : 0);
       }
+      if (traced(DPRC_KERNEL_QR_EXPAND, stream, [&] { return launch_hpp_csum_batch(fb, stream); }) != hipSuccess ||
+          traced(DPRC_KERNEL_HUTCHPP_FINAL, stream, [&] { return launch_hpp_rows_batch(fb, stream); }) != hipSuccess ||
+          traced(DPRC_KERNEL_HUTCHPP_SUM, stream, [&] { return launch_hpp_sum_batch(fb, stream); }) != hipSuccess)
+        return DPRC_ERROR_HIP;
     }
     return DPRC_SUCCESS;
   }

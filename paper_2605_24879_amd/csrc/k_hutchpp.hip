@@ -441,10 +441,9 @@ constexpr int kFinRows = 32;                 // rows per workgroup
 constexpr int kFinGroups = kQrThreads / kFinRows;
 
 // C = sum of the block partials C_b, in block order (one thread per entry).
-__global__ __launch_bounds__(kQrThreads) void hpp_csum_kernel(FinalArgs a) {
-  const int i = blockIdx.y;
+__device__ __forceinline__ void hpp_csum_block(const FinalArgs& a, int bx, int i) {
   const int sr = a.s * a.r;
-  const int e = blockIdx.x * kQrThreads + threadIdx.x;
+  const int e = bx * kQrThreads + threadIdx.x;
   if (e >= sr) return;
   const double* cp = a.Cpart + (int64_t)i * a.nblk * sr + e;
   double v = 0.0;
@@ -459,13 +458,14 @@ __global__ __launch_bounds__(kQrThreads) void hpp_csum_kernel(FinalArgs a) {
   for (; b < a.nblk; ++b) v += cp[(int64_t)b * sr];
   a.C[(int64_t)i * sr + e] = v;
 }
+__global__ __launch_bounds__(kQrThreads) void hpp_csum_kernel(FinalArgs a) { hpp_csum_block(a, blockIdx.x, blockIdx.y); }
 
 // Rows of one chunk: ||U_j||^2 and ||W_P,j - U_j C||^2 summed over the chunk.
 template <int SP>
-__global__ __launch_bounds__(kQrThreads) void hpp_rows_kernel(FinalArgs a) {
+__device__ __forceinline__ void hpp_rows_block(const FinalArgs& a, int ch, int i) {
   extern __shared__ __attribute__((aligned(16))) float fs[];
   __shared__ double sh[4];
-  const int ch = blockIdx.x, i = blockIdx.y, tid = threadIdx.x;
+  const int tid = threadIdx.x;
   const int s = a.s, r = a.r;
   float* C = fs;                           // [s][r]
   for (int e = tid; e < s * r; e += kQrThreads) C[e] = (float)a.C[(int64_t)i * s * r + e];
@@ -510,10 +510,35 @@ __global__ __launch_bounds__(kQrThreads) void hpp_rows_kernel(FinalArgs a) {
     a.Fpart[((int64_t)i * a.nchunk + ch) * 2 + 1] = sv;
   }
 }
+template <int SP>
+__global__ __launch_bounds__(kQrThreads) void hpp_rows_kernel(FinalArgs a) { hpp_rows_block<SP>(a, blockIdx.x, blockIdx.y); }
 
-__global__ __launch_bounds__(kQrThreads) void hpp_sum_kernel(FinalArgs a) {
+// The finalize of several layers in one launch per step: block (x, sample) of job j at
+// blk0[j] + sample * (x blocks of the job) + x.  The per-sample sum walks the jobs in
+// order, so n2 adds the layers' estimates in layer order.
+__device__ __forceinline__ int fin_job_index(const FinalBatch& bt) {
+  int jb = 0;
+#pragma unroll
+  for (int q = 1; q < kFinMaxJobs; ++q) jb += (q < bt.njobs && (int)blockIdx.x >= bt.blk0[q]) ? 1 : 0;
+  return jb;
+}
+__global__ __launch_bounds__(kQrThreads) void hpp_csum_batch_kernel(FinalBatch bt) {
+  const int jb = fin_job_index(bt);
+  const FinalArgs& a = bt.job[jb];
+  const int nx = (a.s * a.r + kQrThreads - 1) / kQrThreads;
+  const int rel = (int)blockIdx.x - bt.blk0[jb];
+  hpp_csum_block(a, rel % nx, rel / nx);
+}
+template <int SP>
+__global__ __launch_bounds__(kQrThreads) void hpp_rows_batch_kernel(FinalBatch bt) {
+  const int jb = fin_job_index(bt);
+  const FinalArgs& a = bt.job[jb];
+  const int rel = (int)blockIdx.x - bt.blk0[jb];
+  hpp_rows_block<SP>(a, rel % a.nchunk, rel / a.nchunk);
+}
+
+__device__ __forceinline__ void hpp_sum_block(const FinalArgs& a, int i) {
   __shared__ double sh[4];
-  const int i = blockIdx.x;
   double su = 0.0, sv = 0.0;
   for (int c = threadIdx.x; c < a.nchunk; c += kQrThreads) {
     su += a.Fpart[((int64_t)i * a.nchunk + c) * 2];
@@ -525,6 +550,13 @@ __global__ __launch_bounds__(kQrThreads) void hpp_sum_kernel(FinalArgs a) {
     const float est = (float)(su + sv / (double)a.r);
     a.n2[i] = (a.accumulate ? a.n2[i] : 0.f) + est;
     if (a.n2_layer) a.n2_layer[i] = est;
+  }
+}
+__global__ __launch_bounds__(kQrThreads) void hpp_sum_kernel(FinalArgs a) { hpp_sum_block(a, blockIdx.x); }
+__global__ __launch_bounds__(kQrThreads) void hpp_sum_batch_kernel(FinalBatch bt) {
+  for (int j = 0; j < bt.njobs; ++j) {               // layer order; each job adds to n2 after the last
+    hpp_sum_block(bt.job[j], blockIdx.x);
+    __syncthreads();
   }
 }
 
@@ -545,6 +577,40 @@ hipError_t launch_hpp_csum(const FinalArgs& a, hipStream_t st) {
 
 hipError_t launch_hpp_sum(const FinalArgs& a, hipStream_t st) {
   DPRC_LAUNCH(hpp_sum_kernel, dim3((unsigned)a.B), dim3(kQrThreads), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_hpp_csum_batch(const FinalBatch& bt, hipStream_t st) {
+  if (bt.njobs < 1 || bt.njobs > kFinMaxJobs) return hipErrorInvalidValue;
+  FinalBatch b = bt;
+  int blocks = 0;
+  for (int j = 0; j < b.njobs; ++j) {
+    b.blk0[j] = blocks;
+    blocks += (int)ceil_div((int64_t)b.job[j].s * b.job[j].r, kQrThreads) * b.job[j].B;
+  }
+  DPRC_LAUNCH(hpp_csum_batch_kernel, dim3((unsigned)blocks), dim3(kQrThreads), 0, st, b);
+  return hipGetLastError();
+}
+
+hipError_t launch_hpp_rows_batch(const FinalBatch& bt, hipStream_t st) {
+  if (bt.njobs < 1 || bt.njobs > kFinMaxJobs) return hipErrorInvalidValue;
+  FinalBatch b = bt;
+  int blocks = 0;
+  for (int j = 0; j < b.njobs; ++j) {
+    b.blk0[j] = blocks;
+    blocks += b.job[j].nchunk * b.job[j].B;
+  }
+  const int s = b.job[0].s;
+  const size_t lds = (size_t)s * b.job[0].r * 4;
+  if (s <= 8) DPRC_LAUNCH(hpp_rows_batch_kernel<8>, dim3((unsigned)blocks), dim3(kQrThreads), lds, st, b);
+  else if (s <= 16) DPRC_LAUNCH(hpp_rows_batch_kernel<16>, dim3((unsigned)blocks), dim3(kQrThreads), lds, st, b);
+  else DPRC_LAUNCH(hpp_rows_batch_kernel<32>, dim3((unsigned)blocks), dim3(kQrThreads), lds, st, b);
+  return hipGetLastError();
+}
+
+hipError_t launch_hpp_sum_batch(const FinalBatch& bt, hipStream_t st) {
+  if (bt.njobs < 1 || bt.njobs > kFinMaxJobs) return hipErrorInvalidValue;
+  DPRC_LAUNCH(hpp_sum_batch_kernel, dim3((unsigned)bt.job[0].B), dim3(kQrThreads), 0, st, bt);
   return hipGetLastError();
 }
 

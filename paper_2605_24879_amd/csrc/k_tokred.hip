@@ -265,10 +265,10 @@ __global__ __launch_bounds__(kBlock) void tokred_kernel(TokredArgs a) {
 // takes G = 16 / U float4 groups at a time and U splits of each, so 16 loads are
 // in flight whatever S is (split indices past S are clamped to S-1 and not added).
 template <int U>
-__global__ __launch_bounds__(kBlock) void tokred_splits_kernel(TokredArgs a) {
+__device__ __forceinline__ void tokred_splits_block(const TokredArgs& a, int tile, int i) {
   constexpr int G = 16 / U;
   __shared__ double dred[4];
-  const int tid = threadIdx.x, tile = blockIdx.x, i = blockIdx.y;
+  const int tid = threadIdx.x;
   const int64_t tslot = (int64_t)i * a.ntiles + tile;
   const float* tp = a.part + tslot * a.S * (int64_t)a.ncols_pad * kTile;
   const int64_t sstride = (int64_t)a.ncols_pad * kTile;
@@ -316,6 +316,34 @@ __global__ __launch_bounds__(kBlock) void tokred_splits_kernel(TokredArgs a) {
     }
   }
   if (a.mode == 0) seg_publish(a, tslot, sq, dred);
+}
+
+template <int U>
+__global__ __launch_bounds__(kBlock) void tokred_splits_kernel(TokredArgs a) {
+  tokred_splits_block<U>(a, blockIdx.x, blockIdx.y);
+}
+
+// Split sums of several layers' passes in one launch (block (tile, sample) of job j at
+// blk0[j] + sample * ntiles + tile).
+template <int U>
+__global__ __launch_bounds__(kBlock) void tokred_splits_batch_kernel(TokredBatch bt) {
+  int jb = 0;
+#pragma unroll
+  for (int q = 1; q < kTokMaxJobs; ++q) jb += (q < bt.njobs && (int)blockIdx.x >= bt.blk0[q]) ? 1 : 0;
+  const TokredArgs& a = bt.job[jb];
+  const int rel = (int)blockIdx.x - bt.blk0[jb];
+  tokred_splits_block<U>(a, rel % a.ntiles, rel / a.ntiles);
+}
+
+hipError_t launch_tokred_splits_batch(const TokredBatch& bt, hipStream_t st) {
+  if (bt.njobs < 1 || bt.njobs > kTokMaxJobs || bt.blocks < 1) return hipErrorInvalidValue;
+  int smax = 1;
+  for (int j = 0; j < bt.njobs; ++j) smax = std::max(smax, (int)bt.job[j].S);
+  const dim3 grid((unsigned)bt.blocks);
+  if (smax <= 2) DPRC_LAUNCH(tokred_splits_batch_kernel<2>, grid, dim3(kBlock), 0, st, bt);
+  else if (smax <= 4) DPRC_LAUNCH(tokred_splits_batch_kernel<4>, grid, dim3(kBlock), 0, st, bt);
+  else DPRC_LAUNCH(tokred_splits_batch_kernel<8>, grid, dim3(kBlock), 0, st, bt);
+  return hipGetLastError();
 }
 
 // estimate of layer g for sample i = scale * sum over tiles (in tile order);

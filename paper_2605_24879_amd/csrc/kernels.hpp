@@ -95,6 +95,14 @@ struct TokredArgs {
   int32_t vec;            // token rows of X are 16-byte aligned
 };
 
+// Token-split sums of several layers' passes in one launch.
+constexpr int kTokMaxJobs = 8;
+struct TokredBatch {
+  int32_t njobs, blocks;
+  int32_t blk0[kTokMaxJobs];     // first block of each job (ntiles * B blocks each)
+  TokredArgs job[kTokMaxJobs];   // S > 1
+};
+
 struct GemmArgs {
   const uint16_t* A;
   int64_t lda, a_ss;
@@ -200,6 +208,13 @@ struct FinalArgs {
   int32_t accumulate;
 };
 int32_t final_chunks(int64_t n);
+// The finalize of several layers (same s, r and B): one launch per step for all of them.
+constexpr int kFinMaxJobs = 8;
+struct FinalBatch {
+  int32_t njobs;
+  int32_t blk0[kFinMaxJobs];     // set by the launchers
+  FinalArgs job[kFinMaxJobs];
+};
 
 hipError_t launch_probe_bits(int probe_kind, uint32_t key0, uint32_t key1, uint32_t layer,
                              uint32_t stream_id, int64_t m, int32_t k, uint32_t* out,
@@ -252,6 +267,7 @@ hipError_t launch_fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t st);
 hipError_t launch_project(const ProjectArgs& a, int rows_per_wg, hipStream_t st);
 hipError_t launch_tokred(const TokredArgs& a, hipStream_t st);
 hipError_t launch_tokred_splits(const TokredArgs& a, hipStream_t st);   // S > 1
+hipError_t launch_tokred_splits_batch(const TokredBatch& bt, hipStream_t st);
 hipError_t launch_tokred_sample(const TokredArgs& a, hipStream_t st);   // mode 0
 hipError_t launch_project_f32(const ProjectF32Args& a, hipStream_t st);
 hipError_t launch_tokred_f32(const TokredF32Args& a, hipStream_t st);
@@ -264,6 +280,10 @@ hipError_t launch_qr_expand(const QrBatch& bt, hipStream_t st);   // a level-0 j
 hipError_t launch_hpp_csum(const FinalArgs& a, hipStream_t st);
 hipError_t launch_hpp_rows(const FinalArgs& a, hipStream_t st);
 hipError_t launch_hpp_sum(const FinalArgs& a, hipStream_t st);
+// the finalize of a group of layers (same s, r, B): C sums, row chunks, per-sample sums in layer order
+hipError_t launch_hpp_csum_batch(const FinalBatch& bt, hipStream_t st);
+hipError_t launch_hpp_rows_batch(const FinalBatch& bt, hipStream_t st);
+hipError_t launch_hpp_sum_batch(const FinalBatch& bt, hipStream_t st);
 hipError_t launch_clip_scale(const float* n2, int64_t B, float C, float* c, hipStream_t st);
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t st);
 hipError_t launch_gemm_f32(const float* A, int64_t lda, int64_t a_ss, const float* E, int64_t lde,
