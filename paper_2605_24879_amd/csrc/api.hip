@@ -372,9 +372,12 @@ dprc_status hutch_f32(const View& v, int32_t k, int probe, uint32_t k0, uint32_t
 
 // G layers (G = 1, or a shared-activation group of bf16 OUT layers): one projection
 // per layer into its columns of a shared Y, then one token reduction.
+// With `defer` (bf16 layers), the split sums and the estimate are not launched: the
+// token-reduction arguments are returned for a batched launch, and the group's token-split
+// partials and tile sums go to `own` instead of the scratch.
 dprc_status hutch_group(const View* v, int G, int32_t k, int probe, uint32_t k0, uint32_t k1, float* n2,
                         float* n2_layers, int accumulate, void* ws, hipStream_t st, float clipC = 0.f,
-                        float* clip_c = nullptr) {
+                        float* clip_c = nullptr, TokredArgs* defer = nullptr, const TokBufs* own = nullptr) {
   if (v[0].dtype != DPRC_BF16) {
     dprc_status s = hutch_f32(v[0], k, probe, k0, k1, n2, n2_layers, accumulate, ws, st);
     if (s != DPRC_SUCCESS || !clip_c) return s;
@@ -424,7 +427,15 @@ dprc_status hutch_group(const View* v, int G, int32_t k, int probe, uint32_t k0,
   ta.scale = 1.0f / (float)k; ta.n2 = n2; ta.n2_layer = n2_layers; ta.accumulate = accumulate;
   ta.clip_C = clipC; ta.clip_c = clip_c;
   ta.vec = rows16(v[0].Xo, v[0].ldo);
+  if (own) {
+    ta.part = own->part;
+    ta.tilesq = own->tilesq;
+  }
   if ((e = traced(DPRC_KERNEL_TOKEN_REDUCE, st, [&] { return launch_tokred(ta, st); })) != hipSuccess) return DPRC_ERROR_HIP;
+  if (defer) {
+    *defer = ta;
+    return DPRC_SUCCESS;
+  }
   if (tp.S > 1 && (e = traced(DPRC_KERNEL_TOKEN_SPLITS, st, [&] { return launch_tokred_splits(ta, st); })) != hipSuccess)
     return DPRC_ERROR_HIP;
   return hip_status(traced(DPRC_KERNEL_SAMPLE_SUM, st, [&] { return launch_tokred_sample(ta, st); }));
@@ -737,6 +748,52 @@ dprc_status dprc_trace_launches(hipEvent_t* events, int32_t* kinds, int32_t capa
   return DPRC_SUCCESS;
 }
 
+// Calls whose layers are all bf16 finish up to kTokMaxJobs activation groups at once: the
+// projections and token reductions of every group, one split-sum launch, then one launch
+// that adds every layer's estimate to n2 in layer order (the clip factors follow the last
+// group of the call).  Each group keeps its own token-split partials and tile sums; the
+// rest of the scratch is shared.
+bool hutch_batched(const dprc_layer* layers, int32_t n) {
+  if (n < 2) return false;
+  for (int32_t l = 0; l < n; ++l)
+    if (layers[l].dtype != DPRC_BF16) return false;
+  return true;
+}
+
+// Up to kTokMaxJobs consecutive activation groups starting at layer l0: their bounds in
+// ends[], their own buffers carved from ws (own may be null) after the shared scratch.
+// Returns the bytes used.
+size_t hutch_batch_layout(const dprc_layer* layers, int32_t l0, int32_t n, int32_t k, int probe, dprc_side side,
+                          void* ws, int32_t* ends, int* ngroups, TokBufs* own) {
+  View v[kMaxGroup];
+  size_t shared = 0;
+  int ng = 0;
+  int32_t l = l0;
+  while (l < n && ng < kTokMaxJobs) {
+    const int32_t le = group_end(layers, l, n, k, side);
+    for (int32_t j = l; j < le; ++j) v[j - l] = view_of(layers[j], side);
+    shared = std::max(shared, hutch_group_ws(v, le - l, k, probe));
+    ends[ng++] = le;
+    l = le;
+  }
+  char* base = static_cast<char*>(ws);
+  size_t off = (shared + kAlign - 1) / kAlign * kAlign;
+  l = l0;
+  for (int q = 0; q < ng; ++q) {
+    const View v0 = view_of(layers[l], side);
+    const int G = ends[q] - l;
+    const TokPlan tp = tok_plan(v0.B, v0.T, v0.n);
+    const size_t pf = tp.S > 1 ? (size_t)v0.B * tp.ntiles * tp.S * pad_cols(G * k) * kTile : 0;
+    if (own) own[q].part = base && pf ? reinterpret_cast<float*>(base + off) : nullptr;
+    off = (off + pf * sizeof(float) + kAlign - 1) / kAlign * kAlign;
+    if (own) own[q].tilesq = base ? reinterpret_cast<double*>(base + off) : nullptr;
+    off = (off + (size_t)G * v0.B * tp.ntiles * sizeof(double) + kAlign - 1) / kAlign * kAlign;
+    l = ends[q];
+  }
+  *ngroups = ng;
+  return off;
+}
+
 size_t dprc_norm_hutch_workspace(const dprc_layer* layers, int32_t num_layers, int32_t k, dprc_probe probe,
                                  dprc_side side) {
   if (check_layers(layers, num_layers, side) != DPRC_SUCCESS || k < 1 || k > 256) return 0;
@@ -749,6 +806,14 @@ size_t dprc_norm_hutch_workspace(const dprc_layer* layers, int32_t num_layers, i
     for (int32_t j = l; j < le; ++j) v[j - l] = view_of(layers[j], side);
     need = std::max(need, hutch_group_ws(v, le - l, k, (int)probe));
     l = le;
+  }
+  if (hutch_batched(layers, num_layers)) {
+    int32_t ends[kTokMaxJobs];
+    int ng = 0;
+    for (int32_t l = 0; l < num_layers;) {
+      need = std::max(need, hutch_batch_layout(layers, l, num_layers, k, (int)probe, side, nullptr, ends, &ng, nullptr));
+      l = ends[ng - 1];
+    }
   }
   return need;
 }
@@ -769,6 +834,32 @@ static dprc_status norm_hutch(const dprc_layer* layers, int32_t num_layers, int3
   key_of(seed, k0, k1);
   const int64_t B = layers[0].B;
   View v[kMaxGroup];
+  if (hutch_batched(layers, num_layers)) {
+    for (int32_t l = 0; l < num_layers;) {
+      int32_t ends[kTokMaxJobs];
+      int ng = 0;
+      TokBufs own[kTokMaxJobs];
+      hutch_batch_layout(layers, l, num_layers, k, (int)probe, side, ws, ends, &ng, own);
+      TokredBatch bt{};
+      for (int q = 0; q < ng; ++q) {
+        const int32_t le = ends[q];
+        for (int32_t j = l; j < le; ++j) v[j - l] = view_of(layers[j], side);
+        TokredArgs ta{};
+        s = hutch_group(v, le - l, k, (int)probe, k0, k1, n2, n2_layers ? n2_layers + (int64_t)l * B : nullptr,
+                        (accumulate || l > 0) ? 1 : 0, ws, stream, 0.f, nullptr, &ta, &own[q]);
+        if (s != DPRC_SUCCESS) return s;
+        bt.blk0[bt.njobs] = bt.blocks;
+        bt.job[bt.njobs++] = ta;
+        l = le;
+      }
+      if ((s = run_splits_batch(bt.job, bt.njobs, stream)) != DPRC_SUCCESS) return s;
+      const bool last = l == num_layers;
+      if (traced(DPRC_KERNEL_SAMPLE_SUM, stream, [&] {
+            return launch_tokred_sample_batch(bt, clipC, last ? clip_c : nullptr, stream); }) != hipSuccess)
+        return DPRC_ERROR_HIP;
+    }
+    return DPRC_SUCCESS;
+  }
   for (int32_t l = 0; l < num_layers;) {
     const int32_t le = group_end(layers, l, num_layers, k, side);
     for (int32_t j = l; j < le; ++j) v[j - l] = view_of(layers[j], side);

@@ -367,6 +367,38 @@ __global__ __launch_bounds__(kBlock) void tokred_sample_kernel(TokredArgs a) {
   }
 }
 
+// Estimates of several token reductions (mode 0) in one launch: sample i walks the jobs
+// in order, each job's layers in order, adding each layer's estimate (tile sums in tile
+// order) to n2 as separate launches would; the clip factor follows the last one.
+__global__ __launch_bounds__(kBlock) void tokred_sample_batch_kernel(TokredBatch bt, float clip_C, float* clip_c) {
+  __shared__ double dred[4];
+  const int i = blockIdx.x;
+  const TokredArgs& a0 = bt.job[0];
+  float n2 = a0.accumulate ? a0.n2[i] : 0.f;
+  for (int j = 0; j < bt.njobs; ++j) {
+    const TokredArgs& a = bt.job[j];
+    for (int g = 0; g < a.nseg; ++g) {
+      const double* ts = a.tilesq + ((int64_t)g * a.B + i) * a.ntiles;
+      double t = 0.0;
+      for (int k = threadIdx.x; k < a.ntiles; k += kBlock) t += ts[k];
+      t = block_sum_d(t, dred);
+      const float est = (float)(t * (double)a.scale);
+      n2 += est;
+      if (threadIdx.x == 0 && a.n2_layer) a.n2_layer[(int64_t)g * a.B + i] = est;
+    }
+  }
+  if (threadIdx.x == 0) {
+    a0.n2[i] = n2;
+    if (clip_c) clip_c[i] = clip_factor(n2, clip_C);
+  }
+}
+
+hipError_t launch_tokred_sample_batch(const TokredBatch& bt, float clip_C, float* clip_c, hipStream_t st) {
+  if (bt.njobs < 1 || bt.njobs > kTokMaxJobs) return hipErrorInvalidValue;
+  DPRC_LAUNCH(tokred_sample_batch_kernel, dim3((unsigned)bt.job[0].B), dim3(kBlock), 0, st, bt, clip_C, clip_c);
+  return hipGetLastError();
+}
+
 hipError_t launch_tokred_splits(const TokredArgs& a, hipStream_t st) {
   const dim3 grid((unsigned)a.ntiles, (unsigned)a.B);
   if (a.S <= 2) DPRC_LAUNCH(tokred_splits_kernel<2>, grid, dim3(kBlock), 0, st, a);

@@ -268,6 +268,8 @@ hipError_t launch_project(const ProjectArgs& a, int rows_per_wg, hipStream_t st)
 hipError_t launch_tokred(const TokredArgs& a, hipStream_t st);
 hipError_t launch_tokred_splits(const TokredArgs& a, hipStream_t st);   // S > 1
 hipError_t launch_tokred_splits_batch(const TokredBatch& bt, hipStream_t st);
+// mode 0: the estimates of the jobs' layers added to n2 in order, then the clip factor (clip_c may be null)
+hipError_t launch_tokred_sample_batch(const TokredBatch& bt, float clip_C, float* clip_c, hipStream_t st);
 hipError_t launch_tokred_sample(const TokredArgs& a, hipStream_t st);   // mode 0
 hipError_t launch_project_f32(const ProjectF32Args& a, hipStream_t st);
 hipError_t launch_tokred_f32(const TokredF32Args& a, hipStream_t st);
