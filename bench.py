@@ -157,7 +157,8 @@ def kernel_bytes_per_step(cfg):
 
 
 TRAFFIC_KERNELS = {"project": ("project_kernel", "paper_2605_24879_amd/csrc/k_project.hip"),
-                   "token_reduce": ("tokred_kernel", "paper_2605_24879_amd/csrc/k_tokred.hip")}
+                   "token_reduce": ("tokred_kernel", "paper_2605_24879_amd/csrc/k_tokred.hip"),
+                   "accumulate": ("gemm_kernel", "paper_2605_24879_amd/csrc/k_gemm.hip")}
 
 
 def measured_traffic(workload, kernel):
@@ -374,7 +375,7 @@ def main():
         flops = sum(2 * B * T * d * p for (_, d, p) in cfg["layers"])
         tf = flops * args.steps / (tot_ms * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": round(tf, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(tf / BF16_PEAK_TFLOPS, 4), "traffic": None, "kernel": dom,
+                "frac": round(tf / BF16_PEAK_TFLOPS, 4), "traffic": measured_traffic(cfg["name"], dom), "kernel": dom,
                 "flops_per_launch": int(flops / launches_per_step), "avg_launch_us": round(tot_ms / cnt * 1e3, 2)}
     else:
         roof = {"bound": "hbm", "achieved": None, "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": None,
