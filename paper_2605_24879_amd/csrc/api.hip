@@ -100,10 +100,13 @@ int pad_cols(int ncols) {
   return -1;
 }
 
-int rows_per_wg(int64_t rows, int ncols_pad) {
+int rows_per_wg(int64_t rows, int ncols_pad, bool dense = false) {
   const int nb = ncols_pad / 16;
   // 32-row workgroups while that still gives 256 or more of them (fixed per-workgroup
-  // costs such as the probe generation are spread over twice the data)
+  // costs such as the probe generation are spread over twice the data).  With dense
+  // columns every workgroup reads the whole dense operand from L2 (as many bytes as its
+  // rows for 32 rows and 16 dense columns), so 64-row workgroups halve that traffic.
+  if (dense && rows >= 64 * 256 && nb <= 4) return 64;
   int rb = 1;
   if (rows >= 8 * 1024) rb = 2;
   while (rb > 1 && rb * nb > 8) rb >>= 1;
@@ -221,7 +224,7 @@ dprc_status run_pass(const PassSpec& ps, int64_t B, int64_t T, uint32_t k0, uint
   pa.ylo_off = (int64_t)ncols_pad * pa.yt_ld; pa.ncols_write = ncols_pad;
   pa.zero_ptr = nullptr; pa.zero_count = 0;
   pa.vec = rows16(ps.X, ps.ldx);
-  hipError_t e = traced(DPRC_KERNEL_PROJECT, st, [&] { return launch_project(pa, rows_per_wg(B * tp.T_pad, ncols_pad), st); });
+  hipError_t e = traced(DPRC_KERNEL_PROJECT, st, [&] { return launch_project(pa, rows_per_wg(B * tp.T_pad, ncols_pad, pa.nd > 0), st); });
   if (e != hipSuccess) return DPRC_ERROR_HIP;
 
   TokredArgs ta;
@@ -414,7 +417,7 @@ dprc_status hutch_group(const View* v, int G, int32_t k, int probe, uint32_t k0,
     pa.ncols_write = G == 1 ? pa.ncols_pad : k;   // inside a shared Y only the layer's own columns
     pa.zero_ptr = nullptr; pa.zero_count = 0;
     pa.vec = rows16(w.X, w.ldx);
-    if ((e = traced(DPRC_KERNEL_PROJECT, st, [&] { return launch_project(pa, rows_per_wg(B * tp.T_pad, pa.ncols_pad), st); })) != hipSuccess)
+    if ((e = traced(DPRC_KERNEL_PROJECT, st, [&] { return launch_project(pa, rows_per_wg(B * tp.T_pad, pa.ncols_pad, pa.nd > 0), st); })) != hipSuccess)
       return DPRC_ERROR_HIP;
   }
   TokredArgs ta{};

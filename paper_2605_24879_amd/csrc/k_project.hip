@@ -302,6 +302,7 @@ hipError_t launch_project(const ProjectArgs& a, int rows_per_wg, hipStream_t st)
   switch (rows_per_wg) {
     case 16: return launch_rb<1>(a, st);
     case 32: return launch_rb<2>(a, st);
+    case 64: return launch_rb<4>(a, st);
     default: return hipErrorInvalidValue;
   }
 }

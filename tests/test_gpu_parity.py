@@ -294,6 +294,21 @@ def test_hutchpp_low_rank_is_exact_deep_tree(D, side):
     assert np.all(_rel(n2.cpu().numpy(), exact) < NORM_RTOL)
 
 
+@pytest.mark.parametrize("estimator", ["hutchpp", "gaussian"])
+def test_dense_columns_many_rows(D, estimator):
+    # B*T >= 16384 token rows: the passes with dense columns (Hutch++ W_S and Q, Gaussian
+    # probes) take 64-row projection workgroups; T is ragged
+    B, T, d, p = 2, 8200, 72, 200
+    A, E = _draw(B, T, d, p, law="student_t", layer=12)
+    if estimator == "hutchpp":
+        n2 = D.dprc_norm_hutchpp([(A, E, 5)], 8, 12, 6)
+        ref = est.hutchpp_layer(_np(A), _np(E), 8, 12, 6, 5)
+    else:
+        n2 = D.dprc_norm_hutch([(A, E, 5)], 16, 6, probe=D.PROBE_GAUSSIAN)
+        ref = est.hutch_layer(_np(A), _np(E), 16, 6, 5, probe="gaussian")
+    assert np.all(_rel(n2.cpu().numpy(), ref) < NORM_RTOL)
+
+
 def test_hutchpp_many_layers_grouped(D):
     # 10 layers: two groups of the batched QR, sketched widths that take 1, 2 and 3 tree levels
     B, T = 2, 160
