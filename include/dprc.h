@@ -102,7 +102,10 @@ typedef struct {
  *   k in [1, 256] (GAUSSIAN probes: k <= 32, else DPRC_ERROR_NOT_SUPPORTED).
  *   All layers must have the same B.
  * Workspace: dprc_norm_hutch_workspace() bytes for the same arguments (0 when
- * they are invalid). */
+ * they are invalid).  When every layer is bf16, up to eight groups of layers
+ * keep their own token-split partials in it at once (their split sums and
+ * estimates take one launch each), so it grows with the number of layers up to
+ * that many groups. */
 size_t dprc_norm_hutch_workspace(const dprc_layer* layers, int32_t num_layers, int32_t k,
                                  dprc_probe probe, dprc_side side);
 dprc_status dprc_norm_hutch(const dprc_layer* layers, int32_t num_layers, int32_t k,
@@ -127,7 +130,10 @@ dprc_status dprc_norm_hutch_clip(const dprc_layer* layers, int32_t num_layers, i
  * s + r <= 256, s <= the sketched dimension.  s = 0 gives Hutchinson with r
  * probes.  A sketched dimension above 2^21 rows returns DPRC_ERROR_NOT_SUPPORTED
  * (the QR tree of 128-row blocks is at most eight levels deep).  Outputs as for
- * dprc_norm_hutch. */
+ * dprc_norm_hutch.  With several bf16 layers and s > 0, up to eight layers keep
+ * their sketches, QR trees and partials in the workspace at once (each level of
+ * their QR trees is one launch for all of them), so dprc_norm_hutchpp_workspace()
+ * grows with the number of layers up to eight. */
 size_t dprc_norm_hutchpp_workspace(const dprc_layer* layers, int32_t num_layers, int32_t s,
                                    int32_t r, dprc_side side);
 dprc_status dprc_norm_hutchpp(const dprc_layer* layers, int32_t num_layers, int32_t s, int32_t r,
