@@ -202,18 +202,11 @@ size_t pass_ws(Arena& ar, int64_t B, int64_t T, int64_t n, int ncols_pad, uint16
 // instead of the pass scratch; with `defer` (store mode), the split sums are not launched
 // and the token-reduction arguments are returned for a batched launch (defer->S tells
 // whether one is needed).
-dprc_status run_pass(const PassSpec& ps, int64_t B, int64_t T, uint32_t k0, uint32_t k1, uint32_t layer,
-                     void* ws, hipStream_t st, float* part = nullptr, TokredArgs* defer = nullptr) {
+// Kernel arguments of one pass over the given Y and token-reduction buffers.
+void pass_args(const PassSpec& ps, int64_t B, int64_t T, uint32_t k0, uint32_t k1, uint32_t layer, uint16_t* Yt,
+               const TokBufs& tb, const TokPlan& tp, ProjectArgs& pa, TokredArgs& ta) {
   const int ncols = ps.nd + ps.nz;
   const int ncols_pad = pad_cols(ncols);
-  Arena ar(ws);
-  uint16_t* Yt;
-  TokBufs tb;
-  TokPlan tp;
-  pass_ws(ar, B, T, ps.n, ncols_pad, &Yt, &tb, &tp);
-  if (part && tp.S > 1) tb.part = part;
-
-  ProjectArgs pa;
   pa.X = ps.X; pa.ldx = ps.ldx; pa.x_ss = T * ps.ldx;
   pa.B = (int32_t)B; pa.T = (int32_t)T; pa.m = (int32_t)ps.m; pa.T_pad = tp.T_pad;
   pa.nd = ps.nd; pa.nz = ps.nz; pa.ncols_pad = ncols_pad;
@@ -224,10 +217,7 @@ dprc_status run_pass(const PassSpec& ps, int64_t B, int64_t T, uint32_t k0, uint
   pa.ylo_off = (int64_t)ncols_pad * pa.yt_ld; pa.ncols_write = ncols_pad;
   pa.zero_ptr = nullptr; pa.zero_count = 0;
   pa.vec = rows16(ps.X, ps.ldx);
-  hipError_t e = traced(DPRC_KERNEL_PROJECT, st, [&] { return launch_project(pa, rows_per_wg(B * tp.T_pad, ncols_pad, pa.nd > 0), st); });
-  if (e != hipSuccess) return DPRC_ERROR_HIP;
 
-  TokredArgs ta;
   ta.X = ps.Xo; ta.ldx = ps.ldo; ta.x_ss = T * ps.ldo;
   ta.B = (int32_t)B; ta.T = (int32_t)T; ta.n = (int32_t)ps.n;
   ta.Yt = Yt; ta.yt_ld = B * tp.T_pad; ta.T_pad = tp.T_pad; ta.ncols = ncols; ta.ncols_pad = ncols_pad;
@@ -239,6 +229,22 @@ dprc_status run_pass(const PassSpec& ps, int64_t B, int64_t T, uint32_t k0, uint
   ta.M = ps.M; ta.m_ld = ps.m_ld; ta.m_ss = (int64_t)ncols * ps.m_ld;
   ta.Mhi = ps.Mhi; ta.Mlo = ps.Mlo; ta.mh_ld = ps.mh_ld; ta.mh_ss = (int64_t)ncols * ps.mh_ld;
   ta.vec = rows16(ps.Xo, ps.ldo);
+}
+
+dprc_status run_pass(const PassSpec& ps, int64_t B, int64_t T, uint32_t k0, uint32_t k1, uint32_t layer,
+                     void* ws, hipStream_t st, float* part = nullptr, TokredArgs* defer = nullptr) {
+  const int ncols_pad = pad_cols(ps.nd + ps.nz);
+  Arena ar(ws);
+  uint16_t* Yt;
+  TokBufs tb;
+  TokPlan tp;
+  pass_ws(ar, B, T, ps.n, ncols_pad, &Yt, &tb, &tp);
+  if (part && tp.S > 1) tb.part = part;
+  ProjectArgs pa;
+  TokredArgs ta;
+  pass_args(ps, B, T, k0, k1, layer, Yt, tb, tp, pa, ta);
+  hipError_t e = traced(DPRC_KERNEL_PROJECT, st, [&] { return launch_project(pa, rows_per_wg(B * tp.T_pad, ncols_pad, pa.nd > 0), st); });
+  if (e != hipSuccess) return DPRC_ERROR_HIP;
   e = traced(DPRC_KERNEL_TOKEN_REDUCE, st, [&] { return launch_tokred(ta, st); });
   if (e != hipSuccess) return DPRC_ERROR_HIP;
   if (defer && ps.mode == 1) {
@@ -458,6 +464,7 @@ struct PPBufs {
   float* Y32;                              // fp32 path
   void* pass_ws;                           // bf16 path: scratch of one pass
   float* part;                             // grouped layers: the layer's own token-split partials
+  uint16_t* Y;                             // grouped layers: the layer's own Y (batched passes)
 };
 
 // Bytes of the bf16 pass scratch of one layer (the Y buffer and token-split partials).
@@ -611,8 +618,7 @@ dprc_status hutchpp_layer(const View& v, int32_t s, int32_t r, uint32_t k0, uint
 
 // Hutch++ pass `which` of a bf16 layer:
 //   1: W_S = Xo^T (X S);  2: O S = X^T (Xo W_S);  3: [U | W_P] = Xo^T (X [Q | P]).
-dprc_status hpp_pass(int which, const View& v, int32_t s, int32_t r, uint32_t k0, uint32_t k1, const PPBufs& b,
-                     hipStream_t st, TokredArgs* defer = nullptr) {
+PassSpec hpp_spec(int which, const View& v, int32_t s, int32_t r, const PPBufs& b) {
   const uint16_t* X = (const uint16_t*)v.X;
   const uint16_t* Xo = (const uint16_t*)v.Xo;
   PassSpec p{};
@@ -632,7 +638,53 @@ dprc_status hpp_pass(int which, const View& v, int32_t s, int32_t r, uint32_t k0
       p.M = b.UW; p.m_ld = v.n;
     }
   }
-  return run_pass(p, v.B, v.T, k0, k1, v.layer_id, b.pass_ws, st, b.part, defer);
+  return p;
+}
+
+dprc_status hpp_pass(int which, const View& v, int32_t s, int32_t r, uint32_t k0, uint32_t k1, const PPBufs& b,
+                     hipStream_t st, TokredArgs* defer = nullptr) {
+  return run_pass(hpp_spec(which, v, s, r, b), v.B, v.T, k0, k1, v.layer_id, b.pass_ws, st, b.part, defer);
+}
+
+// Pass `which` of a group of layers: one projection launch and one token-reduction launch
+// for all of them (each layer has its own Y and partials), the split sums deferred to the
+// caller.  Passes wider than 64 columns take a launch pair per layer.
+dprc_status hpp_pass_group(int which, const View* vs, PPBufs* bufs, int ng, int32_t s, int32_t r, uint32_t k0,
+                           uint32_t k1, hipStream_t st, TokredArgs* def) {
+  const PassSpec p0 = hpp_spec(which, vs[0], s, r, bufs[0]);
+  const int ncols_pad = pad_cols(p0.nd + p0.nz);
+  if (ncols_pad > 64 || ng > kProjMaxJobs || !bufs[0].Y) {
+    for (int q = 0; q < ng; ++q) {
+      const dprc_status stt = hpp_pass(which, vs[q], s, r, k0, k1, bufs[q], st, &def[q]);
+      if (stt != DPRC_SUCCESS) return stt;
+    }
+    return DPRC_SUCCESS;
+  }
+  ProjectArgs pas[kProjMaxJobs];
+  int64_t rows = 0;
+  for (int q = 0; q < ng; ++q) {
+    const PassSpec p = hpp_spec(which, vs[q], s, r, bufs[q]);
+    const TokPlan tp = tok_plan(vs[q].B, vs[q].T, p.n);
+    TokBufs own{tp.S > 1 ? bufs[q].part : nullptr, nullptr};
+    pass_args(p, vs[q].B, vs[q].T, k0, k1, vs[q].layer_id, bufs[q].Y, own, tp, pas[q], def[q]);
+    rows = vs[q].B * tp.T_pad;
+  }
+  // widest layers first, so that the narrow ones fill the tail of each launch
+  int op[kProjMaxJobs], ot[kProjMaxJobs];
+  for (int q = 0; q < ng; ++q) op[q] = ot[q] = q;
+  std::stable_sort(op, op + ng, [&](int a, int b) { return pas[a].m > pas[b].m; });
+  std::stable_sort(ot, ot + ng, [&](int a, int b) { return def[a].n > def[b].n; });
+  ProjectBatch pb{};
+  TokredBatch tb{};
+  for (int q = 0; q < ng; ++q) {
+    pb.job[pb.njobs++] = pas[op[q]];
+    tb.job[tb.njobs++] = def[ot[q]];
+  }
+  const int rpw = rows_per_wg(rows, ncols_pad, p0.nd > 0);
+  if (traced(DPRC_KERNEL_PROJECT, st, [&] { return launch_project_batch(pb, rpw, st); }) != hipSuccess ||
+      traced(DPRC_KERNEL_TOKEN_REDUCE, st, [&] { return launch_tokred_batch(tb, st); }) != hipSuccess)
+    return DPRC_ERROR_HIP;
+  return DPRC_SUCCESS;
 }
 
 // The fp32 Hutch++ path (the tiny workload): SIMT passes, the same QR and finalize.
@@ -915,6 +967,11 @@ size_t hpp_group_layout(const dprc_layer* layers, int32_t l0, int32_t l1, int32_
     if (bufs) bufs[l - l0].part = base && pf > 0 ? reinterpret_cast<float*>(base + off) : nullptr;
     off += (size_t)pf * sizeof(float);
     off = (off + kAlign - 1) / kAlign * kAlign;
+    // and its own Y (the group's passes run as one projection launch and one reduction launch)
+    const size_t ny = (size_t)2 * pad_cols(s + r) * v.B * round_up(v.T, kStage);
+    if (bufs) bufs[l - l0].Y = base ? reinterpret_cast<uint16_t*>(base + off) : nullptr;
+    off += ny * sizeof(uint16_t);
+    off = (off + kAlign - 1) / kAlign * kAlign;
     pass = std::max(pass, hpp_pass_bytes(v, s, r));
   }
   if (bufs)
@@ -971,13 +1028,11 @@ dprc_status dprc_norm_hutchpp(const dprc_layer* layers, int32_t num_layers, int3
       TokredArgs def[kQrMaxJobs];
       // passes 1 and 2 of every layer, each followed by one split-sum launch for the group
       for (int which = 1; which <= 2; ++which) {
-        for (int32_t q = 0; q < ng; ++q)
-          if ((st = hpp_pass(which, views[q], s, r, k0, k1, bufs[q], stream, &def[q])) != DPRC_SUCCESS) return st;
+        if ((st = hpp_pass_group(which, views, bufs, ng, s, r, k0, k1, stream, def)) != DPRC_SUCCESS) return st;
         if ((st = run_splits_batch(def, ng, stream)) != DPRC_SUCCESS) return st;
       }
       if ((st = run_qr(bp, views, ng, k0, k1, true, stream)) != DPRC_SUCCESS) return st;
-      for (int32_t q = 0; q < ng; ++q)
-        if ((st = hpp_pass(3, views[q], s, r, k0, k1, bufs[q], stream, &def[q])) != DPRC_SUCCESS) return st;
+      if ((st = hpp_pass_group(3, views, bufs, ng, s, r, k0, k1, stream, def)) != DPRC_SUCCESS) return st;
       if ((st = run_splits_batch(def, ng, stream)) != DPRC_SUCCESS) return st;
       // the estimates, added to n2 in layer order
       FinalBatch fb{};

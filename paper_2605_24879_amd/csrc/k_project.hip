@@ -40,7 +40,7 @@ struct PInt {
 
 // NBD: column blocks (of 16) holding dense columns, 0 when all columns are probes.
 template <int RB, int NB, int NBD, bool FAST>
-__global__ __launch_bounds__(kBlock) void project_kernel(ProjectArgs a) {
+__device__ __forceinline__ void project_body(const ProjectArgs& a, int bx, int by) {
   extern __shared__ __attribute__((aligned(16))) uint32_t smem[];
   constexpr bool DENSE = NBD > 0;
   constexpr int P = (RB == 1 && !DENSE) ? 4 : 2;  // stages in flight per wave
@@ -48,8 +48,8 @@ __global__ __launch_bounds__(kBlock) void project_kernel(ProjectArgs a) {
   constexpr int ND = DENSE ? 4 * NBD : 1;       // dense operand fragments (hi and lo) per stage
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int g = lane >> 4, l16 = lane & 15;
-  const int i = blockIdx.y;
-  const int t0 = blockIdx.x * 16 * RB;
+  const int i = by;
+  const int t0 = bx * 16 * RB;
   const int wpc = a.words_per_chunk;            // a multiple of 16: chunks are whole stages
   uint32_t* zw = smem;                                            // [nz][wpc + 1]
   uint32_t* region = smem + (a.nz > 0 ? a.nz * (wpc + 1) : 0);
@@ -58,7 +58,7 @@ __global__ __launch_bounds__(kBlock) void project_kernel(ProjectArgs a) {
   float* red = reinterpret_cast<float*>(region);
   constexpr int RS = 16 * NB + 4;                                 // padded row of a reduction slot
 
-  if (a.zero_ptr != nullptr && blockIdx.x == 0 && blockIdx.y == 0)
+  if (a.zero_ptr != nullptr && bx == 0 && by == 0)
     for (int idx = tid; idx < a.zero_count; idx += kBlock) a.zero_ptr[idx] = 0u;
 
   // loads: lane -> row 4j + lane/16 of the tile (j = load index), 16-byte piece
@@ -257,6 +257,91 @@ __global__ __launch_bounds__(kBlock) void project_kernel(ProjectArgs a) {
     split_bf16(y, h, l);
     yhi[(int64_t)c * a.yt_ld + r] = (uint16_t)h;
     ylo[(int64_t)c * a.yt_ld + r] = (uint16_t)l;
+  }
+}
+
+template <int RB, int NB, int NBD, bool FAST>
+__global__ __launch_bounds__(kBlock) void project_kernel(ProjectArgs a) {
+  project_body<RB, NB, NBD, FAST>(a, blockIdx.x, blockIdx.y);
+}
+
+// Projections of several layers in one launch (same instantiation): block (x, sample) of
+// job j at blk0[j] + sample * (T_pad / (16 RB)) + x.
+template <int RB, int NB, int NBD, bool FAST>
+__global__ __launch_bounds__(kBlock) void project_batch_kernel(ProjectBatch bt) {
+  int jb = 0;
+#pragma unroll
+  for (int q = 1; q < kProjMaxJobs; ++q) jb += (q < bt.njobs && (int)blockIdx.x >= bt.blk0[q]) ? 1 : 0;
+  const ProjectArgs& a = bt.job[jb];
+  const int gx = a.T_pad / (16 * RB);
+  const int rel = (int)blockIdx.x - bt.blk0[jb];
+  project_body<RB, NB, NBD, FAST>(a, rel % gx, rel / gx);
+}
+
+template <int RB, int NB>
+static size_t project_lds(const ProjectArgs& a) {
+  const size_t zbytes = a.nz > 0 ? (size_t)a.nz * (a.words_per_chunk + 1) * 4 : 0;
+  const size_t rbytes = std::max((size_t)4 * 16 * RB * (16 * NB + 4) * 4, (size_t)4 * 16 * RB * kProjSlice * 2);
+  return zbytes + rbytes;
+}
+
+template <int RB>
+static bool project_fast(const ProjectArgs& a) {
+  // buffer offsets of one workgroup's rows stay below 2^31
+  return a.vec && a.m % 8 == 0 && (int64_t)16 * RB * a.ldx * 2 < ((int64_t)1 << 31);
+}
+
+template <int RB, int NB>
+static hipError_t launch_batch_rb_nb(const ProjectBatch& bt, hipStream_t st) {
+  size_t lds = 0;
+  bool fast = true;
+  for (int j = 0; j < bt.njobs; ++j) {
+    lds = std::max(lds, project_lds<RB, NB>(bt.job[j]));
+    fast = fast && project_fast<RB>(bt.job[j]);
+  }
+  const int nbd = (bt.job[0].nd + 15) / 16;
+#define DPRC_PROJECT_BATCH_CASE(NBDV)                                                                    \
+  if (nbd == NBDV) {                                                                                      \
+    if (fast) DPRC_LAUNCH((project_batch_kernel<RB, NB, NBDV, true>), dim3(bt.blocks), dim3(kBlock), lds, st, bt); \
+    else DPRC_LAUNCH((project_batch_kernel<RB, NB, NBDV, false>), dim3(bt.blocks), dim3(kBlock), lds, st, bt);     \
+  }
+  DPRC_PROJECT_BATCH_CASE(0)
+  if constexpr (NB >= 1) { DPRC_PROJECT_BATCH_CASE(1) }
+  if constexpr (NB >= 2) { DPRC_PROJECT_BATCH_CASE(2) }
+#undef DPRC_PROJECT_BATCH_CASE
+  return hipGetLastError();
+}
+
+template <int RB>
+static hipError_t launch_batch_rb(const ProjectBatch& bt, hipStream_t st) {
+  switch (bt.job[0].ncols_pad / 16) {
+    case 1: return launch_batch_rb_nb<RB, 1>(bt, st);
+    case 2: return launch_batch_rb_nb<RB, 2>(bt, st);
+    case 3: return launch_batch_rb_nb<RB, 3>(bt, st);
+    case 4: return launch_batch_rb_nb<RB, 4>(bt, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_project_batch(ProjectBatch bt, int rows_per_wg, hipStream_t st) {
+  if (bt.njobs < 1 || bt.njobs > kProjMaxJobs) return hipErrorInvalidValue;
+  const int rb = rows_per_wg / 16;
+  const int nbd = (bt.job[0].nd + 15) / 16;
+  bt.blocks = 0;
+  for (int j = 0; j < bt.njobs; ++j) {
+    const ProjectArgs& a = bt.job[j];
+    // one instantiation serves every job
+    if (a.ncols_pad != bt.job[0].ncols_pad || (a.nd + 15) / 16 != nbd || a.words_per_chunk % 16 != 0 ||
+        a.nd > 32 || a.nd > a.ncols_pad || a.T_pad % rows_per_wg != 0)
+      return hipErrorInvalidValue;
+    bt.blk0[j] = bt.blocks;
+    bt.blocks += (a.T_pad / rows_per_wg) * a.B;
+  }
+  switch (rb) {
+    case 1: return launch_batch_rb<1>(bt, st);
+    case 2: return launch_batch_rb<2>(bt, st);
+    case 4: return launch_batch_rb<4>(bt, st);
+    default: return hipErrorInvalidValue;
   }
 }
 

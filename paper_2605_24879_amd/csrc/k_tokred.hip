@@ -82,7 +82,7 @@ struct Int {
 };
 
 template <int NB, bool FAST>
-__global__ __launch_bounds__(kBlock) void tokred_kernel(TokredArgs a) {
+__device__ __forceinline__ void tokred_body(const TokredArgs& a, int bx, int by) {
   // Y stages go through LDS with X (one 16-byte load per thread per 16 columns)
   // when they are small; wider Y is read straight from global memory at use.
   constexpr bool YLDS = NB <= 4;
@@ -94,8 +94,8 @@ __global__ __launch_bounds__(kBlock) void tokred_kernel(TokredArgs a) {
   static_assert(P == 4, "the stage loop below is written out for four ring slots");
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int g = lane >> 4, l16 = lane & 15, r4 = l16 >> 2, c4 = lane & 3;
-  const int i = blockIdx.y;
-  const int tile = blockIdx.x / a.S, s = blockIdx.x - tile * a.S;
+  const int i = by;
+  const int tile = bx / a.S, s = bx - tile * a.S;
   const int j0 = tile * kTile;
   const int tb = s * a.stages_per_split * kStage;
   const int te = min(a.T, tb + a.stages_per_split * kStage);
@@ -259,6 +259,24 @@ __global__ __launch_bounds__(kBlock) void tokred_kernel(TokredArgs a) {
     }
 }
 
+template <int NB, bool FAST>
+__global__ __launch_bounds__(kBlock) void tokred_kernel(TokredArgs a) {
+  tokred_body<NB, FAST>(a, blockIdx.x, blockIdx.y);
+}
+
+// Token reductions of several layers in one launch (same instantiation): block
+// (tile * S + split, sample) of job j at blk0[j] + sample * ntiles * S + tile * S + split.
+template <int NB, bool FAST>
+__global__ __launch_bounds__(kBlock) void tokred_batch_kernel(TokredBatch bt) {
+  int jb = 0;
+#pragma unroll
+  for (int q = 1; q < kTokMaxJobs; ++q) jb += (q < bt.njobs && (int)blockIdx.x >= bt.blk0[q]) ? 1 : 0;
+  const TokredArgs& a = bt.job[jb];
+  const int gx = a.ntiles * a.S;
+  const int rel = (int)blockIdx.x - bt.blk0[jb];
+  tokred_body<NB, FAST>(a, rel % gx, rel / gx);
+}
+
 // Sum of the token splits of one tile, in split order: its squared norm (mode 0)
 // or the stored tile (mode 1).
 // Sum of the S split partials of one (sample, tile), in split order.  Each thread
@@ -409,6 +427,35 @@ hipError_t launch_tokred_splits(const TokredArgs& a, hipStream_t st) {
 
 hipError_t launch_tokred_sample(const TokredArgs& a, hipStream_t st) {
   DPRC_LAUNCH(tokred_sample_kernel, dim3((unsigned)a.B), dim3(kBlock), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_tokred_batch(TokredBatch bt, hipStream_t st) {
+  if (bt.njobs < 1 || bt.njobs > kTokMaxJobs) return hipErrorInvalidValue;
+  bool fast = true;
+  bt.blocks = 0;
+  for (int j = 0; j < bt.njobs; ++j) {
+    const TokredArgs& a = bt.job[j];
+    if (a.ncols_pad != bt.job[0].ncols_pad) return hipErrorInvalidValue;   // one instantiation
+    // buffer offsets within one 64-row stage stay below 2^31
+    fast = fast && a.vec && a.n % 8 == 0 && (int64_t)kStage * a.ldx * 2 < ((int64_t)1 << 31);
+    bt.blk0[j] = bt.blocks;
+    bt.blocks += a.ntiles * a.S * a.B;
+  }
+  const dim3 grid((unsigned)bt.blocks);
+#define DPRC_TOKRED_BATCH_CASE(NB)                                                             \
+  case NB:                                                                                     \
+    if (fast) DPRC_LAUNCH((tokred_batch_kernel<NB, true>), grid, dim3(kBlock), 0, st, bt);     \
+    else DPRC_LAUNCH((tokred_batch_kernel<NB, false>), grid, dim3(kBlock), 0, st, bt);         \
+    break;
+  switch (bt.job[0].ncols_pad / 16) {
+    DPRC_TOKRED_BATCH_CASE(1)
+    DPRC_TOKRED_BATCH_CASE(2)
+    DPRC_TOKRED_BATCH_CASE(3)
+    DPRC_TOKRED_BATCH_CASE(4)
+    default: return hipErrorInvalidValue;
+  }
+#undef DPRC_TOKRED_BATCH_CASE
   return hipGetLastError();
 }
 

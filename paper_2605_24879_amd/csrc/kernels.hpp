@@ -66,6 +66,15 @@ struct ProjectArgs {
   int32_t vec;              // token rows of X are 16-byte aligned: 16-byte loads
 };
 
+// Projections of several layers in one launch (one kernel instantiation: same columns,
+// same dense-column count, same rows per workgroup).
+constexpr int kProjMaxJobs = 8;
+struct ProjectBatch {
+  int32_t njobs, blocks;         // blocks and blk0 are set by the launcher
+  int32_t blk0[kProjMaxJobs];
+  ProjectArgs job[kProjMaxJobs];
+};
+
 // M_i = X_i^T Y_i per sample (result rows = the n columns of X; result
 // columns = the ncols columns of Y), reduced over tokens in splits.
 // mode 0: squared-norm estimate -> n2; mode 1: store M (fp32 and/or bf16 hi/lo).
@@ -265,6 +274,8 @@ hipError_t launch_gauss_probe(uint32_t key0, uint32_t key1, uint32_t layer, int6
                               uint16_t* hi, uint16_t* lo, float* f32, hipStream_t st);
 hipError_t launch_fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t st);
 hipError_t launch_project(const ProjectArgs& a, int rows_per_wg, hipStream_t st);
+hipError_t launch_project_batch(ProjectBatch bt, int rows_per_wg, hipStream_t st);   // <= 64 columns
+hipError_t launch_tokred_batch(TokredBatch bt, hipStream_t st);                      // <= 64 columns
 hipError_t launch_tokred(const TokredArgs& a, hipStream_t st);
 hipError_t launch_tokred_splits(const TokredArgs& a, hipStream_t st);   // S > 1
 hipError_t launch_tokred_splits_batch(const TokredBatch& bt, hipStream_t st);
