@@ -140,6 +140,7 @@ TokPlan tok_plan(int64_t B, int64_t T, int64_t n) {
 struct TokBufs {
   float* part;
   double* tilesq;
+  uint16_t* Y = nullptr;     // a group's own Y (batched launches)
 };
 
 TokBufs take_tok(Arena& ar, int64_t B, const TokPlan& tp, int ncols_pad, int nseg = 1) {
@@ -386,7 +387,8 @@ dprc_status hutch_f32(const View& v, int32_t k, int probe, uint32_t k0, uint32_t
 // partials and tile sums go to `own` instead of the scratch.
 dprc_status hutch_group(const View* v, int G, int32_t k, int probe, uint32_t k0, uint32_t k1, float* n2,
                         float* n2_layers, int accumulate, void* ws, hipStream_t st, float clipC = 0.f,
-                        float* clip_c = nullptr, TokredArgs* defer = nullptr, const TokBufs* own = nullptr) {
+                        float* clip_c = nullptr, TokredArgs* defer = nullptr, const TokBufs* own = nullptr,
+                        ProjectArgs* pjobs = nullptr, int* npj = nullptr) {
   if (v[0].dtype != DPRC_BF16) {
     dprc_status s = hutch_f32(v[0], k, probe, k0, k1, n2, n2_layers, accumulate, ws, st);
     if (s != DPRC_SUCCESS || !clip_c) return s;
@@ -403,6 +405,7 @@ dprc_status hutch_group(const View* v, int G, int32_t k, int probe, uint32_t k0,
   TokBufs tb;
   TokPlan tp;
   pass_ws(ar, B, T, v[0].n, ncols_pad, &Yt, &tb, &tp, G);
+  if (own && own->Y) Yt = own->Y;
   const int64_t yt_ld = B * tp.T_pad;
   hipError_t e = hipSuccess;
   for (int l = 0; l < G; ++l) {
@@ -423,6 +426,10 @@ dprc_status hutch_group(const View* v, int G, int32_t k, int probe, uint32_t k0,
     pa.ncols_write = G == 1 ? pa.ncols_pad : k;   // inside a shared Y only the layer's own columns
     pa.zero_ptr = nullptr; pa.zero_count = 0;
     pa.vec = rows16(w.X, w.ldx);
+    if (pjobs) {                                   // collected: the caller launches them in batches
+      pjobs[(*npj)++] = pa;
+      continue;
+    }
     if ((e = traced(DPRC_KERNEL_PROJECT, st, [&] { return launch_project(pa, rows_per_wg(B * tp.T_pad, pa.ncols_pad, pa.nd > 0), st); })) != hipSuccess)
       return DPRC_ERROR_HIP;
   }
@@ -439,6 +446,10 @@ dprc_status hutch_group(const View* v, int G, int32_t k, int probe, uint32_t k0,
   if (own) {
     ta.part = own->part;
     ta.tilesq = own->tilesq;
+  }
+  if (pjobs) {
+    *defer = ta;
+    return DPRC_SUCCESS;
   }
   if ((e = traced(DPRC_KERNEL_TOKEN_REDUCE, st, [&] { return launch_tokred(ta, st); })) != hipSuccess) return DPRC_ERROR_HIP;
   if (defer) {
@@ -815,6 +826,43 @@ bool hutch_batched(const dprc_layer* layers, int32_t n) {
   return true;
 }
 
+// The collected projections (widest first, up to kProjMaxJobs per launch) and token
+// reductions (one launch per column count) of a batch of activation groups; work over
+// more than 64 columns takes one launch per layer or group.
+dprc_status hutch_launch_batched(ProjectArgs* pj, int npj, const TokredBatch& groups, hipStream_t st) {
+  std::stable_sort(pj, pj + npj, [](const ProjectArgs& a, const ProjectArgs& b) { return a.m > b.m; });
+  for (int c = 0; c < npj && pj[c].ncols_pad > 64; ++c)    // batched launches take up to 64 columns
+    if (traced(DPRC_KERNEL_PROJECT, st, [&] {
+          return launch_project(pj[c], rows_per_wg((int64_t)pj[c].B * pj[c].T_pad, pj[c].ncols_pad, false), st); }) !=
+        hipSuccess)
+      return DPRC_ERROR_HIP;
+  for (int c = 0; c < npj && pj[0].ncols_pad <= 64; c += kProjMaxJobs) {
+    ProjectBatch pb{};
+    for (int q = c; q < std::min(npj, c + kProjMaxJobs); ++q) pb.job[pb.njobs++] = pj[q];
+    const int rpw = rows_per_wg((int64_t)pb.job[0].B * pb.job[0].T_pad, pb.job[0].ncols_pad, false);
+    if (traced(DPRC_KERNEL_PROJECT, st, [&] { return launch_project_batch(pb, rpw, st); }) != hipSuccess)
+      return DPRC_ERROR_HIP;
+  }
+  TokredArgs tj[kTokMaxJobs];
+  for (int q = 0; q < groups.njobs; ++q) tj[q] = groups.job[q];
+  std::stable_sort(tj, tj + groups.njobs, [](const TokredArgs& a, const TokredArgs& b) {
+    return a.ncols_pad != b.ncols_pad ? a.ncols_pad < b.ncols_pad : a.n > b.n; });
+  for (int q = 0; q < groups.njobs;) {
+    if (tj[q].ncols_pad > 64) {
+      if (traced(DPRC_KERNEL_TOKEN_REDUCE, st, [&] { return launch_tokred(tj[q], st); }) != hipSuccess)
+        return DPRC_ERROR_HIP;
+      ++q;
+      continue;
+    }
+    TokredBatch tb{};
+    const int np = tj[q].ncols_pad;
+    while (q < groups.njobs && tj[q].ncols_pad == np) tb.job[tb.njobs++] = tj[q++];
+    if (traced(DPRC_KERNEL_TOKEN_REDUCE, st, [&] { return launch_tokred_batch(tb, st); }) != hipSuccess)
+      return DPRC_ERROR_HIP;
+  }
+  return DPRC_SUCCESS;
+}
+
 // Up to kTokMaxJobs consecutive activation groups starting at layer l0: their bounds in
 // ends[], their own buffers carved from ws (own may be null) after the shared scratch.
 // Returns the bytes used.
@@ -843,6 +891,12 @@ size_t hutch_batch_layout(const dprc_layer* layers, int32_t l0, int32_t n, int32
     off = (off + pf * sizeof(float) + kAlign - 1) / kAlign * kAlign;
     if (own) own[q].tilesq = base ? reinterpret_cast<double*>(base + off) : nullptr;
     off = (off + (size_t)G * v0.B * tp.ntiles * sizeof(double) + kAlign - 1) / kAlign * kAlign;
+    if (probe != DPRC_PROBE_GAUSSIAN) {          // its own Y: the groups' launches are batched
+      if (own) own[q].Y = base ? reinterpret_cast<uint16_t*>(base + off) : nullptr;
+      off = (off + (size_t)2 * pad_cols(G * k) * v0.B * tp.T_pad * sizeof(uint16_t) + kAlign - 1) / kAlign * kAlign;
+    } else if (own) {
+      own[q].Y = nullptr;
+    }
     l = ends[q];
   }
   *ngroups = ng;
@@ -896,17 +950,22 @@ static dprc_status norm_hutch(const dprc_layer* layers, int32_t num_layers, int3
       TokBufs own[kTokMaxJobs];
       hutch_batch_layout(layers, l, num_layers, k, (int)probe, side, ws, ends, &ng, own);
       TokredBatch bt{};
+      const bool batched = own[0].Y != nullptr;
+      ProjectArgs pj[kTokMaxJobs * kMaxGroup];
+      int npj = 0;
       for (int q = 0; q < ng; ++q) {
         const int32_t le = ends[q];
         for (int32_t j = l; j < le; ++j) v[j - l] = view_of(layers[j], side);
         TokredArgs ta{};
         s = hutch_group(v, le - l, k, (int)probe, k0, k1, n2, n2_layers ? n2_layers + (int64_t)l * B : nullptr,
-                        (accumulate || l > 0) ? 1 : 0, ws, stream, 0.f, nullptr, &ta, &own[q]);
+                        (accumulate || l > 0) ? 1 : 0, ws, stream, 0.f, nullptr, &ta, &own[q],
+                        batched ? pj : nullptr, batched ? &npj : nullptr);
         if (s != DPRC_SUCCESS) return s;
         bt.blk0[bt.njobs] = bt.blocks;
         bt.job[bt.njobs++] = ta;
         l = le;
       }
+      if (batched && (s = hutch_launch_batched(pj, npj, bt, stream)) != DPRC_SUCCESS) return s;
       if ((s = run_splits_batch(bt.job, bt.njobs, stream)) != DPRC_SUCCESS) return s;
       const bool last = l == num_layers;
       if (traced(DPRC_KERNEL_SAMPLE_SUM, stream, [&] {
