@@ -178,6 +178,37 @@ def test_hutch_shared_activations_mixed_sides(D):
         assert np.all(_rel(n2l[j].cpu().numpy(), ref) < NORM_RTOL), j
 
 
+@pytest.mark.parametrize("k,probe", [(16, "rademacher"), (12, "hadamard"), (40, "rademacher"),
+                                     (100, "rademacher")])
+def test_hutch_many_groups_batched(D, k, probe):
+    # 15 bf16 layers in 11 activation groups (two batches of up to eight): shared groups of
+    # three and two layers between single layers, so one batch holds more than eight
+    # projections and token reductions of several column counts (k = 40: groups over 64
+    # columns; k = 100: projections over 64 columns, one launch each)
+    B, T = 2, 150
+    groups = [(96, (130, 72, 72)), (64, (300,)), (136, (520, 260)), (48, (90,)), (80, (200,)),
+              (72, (64,)), (40, (150,)), (88, (110, 96)), (56, (70,)), (64, (260,)), (120, (100,))]
+    pairs, lid = [], 0
+    for g, (d, ps) in enumerate(groups):
+        A, Es = _shared_a(B, T, d, ps, layer0=60 + 10 * g)
+        for E in Es:
+            pairs.append((A, E, lid))
+            lid += 1
+    pid = D.PROBE_HADAMARD if probe == "hadamard" else D.PROBE_RADEMACHER
+    n2l = torch.zeros(len(pairs), B, device="cuda")
+    n2 = D.dprc_norm_hutch(pairs, k, 3, probe=pid, n2_layers=n2l)
+    refs = [est.hutch_layer(_np(A), _np(E), k, 3, j, probe=probe) for (A, E, j) in pairs]
+    got = n2l.cpu().numpy()
+    for j in range(len(pairs)):
+        assert np.all(_rel(got[j], refs[j]) < NORM_RTOL), j
+    assert np.all(_rel(n2.cpu().numpy(), np.sum(refs, axis=0)) < NORM_RTOL)
+    # each layer's estimate as from a call of its own (no batching, no shared reduction)
+    solo = torch.stack([D.dprc_norm_hutch([(A.clone(), E, j)], k, 3, probe=pid) for (A, E, j) in pairs])
+    assert np.all(_rel(got, solo.cpu().numpy()) < 1e-6)
+    if k % 16 == 0:
+        assert torch.equal(n2l, solo)
+
+
 @pytest.mark.parametrize("B,T,p,k", [(1, 64, 4100, 16), (2, 40, 2600, 5), (1, 200, 4096, 32)])
 def test_hutch_few_rows_wide_sketch(D, B, T, p, k):
     # few token rows and a wide sketched side (many 512-column stages per workgroup, ragged end)
