@@ -8,9 +8,10 @@
 // back token-contiguous with the gfx950 LDS transpose read, which is the
 // operand layout of the MFMA (the contraction runs over tokens, X is stored
 // token-major).  Y (bf16 hi + lo, already token-contiguous) is read directly.
-// Splits over tokens are summed in a fixed order by the last workgroup to
-// finish a tile, and per-tile squares by the last tile of a sample, so the
-// result does not depend on scheduling.
+// With several token splits per tile, each split writes its partial tile; a
+// second launch sums the splits of a tile in split order and squares (or
+// stores) the sum, and a third adds the tile sums of each sample in tile
+// order, so the result does not depend on scheduling.
 #include <algorithm>
 #include "device.hpp"
 #include "kernels.hpp"
