@@ -184,8 +184,11 @@ struct PassSpec {
   int32_t nd; const uint16_t* Rhi; const uint16_t* Rlo; int64_t ld_r;   // dense columns
   bool shared_r;                                                        // one R for all samples
   int32_t nz; uint32_t stream_id; int probe_kind;                       // generated columns
+  int32_t z_split; uint32_t stream_id2;    // columns from z_split on: stream_id2 (0: none)
   int mode; float scale; float* n2; float* n2_layer; int accumulate;    // mode 0
   float* M; int64_t m_ld; uint16_t* Mhi; uint16_t* Mlo; int64_t mh_ld;  // mode 1
+  int32_t m_col0, mh_ncols;                // M takes columns >= m_col0, Mhi/Mlo < mh_ncols (0: all)
+  int64_t m_ss, mh_ss;                     // per-sample strides (0: columns x leading dimension)
 };
 
 size_t pass_ws(Arena& ar, int64_t B, int64_t T, int64_t n, int ncols_pad, uint16_t** Yt, TokBufs* tb,
@@ -213,6 +216,7 @@ void pass_args(const PassSpec& ps, int64_t B, int64_t T, uint32_t k0, uint32_t k
   pa.nd = ps.nd; pa.nz = ps.nz; pa.ncols_pad = ncols_pad;
   pa.Rhi = ps.Rhi; pa.Rlo = ps.Rlo; pa.ld_r = ps.ld_r; pa.r_ss = ps.shared_r ? 0 : (int64_t)ps.nd * ps.ld_r;
   pa.probe_kind = ps.probe_kind; pa.key0 = k0; pa.key1 = k1; pa.layer_id = layer; pa.stream_id = ps.stream_id;
+  pa.z_split = ps.z_split > 0 ? ps.z_split : ps.nz; pa.stream_id2 = ps.stream_id2;
   pa.words_per_chunk = words_per_chunk(ps.m, ps.nz);
   pa.Yt = Yt; pa.yt_ld = B * tp.T_pad;
   pa.ylo_off = (int64_t)ncols_pad * pa.yt_ld; pa.ncols_write = ncols_pad;
@@ -227,8 +231,9 @@ void pass_args(const PassSpec& ps, int64_t B, int64_t T, uint32_t k0, uint32_t k
   ta.clip_C = 0.f; ta.clip_c = nullptr;
   ta.part = tb.part; ta.tilesq = tb.tilesq;
   ta.scale = ps.scale; ta.n2 = ps.n2; ta.n2_layer = ps.n2_layer; ta.accumulate = ps.accumulate;
-  ta.M = ps.M; ta.m_ld = ps.m_ld; ta.m_ss = (int64_t)ncols * ps.m_ld;
-  ta.Mhi = ps.Mhi; ta.Mlo = ps.Mlo; ta.mh_ld = ps.mh_ld; ta.mh_ss = (int64_t)ncols * ps.mh_ld;
+  ta.M = ps.M; ta.m_ld = ps.m_ld; ta.m_ss = ps.m_ss > 0 ? ps.m_ss : (int64_t)ncols * ps.m_ld;
+  ta.Mhi = ps.Mhi; ta.Mlo = ps.Mlo; ta.mh_ld = ps.mh_ld; ta.mh_ss = ps.mh_ss > 0 ? ps.mh_ss : (int64_t)ncols * ps.mh_ld;
+  ta.m_col0 = ps.m_col0; ta.mh_ncols = ps.mh_ncols;
   ta.vec = rows16(ps.Xo, ps.ldo);
 }
 
@@ -420,6 +425,7 @@ dprc_status hutch_group(const View* v, int G, int32_t k, int probe, uint32_t k0,
     pa.nd = gauss ? k : 0; pa.nz = gauss ? 0 : k; pa.ncols_pad = pad_cols(k);
     pa.Rhi = gz.hi; pa.Rlo = gz.lo; pa.ld_r = gauss ? ldz : 0; pa.r_ss = 0;
     pa.probe_kind = probe; pa.key0 = k0; pa.key1 = k1; pa.layer_id = w.layer_id; pa.stream_id = 0;
+    pa.z_split = pa.nz; pa.stream_id2 = 0;
     pa.words_per_chunk = words_per_chunk(w.m, pa.nz);
     pa.Yt = Yt + (int64_t)l * k * yt_ld; pa.yt_ld = yt_ld;
     pa.ylo_off = (int64_t)ncols_pad * yt_ld;
@@ -628,7 +634,10 @@ dprc_status hutchpp_layer(const View& v, int32_t s, int32_t r, uint32_t k0, uint
 }
 
 // Hutch++ pass `which` of a bf16 layer:
-//   1: W_S = Xo^T (X S);  2: O S = X^T (Xo W_S);  3: [U | W_P] = Xo^T (X [Q | P]).
+//   1: [W_S | W_P] = Xo^T (X [S | P]);  2: O S = X^T (Xo W_S);  3: U = Xo^T (X Q).
+// The residual probes P do not depend on Q, so they ride along with the sketch S in
+// pass 1 (W_S goes to the bf16 operand of pass 2, W_P to its columns of [U | W_P]);
+// pass 3 then projects Q alone.  Each column's arithmetic is what it would be in pass 3.
 PassSpec hpp_spec(int which, const View& v, int32_t s, int32_t r, const PPBufs& b) {
   const uint16_t* X = (const uint16_t*)v.X;
   const uint16_t* Xo = (const uint16_t*)v.Xo;
@@ -640,13 +649,13 @@ PassSpec hpp_spec(int which, const View& v, int32_t s, int32_t r, const PPBufs& 
   } else {
     p.X = X; p.ldx = v.ldx; p.m = v.m; p.Xo = Xo; p.ldo = v.ldo; p.n = v.n;
     p.mode = 1; p.probe_kind = 0;
+    p.M = b.UW; p.m_ld = v.n; p.m_ss = (int64_t)(s + r) * v.n;     // [U | W_P], [B][s + r][n]
     if (which == 1) {
-      p.nz = s; p.stream_id = 1;
-      p.Mhi = b.WShi; p.Mlo = b.WSlo; p.mh_ld = b.ld_ws;
+      p.nz = s + r; p.stream_id = 1; p.z_split = s; p.stream_id2 = 0;
+      p.Mhi = b.WShi; p.Mlo = b.WSlo; p.mh_ld = b.ld_ws; p.mh_ncols = s; p.mh_ss = (int64_t)s * b.ld_ws;
+      p.m_col0 = s;
     } else {
       p.nd = s; p.Rhi = b.Qhi; p.Rlo = b.Qlo; p.ld_r = b.ld_q;
-      p.nz = r; p.stream_id = 0;
-      p.M = b.UW; p.m_ld = v.n;
     }
   }
   return p;

@@ -189,7 +189,9 @@ __device__ __forceinline__ void project_body(const ProjectArgs& a, int bx, int b
         const uint32_t w0 = wbase + 4u * (uint32_t)b;
         u32x4 v;
         if (a.probe_kind == kProbeRademacher)
-          v = rademacher_block(a.key0, a.key1, a.layer_id, a.stream_id, w0 >> 2, (uint32_t)c);
+          v = c < a.z_split ? rademacher_block(a.key0, a.key1, a.layer_id, a.stream_id, w0 >> 2, (uint32_t)c)
+                            : rademacher_block(a.key0, a.key1, a.layer_id, a.stream_id2, w0 >> 2,
+                                               (uint32_t)(c - a.z_split));
         else
           v = u32x4{hadamard_word(w0, c), hadamard_word(w0 + 1, c), hadamard_word(w0 + 2, c),
                     hadamard_word(w0 + 3, c)};

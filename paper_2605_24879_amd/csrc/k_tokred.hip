@@ -38,13 +38,13 @@ __device__ __forceinline__ double block_sum_d(double v, double* red4) {
 
 __device__ __forceinline__ void store4(const TokredArgs& a, int i, int c, int j, const float v[4]) {
   if (c >= a.ncols) return;
-  if (a.M) {
+  if (a.M && c >= a.m_col0) {
     float* dst = a.M + (int64_t)i * a.m_ss + (int64_t)c * a.m_ld;
 #pragma unroll
     for (int q = 0; q < 4; ++q)
       if (j + q < a.n) dst[j + q] = v[q];
   }
-  if (a.Mhi) {
+  if (a.Mhi && (a.mh_ncols == 0 || c < a.mh_ncols)) {
     uint16_t* hi = a.Mhi + (int64_t)i * a.mh_ss + (int64_t)c * a.mh_ld;
     uint16_t* lo = a.Mlo + (int64_t)i * a.mh_ss + (int64_t)c * a.mh_ld;
 #pragma unroll

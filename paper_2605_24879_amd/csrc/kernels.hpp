@@ -56,6 +56,8 @@ struct ProjectArgs {
   int64_t ld_r, r_ss;
   int32_t probe_kind;
   uint32_t key0, key1, layer_id, stream_id;
+  int32_t z_split;          // generated columns c >= z_split come from stream_id2, as its column c - z_split
+  uint32_t stream_id2;
   int32_t words_per_chunk;  // probe words per column staged in LDS at a time
   uint16_t* Yt;             // hi plane: Yt[c*yt_ld + i*T_pad + t]; lo plane at Yt + ylo_off
   int64_t yt_ld;            // B * T_pad
@@ -101,6 +103,8 @@ struct TokredArgs {
   uint16_t* Mhi;          // Mhi/Mlo[i*mh_ss + c*mh_ld + j]
   uint16_t* Mlo;
   int64_t mh_ld, mh_ss;
+  int32_t m_col0;         // M takes the columns c >= m_col0
+  int32_t mh_ncols;       // Mhi/Mlo take the columns c < mh_ncols (0: all)
   int32_t vec;            // token rows of X are 16-byte aligned
 };
 
