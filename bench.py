@@ -257,6 +257,24 @@ def accumulate_extra(D, torch, workloads, hip, steps):
             "flops_per_launch": flops, "vendor_gemm_tflops_same_shape": round(vendor_tf, 1)}
 
 
+def read_reference(torch, sets, copies, steps):
+    """Context only: torch's own reduction reading the first layer's E (the operand the
+    projection streams) of each rotated input copy in turn, one launch per copy, back to back."""
+    Es = [layers[0][1] for layers in sets]
+    for e in Es[:3]:
+        torch.sum(e, dtype=torch.float32)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for k in range(steps):
+        torch.sum(Es[k % copies], dtype=torch.float32)
+    ev1.record()
+    torch.cuda.synchronize()
+    us = ev0.elapsed_time(ev1) / steps * 1e3
+    nbytes = Es[0].numel() * Es[0].element_size()
+    return {"op": "torch.sum (fp32 accumulation) of E, rotated input copies", "bytes": nbytes,
+            "avg_us": round(us, 2), "GB/s": round(nbytes / (us * 1e-6) / 1e9, 1)}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -395,6 +413,8 @@ def main():
              "hot_cache_tokens_per_s": round(B * T / (hot_ms * 1e-3), 1) if hot_ms else None}
     if not args.no_extra:
         extra["accumulate"] = accumulate_extra(D, torch, workloads, hip, max(5, args.steps // 5))
+        if len(cfg["layers"]) == 1 and copies > 1:
+            extra["vendor_read_same_operand"] = read_reference(torch, sets, copies, args.steps)
     rec = {"metric": "per-sample norm-estimation tokens/s + HBM GB/s (% peak), Llama-3.2-1B shapes",
            "value": round(B * T / (ms_per_step * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1,
            "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5),
