@@ -156,9 +156,10 @@ def kernel_bytes_per_step(cfg):
     return {"project": proj, "token_reduce": tok}
 
 
-TRAFFIC_KERNELS = {"project": ("project_kernel", "paper_2605_24879_amd/csrc/k_project.hip"),
-                   "token_reduce": ("tokred_kernel", "paper_2605_24879_amd/csrc/k_tokred.hip"),
-                   "accumulate": ("gemm_kernel", "paper_2605_24879_amd/csrc/k_gemm.hip")}
+# launch kind -> the kernel families it dispatches (single-layer and batched) and their source
+TRAFFIC_KERNELS = {"project": (("project_kernel", "project_batch_kernel"), "paper_2605_24879_amd/csrc/k_project.hip"),
+                   "token_reduce": (("tokred_kernel", "tokred_batch_kernel"), "paper_2605_24879_amd/csrc/k_tokred.hip"),
+                   "accumulate": (("gemm_kernel",), "paper_2605_24879_amd/csrc/k_gemm.hip")}
 
 
 def measured_traffic(workload, kernel):
@@ -169,15 +170,19 @@ def measured_traffic(workload, kernel):
     path = os.path.join(root, "profiles", f"{workload}_hbm_traffic.json")
     if kernel not in TRAFFIC_KERNELS or not os.path.exists(path):
         return None
-    key, src = TRAFFIC_KERNELS[kernel]
-    rec = json.load(open(path)).get("kernels", {}).get(key)
-    if rec is None:
+    keys, src = TRAFFIC_KERNELS[kernel]
+    kernels = json.load(open(path)).get("kernels", {})
+    recs = [kernels[k] for k in keys if k in kernels]
+    if not recs:
         return None
     sha = lambda p: hashlib.sha256(open(os.path.join(root, p), "rb").read()).hexdigest()[:16]
-    if rec.get("source_sha256_16") != sha(src) or \
-            rec.get("device_hpp_sha256_16") != sha("paper_2605_24879_amd/csrc/device.hpp"):
-        return None
-    return int(rec["read_bytes"] + rec["write_bytes"])
+    for rec in recs:
+        if rec.get("source_sha256_16") != sha(src) or \
+                rec.get("device_hpp_sha256_16") != sha("paper_2605_24879_amd/csrc/device.hpp"):
+            return None
+    # per launch, averaged over the dispatches of the kind's kernel families
+    n = sum(rec.get("dispatches", 1) for rec in recs)
+    return int(sum((rec["read_bytes"] + rec["write_bytes"]) * rec.get("dispatches", 1) for rec in recs) / n)
 
 
 def cpu_baseline(cfg, sets, budget_s):
