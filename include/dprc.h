@@ -135,7 +135,12 @@ dprc_status dprc_norm_hutch_clip(const dprc_layer* layers, int32_t num_layers, i
  * dprc_norm_hutch.  With several bf16 layers and s > 0, up to eight layers keep
  * their sketches, QR trees and partials in the workspace at once (each level of
  * their QR trees is one launch for all of them), so dprc_norm_hutchpp_workspace()
- * grows with the number of layers up to eight. */
+ * grows with the number of layers up to eight.  Such a group's QR runs, half of
+ * the layers at a time, on a second stream that the library creates on first use
+ * (one per device, default priority, kept until the process ends) beside the other
+ * half's passes on `stream`; the call orders all of it back onto `stream` with
+ * events before it returns, so later work on `stream` (and graph capture of the
+ * call) sees one ordered sequence. */
 size_t dprc_norm_hutchpp_workspace(const dprc_layer* layers, int32_t num_layers, int32_t s,
                                    int32_t r, dprc_side side);
 dprc_status dprc_norm_hutchpp(const dprc_layer* layers, int32_t num_layers, int32_t s, int32_t r,
