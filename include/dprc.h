@@ -19,8 +19,9 @@
  *     dprc_layer array itself is HOST memory and is read during the call only.
  *   - Every call is asynchronous on `stream` (0 = the null stream) and returns
  *     after enqueueing; results are valid once the stream reaches that point.
- *   - The library never allocates or frees memory and keeps no global state.
- *     Scratch space is the caller's `ws` buffer of at least the size returned
+ *   - The library never allocates or frees memory and creates no streams or
+ *     events; its only host state is the opt-in, per-thread launch-trace hook
+ *     (dprc_trace_launches).  Scratch space is the caller's `ws` buffer of at least the size returned
  *     by the matching *_workspace() query, 256-byte aligned.  Calls that share
  *     a workspace must be ordered (same stream, or synchronised).
  *   - Arguments are validated on the host before anything is enqueued; a
@@ -135,12 +136,8 @@ dprc_status dprc_norm_hutch_clip(const dprc_layer* layers, int32_t num_layers, i
  * dprc_norm_hutch.  With several bf16 layers and s > 0, up to eight layers keep
  * their sketches, QR trees and partials in the workspace at once (each level of
  * their QR trees is one launch for all of them), so dprc_norm_hutchpp_workspace()
- * grows with the number of layers up to eight.  Such a group's QR runs, half of
- * the layers at a time, on a second stream that the library creates on first use
- * (one per device, default priority, kept until the process ends) beside the other
- * half's passes on `stream`; the call orders all of it back onto `stream` with
- * events before it returns, so later work on `stream` (and graph capture of the
- * call) sees one ordered sequence. */
+ * grows with the number of layers up to eight.  Everything is enqueued on
+ * `stream` alone. */
 size_t dprc_norm_hutchpp_workspace(const dprc_layer* layers, int32_t num_layers, int32_t s,
                                    int32_t r, dprc_side side);
 dprc_status dprc_norm_hutchpp(const dprc_layer* layers, int32_t num_layers, int32_t s, int32_t r,

@@ -43,12 +43,6 @@ def as_f64(x):
     return np.asarray(x, dtype=np.float64)
 
 
-def bf16_bits_to_f64(bits):
-    """Decode bfloat16 bit patterns (uint16) exactly: the value is the float32 with these top bits."""
-    b = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
-    return b.view(np.float32).astype(np.float64)
-
-
 def resolve_side(d, p, side):
     """Which dimension is projected: returns SIDE_OUT (p) or SIDE_IN (d)."""
     if side == SIDE_AUTO:

@@ -1,6 +1,6 @@
 """Build libdprc.so for gfx950 with hipcc (in-tree, next to this file).
 
-    python -m paper_2605_24879_amd.build [--jobs N] [--debug]
+    python -m paper_2605_24879_amd.build [--jobs N] [--debug] [--incremental]
 
 Every .hip source under csrc/ is compiled to an object in _build/ (in
 parallel) and linked into paper_2605_24879_amd/libdprc.so.  Packed-fp32 VALU
@@ -41,13 +41,26 @@ def _compile(src, opt):
     return src, obj, r.returncode, msgs
 
 
-def build(jobs=None, debug=False, verbose=False):
+def _stale(src):
+    """True when the object of `src` is missing or older than the source or a shared header."""
+    obj = os.path.join(BUILD, os.path.basename(src)[:-4] + ".o")
+    if not os.path.exists(obj):
+        return True
+    deps = [src, os.path.join(ROOT, "include", "dprc.h")] + \
+        [os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".hpp")]
+    return any(os.path.getmtime(d) > os.path.getmtime(obj) for d in deps)
+
+
+def build(jobs=None, debug=False, verbose=False, incremental=False):
+    """Compile every source (or, with `incremental`, only those whose object is out of date)
+    and link libdprc.so."""
     os.makedirs(BUILD, exist_ok=True)
     opt = "-O1" if debug else "-O3"
     srcs = sources()
-    objs = []
-    with cf.ThreadPoolExecutor(max_workers=jobs or min(8, len(srcs))) as ex:
-        for src, obj, rc, msgs in ex.map(lambda s: _compile(s, opt), srcs):
+    todo = [s for s in srcs if _stale(s)] if incremental else srcs
+    objs = [os.path.join(BUILD, os.path.basename(s)[:-4] + ".o") for s in srcs if s not in todo]
+    with cf.ThreadPoolExecutor(max_workers=jobs or min(8, max(1, len(todo)))) as ex:
+        for src, obj, rc, msgs in ex.map(lambda s: _compile(s, opt), todo):
             if msgs.strip() and (rc != 0 or verbose):
                 print(msgs, file=sys.stderr)
             if rc != 0:
@@ -68,5 +81,6 @@ if __name__ == "__main__":
     ap.add_argument("--jobs", type=int, default=None)
     ap.add_argument("--debug", action="store_true")
     ap.add_argument("-v", "--verbose", action="store_true")
+    ap.add_argument("--incremental", action="store_true", help="recompile only out-of-date objects")
     a = ap.parse_args()
-    print(build(a.jobs, a.debug, a.verbose))
+    print(build(a.jobs, a.debug, a.verbose, a.incremental))

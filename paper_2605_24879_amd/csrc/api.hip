@@ -4,7 +4,6 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
-#include <mutex>
 #include <vector>
 
 #include "../../include/dprc.h"
@@ -564,36 +563,6 @@ QrJob qr_job(const PPBufs& b, const View& v, int level, uint32_t k0, uint32_t k1
 // with C = Q^T P formed alongside by each layer's last expansion.  The layers' trees are
 // independent, so one launch takes a level of up to kQrMaxJobs layers: the whole step
 // costs (levels of the tallest tree) x 2 launches instead of that many per layer.
-// A second stream per device (default priority, created on first use and kept until the
-// process ends) for work that can run beside the caller's stream: the Hutch++ QR of one
-// half of a group while the other half streams.  Four events order it against the
-// caller's stream; every call joins it back before returning, so graph capture sees one
-// fork and one join per overlapped QR.  Calls on one device share it: a call holds `mu`
-// while it enqueues, so calls from several host threads cannot interleave their event
-// records (their QRs then run one after the other on the side stream).
-struct SideStream {
-  hipStream_t s = nullptr;
-  hipEvent_t ev[4] = {};
-  std::mutex mu;
-};
-
-SideStream* side_stream() {
-  static std::mutex mu;
-  static SideStream side[64];
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
-  std::lock_guard<std::mutex> lk(mu);
-  SideStream& ss = side[dev];
-  if (!ss.s) {
-    hipStream_t st = nullptr;
-    if (hipStreamCreateWithFlags(&st, hipStreamNonBlocking) != hipSuccess) return nullptr;
-    for (hipEvent_t& e : ss.ev)
-      if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return nullptr;
-    ss.s = st;
-  }
-  return &ss;
-}
-
 dprc_status run_qr(PPBufs* const* bs, const View* vs, int n, uint32_t k0, uint32_t k1, bool bf16_out,
                    hipStream_t st) {
   int maxlev = 0;
@@ -1130,34 +1099,9 @@ dprc_status dprc_norm_hutchpp(const dprc_layer* layers, int32_t num_layers, int3
         dprc_status e = hpp_pass_group(which, views + q0, bufs + q0, q1 - q0, s, r, k0, k1, stream, def + q0);
         return e != DPRC_SUCCESS ? e : run_splits_batch(def + q0, q1 - q0, stream);
       };
-      SideStream* side = ng >= 2 ? side_stream() : nullptr;
-      if (side) {
-        // the QR of each half runs on the side stream under the other half's streaming
-        // passes: passes 1, 2 of the first half; its QR beside passes 1, 2 of the second;
-        // the second half's QR beside the first half's pass 3; then the second half's pass 3
-        const int h = (ng + 1) / 2;
-        std::lock_guard<std::mutex> lk(side->mu);
-        auto fork_qr = [&](int q0, int q1, hipEvent_t after, hipEvent_t done) {
-          if (hipEventRecord(after, stream) != hipSuccess || hipStreamWaitEvent(side->s, after, 0) != hipSuccess)
-            return DPRC_ERROR_HIP;
-          const dprc_status e = run_qr(bp + q0, views + q0, q1 - q0, k0, k1, true, side->s);
-          if (e != DPRC_SUCCESS) return e;
-          return hipEventRecord(done, side->s) == hipSuccess ? DPRC_SUCCESS : DPRC_ERROR_HIP;
-        };
-        if ((st = pass(1, 0, h)) != DPRC_SUCCESS || (st = pass(2, 0, h)) != DPRC_SUCCESS ||
-            (st = fork_qr(0, h, side->ev[0], side->ev[1])) != DPRC_SUCCESS ||
-            (st = pass(1, h, ng)) != DPRC_SUCCESS || (st = pass(2, h, ng)) != DPRC_SUCCESS ||
-            (st = fork_qr(h, ng, side->ev[2], side->ev[3])) != DPRC_SUCCESS)
-          return st;
-        if (hipStreamWaitEvent(stream, side->ev[1], 0) != hipSuccess) return DPRC_ERROR_HIP;
-        if ((st = pass(3, 0, h)) != DPRC_SUCCESS) return st;
-        if (hipStreamWaitEvent(stream, side->ev[3], 0) != hipSuccess) return DPRC_ERROR_HIP;
-        if ((st = pass(3, h, ng)) != DPRC_SUCCESS) return st;
-      } else {
-        if ((st = pass(1, 0, ng)) != DPRC_SUCCESS || (st = pass(2, 0, ng)) != DPRC_SUCCESS) return st;
-        if ((st = run_qr(bp, views, ng, k0, k1, true, stream)) != DPRC_SUCCESS) return st;
-        if ((st = pass(3, 0, ng)) != DPRC_SUCCESS) return st;
-      }
+      if ((st = pass(1, 0, ng)) != DPRC_SUCCESS || (st = pass(2, 0, ng)) != DPRC_SUCCESS) return st;
+      if ((st = run_qr(bp, views, ng, k0, k1, true, stream)) != DPRC_SUCCESS) return st;
+      if ((st = pass(3, 0, ng)) != DPRC_SUCCESS) return st;
       // the estimates, added to n2 in layer order
       FinalBatch fb{};
       for (int32_t q = 0; q < ng; ++q) {

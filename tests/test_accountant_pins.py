@@ -131,3 +131,61 @@ def test_accountant_envelope_point_mass_is_a_rescaled_sigma():
     # more noise, less privacy loss; more sampling, more loss
     assert ac.epsilon(1.5, 1000, 100, 2, 1e-5) < ac.epsilon(1.1, 1000, 100, 2, 1e-5)
     assert ac.epsilon(1.1, 1000, 50, 2, 1e-5) < ac.epsilon(1.1, 1000, 100, 2, 1e-5)
+
+
+# ---- envelope binning (Algorithm accounting: bins of the envelope law) -----------------------
+
+@pytest.mark.parametrize("c", [0.3141, 1.0 + 1e-9, 2.99])
+def test_envelope_bins_step_cdf_puts_one_unit_at_the_midpoint_of_its_bin(c):
+    # Y == c: the CDF jumps from 0 to 1 inside the bin (y_{j-1}, y_j] that holds c, so all of
+    # the weight sits there and its representative is that bin's midpoint
+    y0, y1, n = 0.0, 3.0, 300
+    ybar, w = ac.envelope_bins(lambda y: 1.0 if y >= c else 0.0, y0, y1, n)
+    edges = np.linspace(y0, y1, n + 1)
+    j = int(np.searchsorted(edges, c))               # edges[j - 1] < c <= edges[j]
+    assert edges[j - 1] < c <= edges[j]
+    assert w[j - 1] == 1.0 and np.count_nonzero(w) == 1
+    assert abs(ybar[j - 1] - 0.5 * (edges[j - 1] + edges[j])) < 1e-15
+    assert abs(ybar[j - 1] - c) <= 0.5 * (y1 - y0) / n
+
+
+def test_envelope_bins_linear_cdf_gives_equal_weights_and_midpoints():
+    y0, y1, n = 0.5, 2.5, 64
+    ybar, w = ac.envelope_bins(lambda y: (y - y0) / (y1 - y0), y0, y1, n)
+    assert np.allclose(w, 1.0 / n, rtol=0, atol=1e-15)
+    assert np.allclose(ybar, y0 + (np.arange(n) + 0.5) * (y1 - y0) / n, rtol=0, atol=1e-15)
+
+
+def test_envelope_bins_normalise_a_cdf_that_stops_short_of_one():
+    # a law with mass outside [y_min, y_max]: only the increments inside count, rescaled to sum
+    # to one (here half the mass, uniform over the range, so still 1/n per bin)
+    y0, y1, n = 0.0, 1.0, 50
+    ybar, w = ac.envelope_bins(lambda y: 0.25 + 0.5 * y, y0, y1, n)
+    assert abs(w.sum() - 1.0) < 1e-14
+    assert np.allclose(w, 1.0 / n, rtol=0, atol=1e-15)
+
+
+def test_envelope_bins_clip_a_cdf_that_dips():
+    # a CDF evaluated with a small dip (rounding) never yields negative weights: the running
+    # maximum makes it monotone, so the dip's bin and the recovery bin get zero weight
+    vals = {0: 0.0, 1: 0.4, 2: 0.39, 3: 0.4, 4: 1.0}
+    ybar, w = ac.envelope_bins(lambda y: vals[int(round(y))], 0.0, 4.0, 4)
+    assert np.all(w >= 0.0)
+    assert np.allclose(w, [0.4, 0.0, 0.0, 0.6], atol=1e-15)
+
+
+def test_envelope_bins_reproduce_the_chi_square_moments():
+    # Y = chi^2(k)/k: mean 1, variance 2/k.  The binned law puts each bin's mass at the bin
+    # midpoint.  Its mean is a midpoint Riemann-Stieltjes sum whose h^2 term is
+    # (h^2/12) (f(y_max) - f(y_min)) = 0 for a density vanishing at both ends, so it is exact
+    # to rounding (a representative at the bin's right edge would be off by h/2); its variance
+    # exceeds 2/k by h^2/12, Sheppard's correction for grouping into bins of width h.
+    k = 32
+    y_max = 1.0 + 12.0 * math.sqrt(2.0 / k)
+    for n in (100, 400, 1600):
+        h = y_max / n
+        ybar, w = ac.envelope_bins(lambda y: ac.vertex_cdf(y, k), 0.0, y_max, n)
+        mean = float(np.sum(w * ybar))
+        var = float(np.sum(w * ybar ** 2)) - mean * mean
+        assert abs(mean - 1.0) < 1e-9, n
+        assert abs((var - 2.0 / k) / (h * h / 12.0) - 1.0) < 1e-3, n

@@ -73,3 +73,37 @@ def test_graph_replays_match_eager(D, estimator):
         assert torch.equal(c, ref_c), rep
         for g, r in zip(grads, ref_g):
             assert torch.equal(g, r), rep
+
+
+def test_capture_before_any_eager_call(D):
+    # a grouped Hutch++ call (three bf16 layers, one QR launch per tree level for all of them)
+    # captured before the same buffers ever ran eagerly: the call keeps no lazily created
+    # state, so the replays must equal the eager result computed afterwards
+    B, T = 1, 700
+    shapes = [(256, 384), (96, 520), (200, 136)]
+    pairs = []
+    for li, (d, p) in enumerate(shapes):
+        A, E = workloads.draw(B, T, d, p, dtype="bf16", law="student_t", seed=11, layer=li, device="cuda")
+        pairs.append((A, E, li))
+    ws = torch.empty(D.dprc_norm_hutchpp_workspace(pairs, 8, 24), dtype=torch.uint8, device="cuda")
+    n2 = torch.zeros(B, device="cuda")
+    n2l = torch.zeros(len(shapes), B, device="cuda")
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        D.dprc_norm_hutchpp(pairs, 8, 24, 21, n2=n2, n2_layers=n2l, ws=ws)
+    outs = []
+    for _ in range(3):
+        n2.fill_(-1.0)
+        n2l.fill_(-1.0)
+        graph.replay()
+        torch.cuda.synchronize()
+        outs.append((n2.clone(), n2l.clone()))
+    ref_n2 = torch.zeros(B, device="cuda")
+    ref_l = torch.zeros(len(shapes), B, device="cuda")
+    D.dprc_norm_hutchpp(pairs, 8, 24, 21, n2=ref_n2, n2_layers=ref_l, ws=ws)
+    torch.cuda.synchronize()
+    assert torch.all(ref_n2 > 0)
+    for rep, (a, b) in enumerate(outs):
+        assert torch.equal(a, ref_n2), rep
+        assert torch.equal(b, ref_l), rep
