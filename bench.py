@@ -1,23 +1,29 @@
 #!/usr/bin/env python3
 """Throughput of randomized per-sample norm estimation (DP-SGD-RC) on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload q_proj|tiny|mlp|decoder|stack]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload stack|q_proj|tiny|mlp|decoder]
                     [--probe rademacher|gaussian]
 
 One step is one pass of the workload's hot path over one batch already
 resident in HBM: the norm estimates of every layer (Hutchinson, or Hutch++ for
 ``decoder``) summed per sample, the clip factors, and -- where the workload
 has them -- the clipped accumulation of every layer and the Gaussian noise.
-The default workload is one Llama-3.2-1B q_proj-shaped layer (B=4, T=2048,
-d=p=2048, bf16, k=16 Rademacher probes, clip C=1).  Inputs are synthetic
-(seeded) and several copies are rotated so that the 256 MB Infinity Cache
-does not serve a step from a previous step's reads.
+The default workload is the whole Llama-3.2-1B linear stack: 16 decoder layers
+x 7 projections plus a 2048 -> 128256 lm_head, B=8, T=4096, bf16, k=32
+Rademacher probes, clip C=1, clipped accumulation and noise sigma=0.8 (54.7 GB
+of inputs).  Inputs are synthetic (seeded); workloads smaller than the 256 MB
+Infinity Cache rotate several input copies.
 
-Prints one JSON line.  ``roofline`` covers the kernel that takes the most time
-in the step, timed with HIP events around each launch on the launch stream;
-``extra.accumulate`` times the clipped-accumulation GEMM on an mlp-shaped
-layer against the bf16 matrix-core peak; ``cpu_baseline`` is the CPU oracle
-timed on a bounded sample of the same workload.
+Prints one JSON line.  ``value`` is the norm stage's tokens/s, B*T / t_norm,
+with t_norm the wall time of the norm call (every pass, the finishing kernels
+and the clip factors) between HIP events on the launch stream, averaged over
+the K timed steps; ``ms_per_step`` is the whole step.  ``roofline`` covers the
+norm stage's dominant streaming kernel: algorithmic bytes per launch over its
+average launch duration, each launch bracketed by HIP events that the dispatch
+itself stamps, during the same timed steps.  ``extra.accumulate`` gives the
+clipped-accumulation GEMM's matrix-core throughput on the same workload and
+steps; ``cpu_baseline`` is the CPU oracle timed on a bounded sample of the
+same workload (its norm leg, plus its accumulation-and-noise leg).
 """
 
 import argparse
@@ -35,16 +41,17 @@ BF16_PEAK_TFLOPS = 2500.0       # MI355X dense bf16 matrix cores
 def parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="q_proj")
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="stack")
     ap.add_argument("--probe", default="rademacher", choices=["rademacher", "gaussian"],
                     help="Hutchinson probe family (Gaussian: dense columns, k <= 32)")
     ap.add_argument("--rotate-bytes", type=float, default=1.2e9,
                     help="total bytes of rotated input copies (defeats the 256 MB Infinity Cache)")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU oracle sample")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-extra", action="store_true", help="skip the accumulation-GEMM measurement")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="skip the context measurements (vendor GEMM and read references)")
     ap.add_argument("--graph", action="store_true",
                     help="replay a captured HIP graph per step instead of launching from the host")
     ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="BYTES",
@@ -99,21 +106,56 @@ def probe_id(D, cfg):
 
 
 def step_fn(cfg, D, torch, ws_norm, grads, ws_acc):
+    """One step: the norm stage (with the clip factors), then the clipped accumulation and the
+    noise of every layer where the workload has them.  `marks` (two events, may be None) are
+    recorded on the launch stream around the norm stage."""
     C = cfg["C"]
     probe = probe_id(D, cfg)
 
-    def step(layers, n2, c):
+    def step(layers, n2, c, marks=None):
+        if marks is not None:
+            marks[0].record()
         if cfg["estimator"] == "hutch":       # norms and clip factors in the same launches
             D.dprc_norm_hutch_clip(layers, cfg["k"], 0, C, n2=n2, c=c, ws=ws_norm, probe=probe)
         else:
             D.dprc_norm_hutchpp(layers, cfg["s"], cfg["r"], 0, n2=n2, ws=ws_norm)
             D.dprc_clip_scale(n2, C, c=c)
+        if marks is not None:
+            marks[1].record()
         if cfg["accumulate"]:
             for (A, E, li), g in zip(layers, grads):
                 D.dprc_clip_accumulate(A, E, c, grad=g, ws=ws_acc)
                 if cfg["noise_sigma"] is not None:
                     D.dprc_add_noise(g, cfg["noise_sigma"], C, 0, li)
     return step
+
+
+class LaunchTrace:
+    """While active, every library launch from this thread is bracketed by HIP events that the
+    dispatch stamps itself (dprc_trace_launches); records() gives (kind, ms) per launch."""
+
+    def __init__(self, hip, D, capacity):
+        self.hip, self.D, self.capacity = hip, D, capacity
+        self.events = hip.events(2 * capacity)
+        self.kinds = (ctypes.c_int32 * capacity)()
+        self.count = ctypes.c_int32(0)
+
+    def __enter__(self):
+        self.D.dprc_trace_launches(ctypes.cast(self.events, ctypes.c_void_p), ctypes.cast(self.kinds, ctypes.c_void_p),
+                                   self.capacity, ctypes.cast(ctypes.pointer(self.count), ctypes.c_void_p))
+        return self
+
+    def __exit__(self, *exc):
+        self.D.dprc_trace_launches(None, None, 0, None)
+        return False
+
+    def records(self):
+        if self.count.value >= self.capacity:
+            raise RuntimeError(f"launch trace full ({self.capacity} launches): per-kernel figures would be wrong")
+        out = [(self.D.KERNEL_NAMES.get(self.kinds[j], str(self.kinds[j])),
+                self.hip.elapsed_ms(self.events[2 * j], self.events[2 * j + 1])) for j in range(self.count.value)]
+        self.hip.destroy(self.events)
+        return out
 
 
 def trace_kernels(hip, D, fn, reps, capacity=4096):
@@ -185,69 +227,103 @@ def measured_traffic(workload, kernel):
     return int(sum((rec["read_bytes"] + rec["write_bytes"]) * rec.get("dispatches", 1) for rec in recs) / n)
 
 
-def cpu_baseline(cfg, sets, budget_s):
-    """The oracle (fp64 numpy, explicit per-sample gradients) on a bounded sample of the workload."""
+CPU_MAX_COLS = 1 << 15      # widest operand slice the CPU oracle sample takes (cost is linear in width)
+
+
+def cpu_baseline(cfg, layers, budget_s):
+    """The oracle (fp64 numpy, explicit per-sample gradients G_i = A_i^T E_i) timed on one sample
+    of each distinct layer shape of the workload, and scaled to the whole workload by the number
+    of (layer, sample) pairs of that shape.  Legs: the norm stage (G_i, then the estimator) and
+    the clipped accumulation plus noise (G_i scaled into the layer sum, noise on every element).
+    Operands wider than CPU_MAX_COLS columns are cut to that many and the time scaled by the
+    width.  Shapes are cycled until the budget is spent (every shape at least once)."""
     import numpy as np
     from threadpoolctl import threadpool_info
     from oracle import estimators as est
-    from oracle import philox
-    layers = sets[0]
-    B, T = cfg["B"], cfg["T"]
-    done_tokens = 0
-    pairs = []
+    B = cfg["B"]
+    first = {}
+    for (A, E, li) in layers:
+        first.setdefault((A.shape[2], E.shape[2]), (A, E, li))
+    count = {}
+    for (_, d, p) in cfg["layers"]:
+        count[(d, p)] = count.get((d, p), 0) + 1
+    t_norm = {s: [] for s in first}
+    t_acc = {s: [] for s in first}
+    t_noise = []
+    kind = cfg.get("probe", "rademacher")
     t0 = time.perf_counter()
-    # (layer, sample) pairs in order, cycled until the budget is spent (small workloads finish a
-    # pass in well under a second)
-    while time.perf_counter() - t0 <= budget_s:
-        for (A, E, li) in layers:
-            _, d, p = cfg["layers"][li]
-            for i in range(B):
-                Ai = A[i].float().cpu().numpy().astype(np.float64)
-                Ei = E[i].float().cpu().numpy().astype(np.float64)
-                if cfg["estimator"] == "hutch":
-                    kind = cfg.get("probe", "rademacher")
-                    Z = est.probe_matrix(kind, 0, li, 0, p, cfg["k"])
-                    est.hutch_layer(Ai[None], Ei[None], cfg["k"], 0, li, probe=kind, Z=Z)
-                else:
-                    est.hutchpp_layer(Ai[None], Ei[None], cfg["s"], cfg["r"], 0, li)
-                done_tokens += T
-                pairs.append(f"{cfg['layers'][li][0]}[{i}]")
-                if time.perf_counter() - t0 > budget_s:
-                    break
-            if time.perf_counter() - t0 > budget_s:
-                break
-    dt = time.perf_counter() - t0
+    while True:
+        for (d, p), (A, E, li) in first.items():
+            pc = min(p, CPU_MAX_COLS)
+            scale = p / pc
+            t1 = time.perf_counter()
+            Ai = A[0:1].float().cpu().numpy().astype(np.float64)
+            Ei = E[0:1, :, :pc].float().cpu().numpy().astype(np.float64)
+            if cfg["estimator"] == "hutch":
+                est.hutch_layer(Ai, Ei, cfg["k"], 0, li, probe=kind)
+            else:
+                est.hutchpp_layer(Ai, Ei, cfg["s"], cfg["r"], 0, li)
+            t2 = time.perf_counter()
+            if cfg["accumulate"]:
+                est.clip_accumulate(Ai, Ei, np.array([0.5]))
+            t3 = time.perf_counter()
+            t_norm[(d, p)].append((t2 - t1) * scale)
+            t_acc[(d, p)].append((t3 - t2) * scale)
+        if cfg["noise_sigma"] is not None:
+            n = 1 << 22
+            t1 = time.perf_counter()
+            est.add_noise(np.zeros(n), cfg["noise_sigma"], cfg["C"], 0, 0)
+            t_noise.append((time.perf_counter() - t1) / n)
+        if time.perf_counter() - t0 > budget_s:
+            break
+    wall = time.perf_counter() - t0
+    mean = lambda v: sum(v) / len(v)
+    norm_s = sum(count[s] * B * mean(t_norm[s]) for s in first)
+    noise_s = sum(count[(d, p)] * d * p for (d, p) in first) * mean(t_noise) if t_noise else 0.0
+    acc_s = sum(count[s] * B * mean(t_acc[s]) for s in first) + noise_s if cfg["accumulate"] else None
     info = threadpool_info()
     threads = max([x.get("num_threads", 1) for x in info] or [1])
-    # the oracle's norm stage over all layers: tokens/s per layer-sample pass, scaled to whole-step tokens
-    layer_tokens = B * T * len(cfg["layers"])
-    return {"value": done_tokens / dt * (B * T) / layer_tokens, "unit": "tokens/s", "cores": threads,
-            "kind": "oracle",
-            "sample": f"fp64 explicit per-sample gradients + Hutchinson for {len(pairs)} (layer, sample) pair "
-                      f"evaluations ({', '.join(pairs[:6])}{'...' if len(pairs) > 6 else ''}; pairs cycled in "
-                      f"order until the budget was spent) in {dt:.1f} s; "
-                      f"blas={','.join(sorted(set(x.get('internal_api', '?') for x in info))) or 'unknown'}, "
-                      f"os.cpu_count={os.cpu_count()}, affinity={len(os.sched_getaffinity(0))}"}
+    blas = ",".join(sorted(set(f"{x.get('internal_api', '?')}" for x in info))) or "unknown"
+    shapes = ", ".join(f"{d}x{p}" + (f" (first {CPU_MAX_COLS} cols, x{p / CPU_MAX_COLS:.2f})" if p > CPU_MAX_COLS else "")
+                       + f" x{len(t_norm[(d, p)])}" for (d, p) in first)
+    out = {"value": B * cfg["T"] / norm_s, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+           "sample": f"fp64 oracle on one sample of each distinct layer shape ({shapes} passes), scaled by the "
+                     f"workload's {sum(count.values())} layers x B={B} samples; {wall:.1f} s of CPU work; "
+                     f"blas={blas}, os.cpu_count={os.cpu_count()}, affinity={len(os.sched_getaffinity(0))}",
+           "norm_s_per_step": round(norm_s, 3)}
+    if acc_s is not None:
+        out["accumulate_noise_s_per_step"] = round(acc_s, 3)
+        out["accumulate_noise_note"] = ("explicit G_i scaled into the layer sum for every (layer, sample) pair, "
+                                        "plus Box-Muller noise per element (timed on 4M elements)"
+                                        if noise_s else "explicit G_i scaled into the layer sum")
+    return out
 
 
-def accumulate_extra(D, torch, workloads, hip, steps):
-    """Clipped accumulation GEMM on one mlp gate layer (d=2048, p=8192, B=2, T=8192)."""
-    cfg = workloads.BY_NAME["mlp"]
-    A, E = workloads.layer_inputs(cfg, 0, device="cuda")
-    c = torch.tensor([0.37, 0.81], device="cuda")
-    g = torch.empty(A.shape[2], E.shape[2], device="cuda")
-    for _ in range(3):
-        D.dprc_clip_accumulate(A, E, c, grad=g)
-    recs = trace_kernels(hip, D, lambda: D.dprc_clip_accumulate(A, E, c, grad=g), steps)
-    t = [ms for (k, ms) in recs if k == "accumulate"]
-    avg_ms = sum(t) / len(t)
-    flops = 2.0 * cfg["B"] * cfg["T"] * A.shape[2] * E.shape[2]
-    tf = flops / (avg_ms * 1e-3) / 1e12
-    # context only: the vendor bf16 GEMM (hipBLASLt through torch) on the same operands and layout
-    # (both token-major, A^T E over B*T tokens), without the per-sample factors
+def accumulate_roofline(cfg, per_kind, steps):
+    """The clipped-accumulation GEMM of the timed steps against the bf16 matrix-core peak."""
+    tot_ms, cnt = per_kind.get("accumulate", (0.0, 0))
+    if not cnt:
+        return None
+    flops = workloads_accumulate_flops(cfg)
+    tf = flops * steps / (tot_ms * 1e-3) / 1e12
+    red_ms = per_kind.get("splitk_reduce", (0.0, 0))[0]
+    return {"kernel": "accumulate", "bound": "mfma", "achieved": round(tf, 1), "peak": BF16_PEAK_TFLOPS,
+            "unit": "TFLOP/s", "frac": round(tf / BF16_PEAK_TFLOPS, 4), "launches_per_step": cnt / steps,
+            "avg_launch_us": round(tot_ms / cnt * 1e3, 2), "flops_per_step": flops,
+            "gemm_ms_per_step": round(tot_ms / steps, 3), "splitk_reduce_ms_per_step": round(red_ms / steps, 3),
+            "with_splitk_reduce_frac": round(flops * steps / ((tot_ms + red_ms) * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4)}
+
+
+def workloads_accumulate_flops(cfg):
+    return sum(2 * cfg["B"] * cfg["T"] * d * p for (_, d, p) in cfg["layers"])
+
+
+def vendor_gemm(torch, A, E, steps):
+    """Context only: the vendor bf16 GEMM (hipBLASLt through torch) on one layer's operands in the
+    accumulation's layout (both token-major, A^T E over B*T tokens), without per-sample factors."""
     A2 = A.reshape(-1, A.shape[2])
     E2 = E.reshape(-1, E.shape[2])
-    for _ in range(3):
+    for _ in range(2):
         A2.t() @ E2
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     ev0.record()
@@ -255,11 +331,8 @@ def accumulate_extra(D, torch, workloads, hip, steps):
         A2.t() @ E2
     ev1.record()
     torch.cuda.synchronize()
-    vendor_tf = flops / (ev0.elapsed_time(ev1) / steps * 1e-3) / 1e12
-    return {"workload": "mlp.gate B=2 T=8192 d=2048 p=8192", "kernel": "accumulate",
-            "bound": "mfma", "achieved": round(tf, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-            "frac": round(tf / BF16_PEAK_TFLOPS, 4), "avg_launch_us": round(avg_ms * 1e3, 2),
-            "flops_per_launch": flops, "vendor_gemm_tflops_same_shape": round(vendor_tf, 1)}
+    flops = 2.0 * A2.shape[0] * A2.shape[1] * E2.shape[1]
+    return round(flops / (ev0.elapsed_time(ev1) / steps * 1e-3) / 1e12, 1)
 
 
 def read_reference(torch, sets, copies, steps):
@@ -278,6 +351,11 @@ def read_reference(torch, sets, copies, steps):
     nbytes = Es[0].numel() * Es[0].element_size()
     return {"op": "torch.sum (fp32 accumulation) of E, rotated input copies", "bytes": nbytes,
             "avg_us": round(us, 2), "GB/s": round(nbytes / (us * 1e-6) / 1e9, 1)}
+
+
+NORM_KINDS = ("project", "token_reduce", "token_splits", "sample_sum", "qr", "qr_combine", "qr_expand",
+              "hutchpp_final", "hutchpp_sum", "project_f32", "token_reduce_f32", "sample_sq", "probe_bits",
+              "probe_gauss", "clip_scale")
 
 
 def main():
@@ -317,11 +395,12 @@ def main():
     in_bytes = sum(B * T * (d + p) * elem for (_, d, p) in cfg["layers"])
     copies = max(1, min(32, math.ceil(args.rotate_bytes / in_bytes))) if in_bytes < 256e6 else 1
     print(f"[bench] workload={cfg['name']} layers={len(cfg['layers'])} input={in_bytes/1e9:.3f} GB "
-          f"copies={copies}", file=sys.stderr, flush=True)
+          f"copies={copies}: drawing inputs", file=sys.stderr, flush=True)
     sets = make_inputs(cfg, torch, workloads, copies)
     pairs0 = sets[0]
     if cfg["estimator"] == "hutch":
-        ws_n = torch.empty(max(1, D.dprc_norm_hutch_workspace(pairs0, cfg["k"], probe=probe_id(D, cfg))), dtype=torch.uint8, device="cuda")
+        ws_n = torch.empty(max(1, D.dprc_norm_hutch_workspace(pairs0, cfg["k"], probe=probe_id(D, cfg))),
+                           dtype=torch.uint8, device="cuda")
     else:
         ws_n = torch.empty(max(1, D.dprc_norm_hutchpp_workspace(pairs0, cfg["s"], cfg["r"])), dtype=torch.uint8,
                            device="cuda")
@@ -333,105 +412,145 @@ def main():
         need = max(D.dprc_clip_accumulate_workspace(A, E) for (A, E, _) in pairs0)
         ws_acc = torch.empty(max(1, need), dtype=torch.uint8, device="cuda")
     step = step_fn(cfg, D, torch, ws_n, grads, ws_acc)
+    torch.cuda.synchronize()
+    print("[bench] inputs resident; warming up", file=sys.stderr, flush=True)
 
     for w in range(max(args.warmup, 1)):
         step(sets[w % copies], n2, c)
     torch.cuda.synchronize()
-    run = lambda s: step(sets[s % copies], n2, c)
+    Ev = lambda: torch.cuda.Event(enable_timing=True)
+    graphs = None
     if args.graph:
-        # one captured graph per input copy; the library enqueues on torch's capture stream
+        # per input copy: one captured graph for the norm stage and one for the rest of the step,
+        # so that events between the replays bracket the norm stage
         graphs = []
         for ci in range(copies):
-            gr = torch.cuda.CUDAGraph()
+            gn, gr = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gn):
+                step_norm_only(cfg, D, sets[ci], n2, c, ws_n)
             with torch.cuda.graph(gr):
-                step(sets[ci], n2, c)
-            graphs.append(gr)
+                step_rest_only(cfg, D, sets[ci], c, grads, ws_acc)
+            graphs.append((gn, gr))
         for w in range(args.warmup):
-            graphs[w % copies].replay()
+            graphs[w % copies][0].replay()
+            graphs[w % copies][1].replay()
         torch.cuda.synchronize()
-        run = lambda s: graphs[s % copies].replay()
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    t_start.record()
-    for s in range(args.steps):
-        run(s)
-    t_end.record()
+
+    # launches per step, to size the per-launch trace of the timed steps
+    hip = Hip()
+    probe_trace = LaunchTrace(hip, D, 1 << 15)
+    with probe_trace:
+        step(sets[0], n2, c)
+    torch.cuda.synchronize()
+    per_step = len(probe_trace.records())
+
+    # the timed steps: a whole-step bracket, the norm stage bracketed per step, and every
+    # library launch bracketed by the events its dispatch stamps (graph replays are not traced)
+    marks = [(Ev(), Ev()) for _ in range(args.steps)]
+    t_start, t_end = Ev(), Ev()
+    trace = LaunchTrace(hip, D, per_step * args.steps + 16)
+    with trace:
+        t_start.record()
+        for s_ in range(args.steps):
+            if graphs is None:
+                step(sets[s_ % copies], n2, c, marks[s_])
+            else:
+                marks[s_][0].record()
+                graphs[s_ % copies][0].replay()
+                marks[s_][1].record()
+                graphs[s_ % copies][1].replay()
+        t_end.record()
     torch.cuda.synchronize()
     ms_per_step = t_start.elapsed_time(t_end) / args.steps
+    norm_ms = sum(a.elapsed_time(b) for (a, b) in marks) / args.steps
     print(f"[bench] timed {args.steps} steps ({'graph replay' if args.graph else 'eager'}): "
-          f"{ms_per_step*1e3:.2f} us/step", file=sys.stderr, flush=True)
+          f"{ms_per_step:.3f} ms/step, norm stage {norm_ms:.3f} ms", file=sys.stderr, flush=True)
+    recs = trace.records()
+
     # context only: the same steps on one input copy, which the 256 MB Infinity Cache may hold
-    hot_ms = None
+    hot_norm_ms = None
     if copies > 1:
         for _ in range(3):
             step(sets[0], n2, c)
-        t_start.record()
-        for _ in range(args.steps):
-            step(sets[0], n2, c)
-        t_end.record()
+        hm = [(Ev(), Ev()) for _ in range(args.steps)]
+        for s_ in range(args.steps):
+            step(sets[0], n2, c, hm[s_])
         torch.cuda.synchronize()
-        hot_ms = t_start.elapsed_time(t_end) / args.steps
+        hot_norm_ms = sum(a.elapsed_time(b) for (a, b) in hm) / args.steps
 
-    # per-kernel durations over the same number of steps, with the launch hook on
-    hip = Hip()
-    it = iter(range(10 ** 9))
-    # one traced step sizes the trace (the stack workload launches several hundred kernels per step)
-    per_step = len(trace_kernels(hip, D, lambda: step(sets[0], n2, c), 1, capacity=1 << 14))
-    recs = trace_kernels(hip, D, lambda: step(sets[next(it) % copies], n2, c), args.steps,
-                         capacity=per_step * args.steps + 16)
     per_kind = {}
     for k, ms in recs:
         tot, cnt = per_kind.get(k, (0.0, 0))
         per_kind[k] = (tot + ms, cnt + 1)
-    dom = max(per_kind, key=lambda k: per_kind[k][0])
     kb = kernel_bytes_per_step(cfg)
-    tot_ms, cnt = per_kind[dom]
-    launches_per_step = cnt / args.steps
-    if dom in kb:
-        bytes_per_launch = kb[dom] / launches_per_step
-        achieved = kb[dom] * args.steps / (tot_ms * 1e-3) / 1e9
-        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": measured_traffic(cfg["name"] + ("_gaussian" if cfg.get("probe") == "gaussian" else ""), dom),
-                "kernel": dom,
-                "bytes_per_launch": int(bytes_per_launch), "avg_launch_us": round(tot_ms / cnt * 1e3, 2)}
-    elif dom == "accumulate":
-        flops = sum(2 * B * T * d * p for (_, d, p) in cfg["layers"])
-        tf = flops * args.steps / (tot_ms * 1e-3) / 1e12
-        roof = {"bound": "mfma", "achieved": round(tf, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(tf / BF16_PEAK_TFLOPS, 4), "traffic": measured_traffic(cfg["name"], dom), "kernel": dom,
-                "flops_per_launch": int(flops / launches_per_step), "avg_launch_us": round(tot_ms / cnt * 1e3, 2)}
-    else:
-        roof = {"bound": "hbm", "achieved": None, "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": None,
-                "traffic": None, "kernel": dom}
+    streaming = [k for k in kb if k in per_kind]
+    dom = max(streaming, key=lambda k: per_kind[k][0]) if streaming else None
+
+    def stream_roof(kind):
+        tot_ms, cnt = per_kind[kind]
+        achieved = kb[kind] * args.steps / (tot_ms * 1e-3) / 1e9
+        return {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                "traffic": measured_traffic(cfg["name"] + ("_gaussian" if cfg.get("probe") == "gaussian" else ""), kind),
+                "kernel": kind, "bytes_per_launch": int(kb[kind] / (cnt / args.steps)),
+                "avg_launch_us": round(tot_ms / cnt * 1e3, 2), "launches_per_step": cnt / args.steps}
+
+    roof = stream_roof(dom) if dom else {"bound": "hbm", "achieved": None, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                                         "frac": None, "traffic": None, "kernel": None}
     norm_bytes = workloads.algorithmic_norm_bytes(cfg)
-    norm_ms = sum(per_kind.get(k, (0.0, 0))[0] for k in ("project", "token_reduce", "qr", "hutchpp_final",
-                                                          "project_f32", "token_reduce_f32", "sample_sq",
-                                                          "probe_bits", "token_splits", "sample_sum", "qr_combine", "qr_expand",
-                                                          "hutchpp_sum", "probe_gauss")) / args.steps
     kernels = {k: {"launches_per_step": v[1] / args.steps, "avg_launch_us": round(v[0] / v[1] * 1e3, 2),
                    "us_per_step": round(v[0] / args.steps * 1e3, 2)} for k, v in sorted(per_kind.items())}
-    extra = {"norm_kernels_us_per_step": round(norm_ms * 1e3, 2),
-             "norm_hbm_gbps_kernels": round(norm_bytes / (norm_ms * 1e-3) / 1e9, 1) if norm_ms else None,
-             "step_hbm_gbps": round(norm_bytes / (ms_per_step * 1e-3) / 1e9, 1),
-             "step_hbm_frac": round(norm_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+    norm_kernel_ms = sum(per_kind.get(k, (0.0, 0))[0] for k in NORM_KINDS) / args.steps
+    extra = {"norm_stage": {"ms": round(norm_ms, 4), "algorithmic_bytes": norm_bytes,
+                            "GB/s": round(norm_bytes / (norm_ms * 1e-3) / 1e9, 1),
+                            "frac_of_hbm_peak": round(norm_bytes / (norm_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+                            "kernel_ms_summed": round(norm_kernel_ms, 4)},
+             "whole_step": {"ms": round(ms_per_step, 4), "tokens_per_s": round(B * T / (ms_per_step * 1e-3), 1),
+                            "parts": step_parts(cfg)},
+             "streaming_kernels": {k: stream_roof(k) for k in streaming},
              "kernels": kernels, "input_copies_rotated": copies,
-             "hot_cache_tokens_per_s": round(B * T / (hot_ms * 1e-3), 1) if hot_ms else None}
+             "hot_cache_norm_tokens_per_s": round(B * T / (hot_norm_ms * 1e-3), 1) if hot_norm_ms else None}
+    acc = accumulate_roofline(cfg, per_kind, args.steps)
+    if acc is not None:
+        acc["traffic"] = measured_traffic(cfg["name"], "accumulate")
+        extra["accumulate"] = acc
     if not args.no_extra:
-        extra["accumulate"] = accumulate_extra(D, torch, workloads, hip, max(5, args.steps // 5))
+        if cfg["accumulate"] and cfg["dtype"] == "bf16":
+            A, E, _ = max(pairs0, key=lambda t: t[0].shape[2] * t[1].shape[2] if t[1].shape[2] <= 8192 else 0)
+            extra["accumulate"]["vendor_gemm_tflops_context"] = {
+                "layer": f"{A.shape[2]}x{E.shape[2]}", "tflops": vendor_gemm(torch, A, E, 5)}
         if len(cfg["layers"]) == 1 and copies > 1:
             extra["vendor_read_same_operand"] = read_reference(torch, sets, copies, args.steps)
     rec = {"metric": "per-sample norm-estimation tokens/s + HBM GB/s (% peak), Llama-3.2-1B shapes",
-           "value": round(B * T / (ms_per_step * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1,
+           "value": round(B * T / (norm_ms * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1,
            "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5),
            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": cfg["dtype"],
            "data": "synthetic (seeded; Llama-3.2-1B layer shapes)",
            "config": workloads.describe(cfg) | {"C": cfg["C"], "steps_include": step_parts(cfg),
+                                                "value_is": "B*T / norm-stage wall time",
                                                 "launch": "hip_graph_replay" if args.graph else "eager"},
            "roofline": roof, "extra": extra}
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
-        rec["cpu_baseline"] = cpu_baseline(cfg, sets, args.cpu_seconds)
+        rec["cpu_baseline"] = cpu_baseline(cfg, pairs0, args.cpu_seconds)
     print(json.dumps(rec), flush=True)
+
+
+def step_norm_only(cfg, D, layers, n2, c, ws_n):
+    if cfg["estimator"] == "hutch":
+        probe = D.PROBE_GAUSSIAN if cfg.get("probe") == "gaussian" else D.PROBE_RADEMACHER
+        D.dprc_norm_hutch_clip(layers, cfg["k"], 0, cfg["C"], n2=n2, c=c, ws=ws_n, probe=probe)
+    else:
+        D.dprc_norm_hutchpp(layers, cfg["s"], cfg["r"], 0, n2=n2, ws=ws_n)
+        D.dprc_clip_scale(n2, cfg["C"], c=c)
+
+
+def step_rest_only(cfg, D, layers, c, grads, ws_acc):
+    if cfg["accumulate"]:
+        for (A, E, li), g in zip(layers, grads):
+            D.dprc_clip_accumulate(A, E, c, grad=g, ws=ws_acc)
+            if cfg["noise_sigma"] is not None:
+                D.dprc_add_noise(g, cfg["noise_sigma"], cfg["C"], 0, li)
 
 
 LLAMA_STEP = dict(B=2, T=2048, k=16, C=1.0, sigma=0.8, lr=1e-4)

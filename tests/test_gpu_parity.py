@@ -358,6 +358,24 @@ def test_hutchpp_many_layers_grouped(D):
     assert np.all(_rel(n2.cpu().numpy(), sum(ref_l)) < NORM_RTOL)
 
 
+def test_hutchpp_grouped_wide_passes(D):
+    # three bf16 layers with s + r = 80 > 64 columns: the grouped passes take one launch pair
+    # per layer (wider than the batched kernels), all sharing the group's pass scratch
+    B, T, s, r = 2, 300, 16, 64
+    shapes = [(120, 260), (72, 500), (200, 136)]
+    pairs = []
+    for li, (d, p) in enumerate(shapes):
+        A, E = _draw(B, T, d, p, law="student_t", layer=40 + li)
+        pairs.append((A, E, li))
+    n2l = torch.zeros(len(pairs), B, device="cuda")
+    n2 = D.dprc_norm_hutchpp(pairs, s, r, 8, n2_layers=n2l)
+    ref_l = [est.hutchpp_layer(_np(A), _np(E), s, r, 8, li) for (A, E, li) in pairs]
+    got_l = n2l.cpu().numpy()
+    for li in range(len(pairs)):
+        assert np.all(_rel(got_l[li], ref_l[li]) < NORM_RTOL), li
+    assert np.all(_rel(n2.cpu().numpy(), sum(ref_l)) < NORM_RTOL)
+
+
 def test_hutchpp_without_sketch_equals_hutch(D):
     A, E = _draw(2, 300, 100, 180, layer=8)
     a = D.dprc_norm_hutchpp([(A, E, 4)], 0, 16, 5)
@@ -380,10 +398,12 @@ def test_clip_scale_edges(D):
     (3, 150, 200, 260, "bf16"),     # ragged tiles; per-sample scaling inside a tile
     (2, 2000, 96, 72, "bf16"),      # few tiles -> split over samples and tokens
     (2, 64, 64, 48, "f32"),         # the tiny workload
+    (2, 300, 500, 1000, "bf16"),    # 2 x 4 = 8 tiles: the XCD tile order (a multiple of 8 tiles), ragged
+    (1, 260, 2000, 700, "bf16"),    # 8 x 3 = 24 tiles with d > p (the other walking order), ragged
 ])
 def test_clip_accumulate_parity(D, B, T, d, p, dtype):
     A, E = _draw(B, T, d, p, dtype=dtype, layer=9)
-    cvals = [0.25, 0.0, 0.8][:B] if B == 3 else [0.37, 1.0]
+    cvals = [0.25, 0.0, 0.8] if B == 3 else [0.37, 1.0][:B]
     c = torch.tensor(cvals, dtype=torch.float32, device="cuda")
     g = D.dprc_clip_accumulate(A, E, c)
     ref = est.clip_accumulate(_np(A), _np(E), np.array(cvals, dtype=np.float32).astype(np.float64))
