@@ -58,7 +58,9 @@ typedef enum {
   DPRC_ERROR_INVALID_VALUE = 1,      /* null pointer, non-positive size, bad enum, ...   */
   DPRC_ERROR_NOT_SUPPORTED = 2,      /* alignment / stride / size outside supported range */
   DPRC_ERROR_WORKSPACE_TOO_SMALL = 3,
-  DPRC_ERROR_HIP = 4                 /* a HIP runtime call or launch failed              */
+  DPRC_ERROR_HIP = 4,                /* a HIP runtime call or launch failed              */
+  DPRC_ERROR_SCRATCH_LIMIT = 5       /* dprc_norm_hutch_clip_static: needs more scratch
+                                        than DPRC_STATIC_SCRATCH_BYTES                   */
 } dprc_status;
 
 typedef enum { DPRC_F32 = 0, DPRC_BF16 = 1 } dprc_dtype;
@@ -124,6 +126,27 @@ dprc_status dprc_norm_hutch_clip(const dprc_layer* layers, int32_t num_layers, i
                                  dprc_probe probe, uint64_t seed, dprc_side side, float C, float* n2,
                                  float* c, float* n2_layers, int32_t accumulate, void* ws,
                                  size_t ws_bytes, hipStream_t stream);
+
+/* The same call for callers that cannot allocate (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation): identical arguments and
+ * results (bit for bit) to dprc_norm_hutch_clip, without the workspace.  Its scratch
+ * is a static device array of DPRC_STATIC_SCRATCH_BYTES that the library's code
+ * object holds on every device it runs on until the process ends; the call allocates
+ * nothing and frees nothing.  A call whose dprc_norm_hutch_workspace() exceeds that
+ * size returns DPRC_ERROR_SCRATCH_LIMIT and enqueues nothing (the 113-layer
+ * Llama-3.2-1B stack at B = 8, T = 4096, k = 32 needs 68 MiB).  `stream` must belong
+ * to the current device (else DPRC_ERROR_INVALID_VALUE); the first call on a device
+ * looks up that device's copy of the array (hipGetSymbolAddress) and keeps its
+ * address for the process, so make that first call outside graph capture.  Every
+ * call on one device shares the array: calls that overlap on one device (different
+ * streams, or host threads without ordering between their streams) race on it and
+ * must be serialised by the caller.  Nothing in it needs to start cleared; it keeps
+ * the last call's contents. */
+#define DPRC_STATIC_SCRATCH_BYTES (128u << 20)
+dprc_status dprc_norm_hutch_clip_static(const dprc_layer* layers, int32_t num_layers, int32_t k,
+                                        dprc_probe probe, uint64_t seed, dprc_side side, float C,
+                                        float* n2, float* c, float* n2_layers, int32_t accumulate,
+                                        hipStream_t stream);
 
 /* ---- Hutch++ (Algorithm 2, Hutch++ branch; estimator section) --------------
  * With M_i = X'_i^T X_i (m probed columns): sketch O S = M_i^T (M_i S) with s

@@ -10,6 +10,7 @@ instructions are disabled for the device code.
 import argparse
 import concurrent.futures as cf
 import os
+import re
 import subprocess
 import sys
 
@@ -41,14 +42,24 @@ def _compile(src, opt):
     return src, obj, r.returncode, msgs
 
 
+def _local_includes(path, seen):
+    """`path` and the repository headers it includes (quoted #include lines), transitively."""
+    if path in seen or not os.path.exists(path):
+        return seen
+    seen.add(path)
+    for line in open(path):
+        m = re.match(r'\s*#\s*include\s+"([^"]+)"', line)
+        if m:
+            _local_includes(os.path.normpath(os.path.join(os.path.dirname(path), m.group(1))), seen)
+    return seen
+
+
 def _stale(src):
-    """True when the object of `src` is missing or older than the source or a shared header."""
+    """True when the object of `src` is missing or older than the source or a header it includes."""
     obj = os.path.join(BUILD, os.path.basename(src)[:-4] + ".o")
     if not os.path.exists(obj):
         return True
-    deps = [src, os.path.join(ROOT, "include", "dprc.h")] + \
-        [os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".hpp")]
-    return any(os.path.getmtime(d) > os.path.getmtime(obj) for d in deps)
+    return any(os.path.getmtime(d) > os.path.getmtime(obj) for d in _local_includes(src, set()))
 
 
 def build(jobs=None, debug=False, verbose=False, incremental=False):

@@ -4,6 +4,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <vector>
 
 #include "../../include/dprc.h"
@@ -792,6 +793,36 @@ void gauss_legendre(int n, double* x, double* w) {
   }
 }
 
+// Scratch of dprc_norm_hutch_clip_static: one array on every device the library runs
+// on, held until the process ends.  In host code the name `scratch` is a host-side
+// stand-in, not a device address: the address comes from hipGetSymbolAddress, taken
+// once per device (with that device current) on the entry point's first call there,
+// and only that pointer reaches kernels.  Nothing in it has to start at zero: every
+// kernel of the Hutchinson path writes the scratch it later reads, as it does with a
+// caller's uninitialised workspace.
+static __device__ __align__(256) uint8_t scratch[DPRC_STATIC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+dprc_status static_scratch(hipStream_t stream, void** out) {
+  int cur = -1;
+  hipDevice_t sdev = -1;
+  if (hipGetDevice(&cur) != hipSuccess || hipStreamGetDevice(stream, &sdev) != hipSuccess) return DPRC_ERROR_HIP;
+  if (sdev != cur) return DPRC_ERROR_INVALID_VALUE;            // the stream's device must be current
+  if (cur < 0 || cur >= kMaxDevices) return DPRC_ERROR_NOT_SUPPORTED;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[cur]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return DPRC_ERROR_HIP;
+    if (!aligned(p, kAlign)) return DPRC_ERROR_HIP;
+    g_scratch_ptr[cur] = p;
+  }
+  *out = g_scratch_ptr[cur];
+  return DPRC_SUCCESS;
+}
+
 }  // namespace
 
 namespace dprc {
@@ -807,6 +838,9 @@ const char* dprc_status_string(dprc_status s) {
     case DPRC_ERROR_NOT_SUPPORTED: return "DPRC_ERROR_NOT_SUPPORTED: unsupported alignment, stride or size";
     case DPRC_ERROR_WORKSPACE_TOO_SMALL: return "DPRC_ERROR_WORKSPACE_TOO_SMALL: workspace smaller than the query";
     case DPRC_ERROR_HIP: return "DPRC_ERROR_HIP: a HIP runtime call or kernel launch failed";
+    case DPRC_ERROR_SCRATCH_LIMIT:
+      return "DPRC_ERROR_SCRATCH_LIMIT: the call needs more scratch than the library's static buffer "
+             "(DPRC_STATIC_SCRATCH_BYTES per device)";
   }
   return "unknown dprc_status";
 }
@@ -1007,6 +1041,20 @@ dprc_status dprc_norm_hutch_clip(const dprc_layer* layers, int32_t num_layers, i
                                  int32_t accumulate, void* ws, size_t ws_bytes, hipStream_t stream) {
   if (!c || !(C > 0.f) || std::isinf(C)) return DPRC_ERROR_INVALID_VALUE;
   return norm_hutch(layers, num_layers, k, probe, seed, side, n2, n2_layers, accumulate, ws, ws_bytes, stream, C, c);
+}
+
+dprc_status dprc_norm_hutch_clip_static(const dprc_layer* layers, int32_t num_layers, int32_t k, dprc_probe probe,
+                                        uint64_t seed, dprc_side side, float C, float* n2, float* c,
+                                        float* n2_layers, int32_t accumulate, hipStream_t stream) {
+  if (!c || !(C > 0.f) || std::isinf(C)) return DPRC_ERROR_INVALID_VALUE;
+  dprc_status s = check_layers(layers, num_layers, side);
+  if (s != DPRC_SUCCESS) return s;
+  const size_t need = dprc_norm_hutch_workspace(layers, num_layers, k, probe, side);
+  if (need > (size_t)DPRC_STATIC_SCRATCH_BYTES) return DPRC_ERROR_SCRATCH_LIMIT;
+  void* ws = nullptr;
+  if ((s = static_scratch(stream, &ws)) != DPRC_SUCCESS) return s;
+  return norm_hutch(layers, num_layers, k, probe, seed, side, n2, n2_layers, accumulate, ws,
+                    (size_t)DPRC_STATIC_SCRATCH_BYTES, stream, C, c);
 }
 
 // Calls with several bf16 layers and a sketch run them in groups of up to kQrMaxJobs:

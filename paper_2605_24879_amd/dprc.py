@@ -22,7 +22,7 @@ SIDE_OUT, SIDE_IN, SIDE_AUTO = 0, 1, 2
 PROBE_RADEMACHER, PROBE_HADAMARD, PROBE_GAUSSIAN = 0, 1, 2
 STREAM_PROBE, STREAM_SKETCH, STREAM_NOISE = 0, 1, 2
 
-EXPORTS = ["dprc_norm_hutch_workspace", "dprc_norm_hutch", "dprc_norm_hutch_clip", "dprc_norm_hutchpp_workspace",
+EXPORTS = ["dprc_norm_hutch_workspace", "dprc_norm_hutch", "dprc_norm_hutch_clip", "dprc_norm_hutch_clip_static", "dprc_norm_hutchpp_workspace",
            "dprc_norm_hutchpp", "dprc_clip_scale", "dprc_clip_accumulate_workspace",
            "dprc_clip_accumulate", "dprc_add_noise", "dprc_probe_bits", "dprc_probe_gaussian", "dprc_private_adamw", "dprc_envelope_middle_workspace",
            "dprc_envelope_middle", "dprc_chi2_cdf", "dprc_status_string",
@@ -61,6 +61,8 @@ def lib():
             "dprc_norm_hutch": (ctypes.c_int, [LP, I32, I32, ctypes.c_int, U64, ctypes.c_int, P, P, I32, P, SZ, P]),
             "dprc_norm_hutch_clip": (ctypes.c_int, [LP, I32, I32, ctypes.c_int, U64, ctypes.c_int, F, P, P, P, I32, P, SZ,
                                                     P]),
+            "dprc_norm_hutch_clip_static": (ctypes.c_int, [LP, I32, I32, ctypes.c_int, U64, ctypes.c_int, F, P, P, P,
+                                                           I32, P]),
             "dprc_norm_hutchpp_workspace": (SZ, [LP, I32, I32, I32, ctypes.c_int]),
             "dprc_norm_hutchpp": (ctypes.c_int, [LP, I32, I32, I32, U64, ctypes.c_int, P, P, I32, P, SZ, P]),
             "dprc_clip_scale": (ctypes.c_int, [P, I64, F, P, P]),
@@ -173,6 +175,22 @@ def dprc_norm_hutch_clip(pairs, k, seed, C, side=SIDE_OUT, probe=PROBE_RADEMACHE
 def dprc_norm_hutchpp_workspace(pairs, s, r, side=SIDE_OUT):
     arr, nl, _, _ = _layers(pairs)
     return lib().dprc_norm_hutchpp_workspace(arr, nl, s, r, side)
+
+
+def dprc_norm_hutch_clip_static(pairs, k, seed, C, side=SIDE_OUT, probe=PROBE_RADEMACHER, n2=None, c=None,
+                                n2_layers=None, accumulate=False):
+    """dprc_norm_hutch_clip on the library's static scratch (no workspace): returns (n2, c).
+    Outputs the caller does not pass are allocated here, by torch; pass them to allocate
+    nothing."""
+    arr, nl, B, dev = _layers(pairs)
+    if n2 is None:
+        n2 = torch.zeros(B, dtype=torch.float32, device=dev)
+    if c is None:
+        c = torch.empty(B, dtype=torch.float32, device=dev)
+    _check(lib().dprc_norm_hutch_clip_static(arr, nl, k, probe, seed, side, C, n2.data_ptr(), c.data_ptr(),
+                                             n2_layers.data_ptr() if n2_layers is not None else None,
+                                             int(bool(accumulate)), _stream(dev)))
+    return n2, c
 
 
 def dprc_norm_hutchpp(pairs, s, r, seed, side=SIDE_OUT, n2=None, n2_layers=None, accumulate=False, ws=None):

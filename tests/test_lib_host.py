@@ -189,3 +189,21 @@ def test_batched_workspaces_grow_with_the_groups_they_hold():
     hpp = lambda n: L.dprc_norm_hutchpp_workspace(arr, n, 4, 8, 0)
     assert hpp(8) > hpp(4) > hpp(1) > 0
     assert hpp(16) == hpp(8)
+
+
+def test_static_scratch_entry_point_limits():
+    # dprc_norm_hutch_clip_static validates like dprc_norm_hutch_clip, and a call whose
+    # workspace query exceeds the static scratch is refused before anything is enqueued
+    L = dprc.lib()
+    small = (dprc.Layer * 1)(_fake_layer())
+
+    def call(arr, n=1, C=1.0, c=0x50000):
+        return L.dprc_norm_hutch_clip_static(arr, n, 4, 0, 0, 0, C, 0x40000, c, None, 0, None)
+    assert call(small, C=0.0) == 1
+    assert call(small, c=None) == 1
+    assert call(small, n=0) == 1
+    limit = 128 << 20
+    big = (dprc.Layer * 1)(_fake_layer(B=64, T=65536, d=4096, p=4096, lda=4096, lde=4096))
+    assert L.dprc_norm_hutch_workspace(big, 1, 256, 0, 0) > limit
+    assert L.dprc_norm_hutch_clip_static(big, 1, 256, 0, 0, 0, 1.0, 0x40000, 0x50000, None, 0, None) == 5
+    assert L.dprc_status_string(5).decode().startswith("DPRC_ERROR_SCRATCH_LIMIT")
