@@ -242,6 +242,49 @@ dprc_status dprc_envelope_middle(const double* x, int32_t nx, int32_t k, int32_t
 dprc_status dprc_chi2_cdf(const double* x, int64_t n, double dof, double scale, double* out,
                           hipStream_t stream);
 
+/* ---- privacy accountant (appendix: Algorithm accounting) ---------------------------
+ * The accountant for DP-SGD-RC runs Poisson-subsampled Gaussian steps whose
+ * effective scale a = 1/sqrt(Y) is averaged over the envelope law of Y, and
+ * composes their privacy-loss distributions (PLD).  All arrays are fp64, device.
+ *
+ * dprc_envelope_bins: the envelope law as bins.  F[0..n_bins] holds the envelope
+ * CDF at y_j = y_min + j (y_max - y_min) / n_bins; the CDF is made monotone by a
+ * running maximum and clipped to [0, 1], w[j] = its increment over bin j (clamped
+ * at zero) divided by the sum of the increments, ybar[j] = the bin's midpoint.  A
+ * CDF with no increase on the range gives NaN weights.  n_bins >= 1, y_max > y_min.
+ *
+ * dprc_pld_step: one step's PLD on the cell-centred grid t_j = (j - n_half + 1) h,
+ * j < 2 n_half - 1 (q, normalised with q_inf to total one), from the survival
+ * function S(t) = P(L > t) at the cuts (c - n_half + 1/2) h, c < 2 n_half:
+ *   S(t) = p betabar(t + s(t)) + (1 - p) alpha(t + s(t)),
+ *   s(t) = log(1/p - (1 - p)/p e^-t), for t > log(1 - p); S = 1 at and below it,
+ *   alpha(u) = sum_i w_i Phi(-u/mu_i - mu_i/2), betabar(u) = sum_i w_i Phi(-u/mu_i + mu_i/2),
+ *   mu_i = 1 / (sigma sqrt(ybar_i))   (n_bins = 0: one term, w = 1, mu = 1/sigma).
+ * q_j = S(cut j) - S(cut j + 1) clamped at zero; the mass below the first cut
+ * joins q_0 and S at the last cut is the atom q_inf[0] at +infinity.  sigma > 0,
+ * 0 < p <= 1, h > 0.  Workspace: dprc_pld_step_workspace(n_half) bytes (S).
+ *
+ * dprc_pld_fold: the composition of two PLDs on the same grid of L cells (L odd)
+ * with atoms *ainf and *binf, given r[0 .. 2L - 2], their linear convolution
+ * (r[j] sits at cell j - (L - 1)/2 of the result grid): negatives clipped; the
+ * L centred cells kept, the mass below them added to the lowest one; the atom
+ * becomes 1 - (1 - ainf)(1 - binf) plus the mass above them, rescaled with the
+ * cells so that the total stays one.  q [L] and q_inf [1] must not overlap r.
+ *
+ * dprc_pld_delta: delta[e] = sum over t_j >= eps[e] of q_j (1 - e^(eps[e] - t_j))
+ * + q_inf[0], clipped to [0, 1], t_j = (j - (L - 1)/2) h, for 1 <= n_eps <= 65535.
+ */
+dprc_status dprc_envelope_bins(const double* F, int32_t n_bins, double y_min, double y_max, double* ybar,
+                               double* w, hipStream_t stream);
+size_t dprc_pld_step_workspace(int64_t n_half);
+dprc_status dprc_pld_step(double sigma, double p, double h, int64_t n_half, const double* ybar,
+                          const double* w, int32_t n_bins, double* q, double* q_inf, void* ws,
+                          size_t ws_bytes, hipStream_t stream);
+dprc_status dprc_pld_fold(const double* r, int64_t L, const double* ainf, const double* binf, double* q,
+                          double* q_inf, hipStream_t stream);
+dprc_status dprc_pld_delta(const double* q, int64_t L, double h, const double* q_inf, const double* eps,
+                           int32_t n_eps, double* delta, hipStream_t stream);
+
 /* ---- probe bits (verification) -------------------------------------------------
  * out[j*ceil(m/32) + w] = packed probe word w of column j (k columns), bits of
  * rows >= m cleared.  probe selects the family; for HADAMARD, seed, layer_id
@@ -288,7 +331,8 @@ typedef enum {
   DPRC_KERNEL_PROBE_GAUSS = 19,       /* Gaussian probe columns                  */
   DPRC_KERNEL_ADAMW = 20,             /* private AdamW step                      */
   DPRC_KERNEL_ENVELOPE = 21,          /* MiddleRegionCDF candidates and reduction */
-  DPRC_KERNEL_CHI2_CDF = 22           /* chi-squared CDF values                  */
+  DPRC_KERNEL_CHI2_CDF = 22,          /* chi-squared CDF values                  */
+  DPRC_KERNEL_PLD = 23                /* accountant: bins, step PLD, fold, delta */
 } dprc_kernel_kind;
 dprc_status dprc_trace_launches(hipEvent_t* events, int32_t* kinds, int32_t capacity,
                                 int32_t* count);

@@ -9,16 +9,21 @@ Appendix "Additional details to Privacy Accounting":
 * ``x_plus`` -- Algorithm binary-search-xplus on [1, 2], deciding at each
   midpoint whether the uniform law dominates every two-level form there
   (single crossing puts x_+ at the first point where it does);
-* ``epsilon`` / ``noise_multiplier`` -- Algorithm accounting: the privacy-loss
-  distribution (PLD) of one Poisson-subsampled Gaussian step whose scale
-  a = 1/sqrt(Y) is averaged over the envelope, composed over the steps of
-  all epochs by FFT, and delta(eps) = E[(1 - e^(eps - L))_+] solved for eps.
-  Without an envelope this is plain DP-SGD accounting.
+* ``envelope_law`` -- the bins of Algorithm accounting (``dprc_envelope_bins``);
+* ``epsilon`` / ``noise_multiplier`` -- Algorithm accounting: one
+  Poisson-subsampled Gaussian step whose scale a = 1/sqrt(Y) is averaged over
+  the envelope (``dprc_pld_step``: survival function, then cell masses),
+  composed over the steps of all epochs by repeated squaring, each product a
+  linear convolution (an FFT product, rocFFT through torch.fft) that
+  ``dprc_pld_fold`` truncates back to the grid, and delta(eps) evaluated for a
+  batch of eps values per round (``dprc_pld_delta``) to narrow a bracket around
+  the target.  Without an envelope this is plain DP-SGD accounting.
 
 The PLD lives on the cell-centred grid t = m h, |t| < t_max; mass that
 composition pushes past t_max is kept as an atom at +infinity (it counts
 fully towards delta) and mass below -t_max is folded into the lowest cell.
-PLD arithmetic runs in fp64 torch on the envelope's device.
+Every arithmetic step runs in HIP kernels of libdprc except the FFTs; this
+module holds the control flow (searches, the squaring schedule).
 """
 
 import math
@@ -72,91 +77,65 @@ def envelope_cdf(x, k, d, xp=None, n_lambda=51):
 
 def envelope_law(k, d, y_max=None, n_bins=4000, n_lambda=51, device=None):
     """Bins of the envelope law of Y on [0, y_max]: representative points (bin midpoints) and
-    weights (CDF increments, negatives clipped, normalised)."""
+    weights (CDF increments, made monotone, clipped and normalised) from dprc_envelope_bins."""
     dev = _dev(device)
     if y_max is None:
         y_max = 1.0 + 12.0 * math.sqrt(2.0 / k)            # far into the single-coordinate tail
     ys = torch.linspace(0.0, y_max, n_bins + 1, dtype=torch.float64, device=dev)
-    F = torch.cummax(envelope_cdf(ys, k, d, n_lambda=n_lambda), dim=0).values.clamp(0.0, 1.0)
-    w = torch.clamp(F[1:] - F[:-1], min=0.0)
-    w = w / w.sum()
-    return 0.5 * (ys[1:] + ys[:-1]), w
-
-
-def _kernels(t, sigma, y, w):
-    """alpha(t), betabar(t) of one step averaged over a = 1/sqrt(y) with weights w
-    (a = 1 when y is None)."""
-    if y is None:
-        mu = torch.tensor([1.0 / sigma], dtype=torch.float64, device=t.device)
-        w = torch.ones(1, dtype=torch.float64, device=t.device)
-    else:
-        keep = w > 0
-        mu = (1.0 / torch.sqrt(y[keep])) / sigma
-        w = w[keep]
-    al = torch.zeros_like(t)
-    beb = torch.zeros_like(t)
-    chunk = max(1, (1 << 24) // max(1, t.numel()))
-    for s in range(0, mu.numel(), chunk):
-        m = mu[s:s + chunk, None]
-        ww = w[s:s + chunk, None]
-        al += (ww * torch.special.ndtr(-t[None, :] / m - m / 2.0)).sum(0)
-        beb += (ww * torch.special.ndtr(-(t[None, :] / m - m / 2.0))).sum(0)
-    return al, beb
+    F = envelope_cdf(ys, k, d, n_lambda=n_lambda).contiguous()
+    return D.dprc_envelope_bins(F, 0.0, y_max)
 
 
 def step_pld(sigma, p, h, t_max, y=None, w=None, device=None):
-    """(masses on the grid, mass at +infinity) of one subsampled step."""
+    """(masses on the grid, mass at +infinity [1]) of one subsampled step, on the device."""
     dev = _dev(device if y is None else y.device)
-    n = int(round(t_max / h))
-    half = (torch.arange(1, n + 1, dtype=torch.float64, device=dev) - 0.5) * h
-    cuts = torch.cat([-half.flip(0), half])
-    S = torch.ones_like(cuts)                              # survival P(L > t); 1 below the support
-    t_min = math.log1p(-p) if p < 1 else -math.inf
-    ok = cuts > t_min
-    tt = cuts[ok]
-    s = torch.log(1.0 / p - (1.0 - p) / p * torch.exp(-tt)) if p < 1 else torch.zeros_like(tt)
-    al, beb = _kernels(tt + s, sigma, y, w)
-    S[ok] = p * beb + (1.0 - p) * al
-    q = torch.clamp(S[:-1] - S[1:], min=0.0)
-    q[0] += torch.clamp(1.0 - S[0], min=0.0)
-    inf = float(torch.clamp(S[-1], min=0.0))
-    tot = float(q.sum()) + inf
-    return q / tot, inf / tot
+    return D.dprc_pld_step(sigma, p, h, int(round(t_max / h)), y, w, device=dev)
 
 
 def _compose2(a, ainf, b, binf):
+    """Composition of two PLDs on one grid: the FFT product gives their linear convolution,
+    dprc_pld_fold truncates it back to the grid and updates the atom."""
     L = a.numel()
-    n = 2 * L - 1
-    size = 1 << (n - 1).bit_length()
-    r = torch.fft.irfft(torch.fft.rfft(a, size) * torch.fft.rfft(b, size), size)[:n].clamp(min=0.0)
-    c = (L - 1) // 2
-    out = r[c:c + L].clone()
-    out[0] += r[:c].sum()
-    top = float(r[c + L:].sum())
-    inf = 1.0 - (1.0 - ainf) * (1.0 - binf)
-    fin = float(out.sum()) + top
-    if fin > 0:
-        out *= (1.0 - inf) / fin
-        inf += top * (1.0 - inf) / fin
-    return out, inf
+    size = 1 << (2 * L - 2).bit_length()
+    r = torch.fft.irfft(torch.fft.rfft(a, size) * torch.fft.rfft(b, size), size)
+    return D.dprc_pld_fold(r, L, ainf, binf)
 
 
 def compose(q, qinf, steps):
     """PLD of `steps` independent steps (repeated squaring)."""
-    res, rinf = None, 0.0
+    res, rinf = None, None
     base, binf = q, qinf
     while steps:
         if steps & 1:
-            res, rinf = (base.clone(), binf) if res is None else _compose2(res, rinf, base, binf)
+            res, rinf = (base.clone(), binf.clone()) if res is None else _compose2(res, rinf, base, binf)
         steps >>= 1
         if steps:
             base, binf = _compose2(base, binf, base, binf)
     return res, rinf
 
 
-def _delta(grid, q, qinf, eps):
-    m = grid >= eps
-    return min(1.0, max(0.0, float((q[m] * (1.0 - torch.exp(eps - grid[m]))).sum()) + qinf))
+EPS_POINTS = 64          # delta evaluations per round of the eps search
+EPS_TOL = 1e-10
+
+
+def _solve_eps(q, qinf, h, delta):
+    """eps with delta(eps) = delta: delta is continuous and non-increasing in eps, so each round
+    evaluates it at EPS_POINTS points across the bracket and keeps the cell where it crosses."""
+    L = q.numel()
+    t_top = (L - 1) // 2 * h
+    ends = D.dprc_pld_delta(q, h, qinf, torch.tensor([0.0, t_top], dtype=torch.float64, device=q.device)).tolist()
+    if ends[0] <= delta:
+        return 0.0
+    if ends[1] > delta:
+        return math.inf
+    lo, hi = 0.0, t_top
+    while hi - lo > EPS_TOL:
+        xs = torch.linspace(lo, hi, EPS_POINTS + 2, dtype=torch.float64, device=q.device)[1:-1].contiguous()
+        vals = D.dprc_pld_delta(q, h, qinf, xs).tolist()
+        xl = xs.tolist()
+        j = next((i for i, v in enumerate(vals) if v <= delta), EPS_POINTS)
+        lo, hi = (xl[j - 1] if j > 0 else lo), (xl[j] if j < EPS_POINTS else hi)
+    return 0.5 * (lo + hi)
 
 
 def epsilon(sigma, N, B, epochs, delta, h=1e-3, t_max=20.0, envelope=None, device=None):
@@ -168,24 +147,7 @@ def epsilon(sigma, N, B, epochs, delta, h=1e-3, t_max=20.0, envelope=None, devic
     q, qi = step_pld(sigma, p, h, t_max, y, w, dev)
     q, qi = compose(q, qi, T)
     q, qi = compose(q, qi, epochs)
-    n = (q.numel() + 1) // 2
-    grid = torch.arange(-(n - 1), n, dtype=torch.float64, device=dev) * h
-    f = lambda e: _delta(grid, q, qi, e) - delta
-    if f(0.0) <= 0:
-        return 0.0
-    hi = float(grid[-1])
-    if f(hi) > 0:
-        return math.inf
-    lo = 0.0
-    for _ in range(200):                                   # bisection to 1e-10
-        mid = 0.5 * (lo + hi)
-        if f(mid) > 0:
-            lo = mid
-        else:
-            hi = mid
-        if hi - lo < 1e-10:
-            break
-    return 0.5 * (lo + hi)
+    return _solve_eps(q, qi, h, delta)
 
 
 def noise_multiplier(eps, N, B, epochs, delta, envelope=None, lo=0.3, hi=50.0, tol=1e-3, **kw):

@@ -1307,6 +1307,55 @@ dprc_status dprc_chi2_cdf(const double* x, int64_t n, double dof, double scale, 
   return hip_status(traced(DPRC_KERNEL_CHI2_CDF, stream, [&] { return launch_chi2_cdf(x, n, dof, scale, out, stream); }));
 }
 
+dprc_status dprc_envelope_bins(const double* F, int32_t n_bins, double y_min, double y_max, double* ybar, double* w,
+                               hipStream_t stream) {
+  if (!F || !ybar || !w || n_bins < 1 || !std::isfinite(y_min) || !std::isfinite(y_max) || !(y_max > y_min))
+    return DPRC_ERROR_INVALID_VALUE;
+  if (!aligned(F, 8) || !aligned(ybar, 8) || !aligned(w, 8)) return DPRC_ERROR_INVALID_VALUE;
+  return hip_status(traced(DPRC_KERNEL_PLD, stream, [&] {
+    return launch_envelope_bins(F, n_bins, y_min, y_max, ybar, w, stream); }));
+}
+
+size_t dprc_pld_step_workspace(int64_t n_half) {
+  if (n_half < 1 || n_half > (1LL << 30)) return 0;
+  return (size_t)round_up(2 * n_half * (int64_t)sizeof(double), kAlign);
+}
+
+dprc_status dprc_pld_step(double sigma, double p, double h, int64_t n_half, const double* ybar, const double* w,
+                          int32_t n_bins, double* q, double* q_inf, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!(sigma > 0.0) || !std::isfinite(sigma) || !(p > 0.0 && p <= 1.0) || !(h > 0.0) || !std::isfinite(h) ||
+      n_half < 1 || n_half > (1LL << 30) || n_bins < 0 || !q || !q_inf)
+    return DPRC_ERROR_INVALID_VALUE;
+  if (n_bins > 0 && (!ybar || !w || !aligned(ybar, 8) || !aligned(w, 8))) return DPRC_ERROR_INVALID_VALUE;
+  const size_t need = dprc_pld_step_workspace(n_half);
+  if (ws_bytes < need) return DPRC_ERROR_WORKSPACE_TOO_SMALL;
+  if (!ws || !aligned(ws, kAlign) || !aligned(q, 8) || !aligned(q_inf, 8)) return DPRC_ERROR_INVALID_VALUE;
+  PldArgs a;
+  a.sigma = sigma; a.p = p; a.h = h;
+  a.t_min = p < 1.0 ? std::log1p(-p) : -INFINITY;
+  a.n = n_half; a.ybar = n_bins > 0 ? ybar : nullptr; a.w = n_bins > 0 ? w : nullptr; a.n_bins = n_bins;
+  a.S = static_cast<double*>(ws); a.q = q; a.q_inf = q_inf;
+  return hip_status(traced(DPRC_KERNEL_PLD, stream, [&] { return launch_pld_step(a, stream); }));
+}
+
+dprc_status dprc_pld_fold(const double* r, int64_t L, const double* ainf, const double* binf, double* q,
+                          double* q_inf, hipStream_t stream) {
+  if (!r || !ainf || !binf || !q || !q_inf || L < 1 || L % 2 == 0 || L > (1LL << 30)) return DPRC_ERROR_INVALID_VALUE;
+  if (!aligned(r, 8) || !aligned(ainf, 8) || !aligned(binf, 8) || !aligned(q, 8) || !aligned(q_inf, 8))
+    return DPRC_ERROR_INVALID_VALUE;
+  return hip_status(traced(DPRC_KERNEL_PLD, stream, [&] { return launch_pld_fold(r, L, ainf, binf, q, q_inf, stream); }));
+}
+
+dprc_status dprc_pld_delta(const double* q, int64_t L, double h, const double* q_inf, const double* eps, int32_t n_eps,
+                           double* delta, hipStream_t stream) {
+  if (!q || !q_inf || !eps || !delta || L < 1 || L % 2 == 0 || !(h > 0.0) || !std::isfinite(h) || n_eps < 1 ||
+      n_eps > 65535)
+    return DPRC_ERROR_INVALID_VALUE;
+  if (!aligned(q, 8) || !aligned(q_inf, 8) || !aligned(eps, 8) || !aligned(delta, 8)) return DPRC_ERROR_INVALID_VALUE;
+  return hip_status(traced(DPRC_KERNEL_PLD, stream, [&] {
+    return launch_pld_delta(q, L, h, q_inf, eps, n_eps, delta, stream); }));
+}
+
 dprc_status dprc_probe_gaussian(uint64_t seed, uint32_t layer_id, int64_t m, int32_t k, float* out,
                                 hipStream_t stream) {
   if (!out || m < 1 || k < 1 || k > 256 || m > (1LL << 36)) return DPRC_ERROR_INVALID_VALUE;

@@ -249,6 +249,26 @@ int env_blocks(int64_t ncand);
 hipError_t launch_env_middle(const EnvArgs& a, hipStream_t st);
 hipError_t launch_chi2_cdf(const double* x, int64_t n, double dof, double scale, double* out, hipStream_t st);
 
+// Privacy accounting (see dprc_pld_step and the others): one subsampled step's
+// survival function at 2n cut points into S, then its 2n - 1 cell masses and atom.
+struct PldArgs {
+  double sigma, p, h, t_min;   // t_min = log(1 - p) (-inf for p = 1)
+  int64_t n;                   // cut points per side
+  const double* ybar;          // envelope bins (null with n_bins = 0: a = 1)
+  const double* w;
+  int32_t n_bins;
+  double* S;                   // [2n] scratch
+  double* q;                   // [2n - 1]
+  double* q_inf;               // [1]
+};
+hipError_t launch_envelope_bins(const double* F, int32_t M, double y_min, double y_max, double* ybar, double* w,
+                                hipStream_t st);
+hipError_t launch_pld_step(const PldArgs& a, hipStream_t st);
+hipError_t launch_pld_fold(const double* r, int64_t L, const double* ainf, const double* binf, double* q,
+                           double* q_inf, hipStream_t st);
+hipError_t launch_pld_delta(const double* q, int64_t L, double h, const double* q_inf, const double* eps,
+                            int32_t n_eps, double* delta, hipStream_t st);
+
 // One private AdamW step on a [d, p] fp32 master (see dprc_private_adamw).
 struct AdamArgs {
   float* theta;

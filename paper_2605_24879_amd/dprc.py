@@ -25,7 +25,8 @@ STREAM_PROBE, STREAM_SKETCH, STREAM_NOISE = 0, 1, 2
 EXPORTS = ["dprc_norm_hutch_workspace", "dprc_norm_hutch", "dprc_norm_hutch_clip", "dprc_norm_hutch_clip_static", "dprc_norm_hutchpp_workspace",
            "dprc_norm_hutchpp", "dprc_clip_scale", "dprc_clip_accumulate_workspace",
            "dprc_clip_accumulate", "dprc_add_noise", "dprc_probe_bits", "dprc_probe_gaussian", "dprc_private_adamw", "dprc_envelope_middle_workspace",
-           "dprc_envelope_middle", "dprc_chi2_cdf", "dprc_status_string",
+           "dprc_envelope_middle", "dprc_chi2_cdf", "dprc_envelope_bins", "dprc_pld_step_workspace",
+           "dprc_pld_step", "dprc_pld_fold", "dprc_pld_delta", "dprc_status_string",
            "dprc_version", "dprc_trace_launches"]
 
 
@@ -74,6 +75,12 @@ def lib():
             "dprc_envelope_middle_workspace": (SZ, [I32, I32, I32]),
             "dprc_envelope_middle": (ctypes.c_int, [P, I32, I32, I32, I32, P, P, P, SZ, P]),
             "dprc_chi2_cdf": (ctypes.c_int, [P, I64, ctypes.c_double, ctypes.c_double, P, P]),
+            "dprc_envelope_bins": (ctypes.c_int, [P, I32, ctypes.c_double, ctypes.c_double, P, P, P]),
+            "dprc_pld_step_workspace": (SZ, [I64]),
+            "dprc_pld_step": (ctypes.c_int, [ctypes.c_double, ctypes.c_double, ctypes.c_double, I64, P, P, I32, P, P,
+                                             P, SZ, P]),
+            "dprc_pld_fold": (ctypes.c_int, [P, I64, P, P, P, P, P]),
+            "dprc_pld_delta": (ctypes.c_int, [P, I64, ctypes.c_double, P, P, I32, P, P]),
             "dprc_private_adamw": (ctypes.c_int, [P, P, P, I64, P, I64, I64, I64, F, F, U64, U32, F,
                                                   ctypes.POINTER(AdamWParams), P, I64, P]),
             "dprc_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -292,6 +299,63 @@ def dprc_probe_bits(probe, seed, layer_id, stream_id, m, k, device="cuda", out=N
     return out
 
 
+def _f64_dev(x, name):
+    if not (x.is_cuda and x.dtype == torch.float64 and x.is_contiguous()):
+        raise ValueError(f"{name} must be a contiguous fp64 GPU tensor")
+    return x
+
+
+def dprc_envelope_bins(F, y_min, y_max):
+    """Envelope-law bins from the CDF at n_bins + 1 even grid points: returns (ybar, w) [n_bins]."""
+    _f64_dev(F, "F")
+    n = F.numel() - 1
+    ybar = torch.empty(n, dtype=torch.float64, device=F.device)
+    w = torch.empty(n, dtype=torch.float64, device=F.device)
+    _check(lib().dprc_envelope_bins(F.data_ptr(), n, float(y_min), float(y_max), ybar.data_ptr(), w.data_ptr(),
+                                    _stream(F.device)))
+    return ybar, w
+
+
+def dprc_pld_step(sigma, p, h, n_half, ybar=None, w=None, device=None):
+    """One subsampled step's PLD: returns (q [2 n_half - 1], q_inf [1]) as fp64 GPU tensors."""
+    dev = ybar.device if ybar is not None else torch.device(device if device is not None else "cuda")
+    if ybar is not None:
+        _f64_dev(ybar, "ybar")
+        _f64_dev(w, "w")
+    q = torch.empty(2 * n_half - 1, dtype=torch.float64, device=dev)
+    q_inf = torch.empty(1, dtype=torch.float64, device=dev)
+    need = lib().dprc_pld_step_workspace(n_half)
+    ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    _check(lib().dprc_pld_step(float(sigma), float(p), float(h), n_half,
+                               ybar.data_ptr() if ybar is not None else None,
+                               w.data_ptr() if w is not None else None, ybar.numel() if ybar is not None else 0,
+                               q.data_ptr(), q_inf.data_ptr(), ws.data_ptr(), need, _stream(dev)))
+    return q, q_inf
+
+
+def dprc_pld_fold(r, L, ainf, binf):
+    """Kept cells and atom of the composition whose linear convolution is r[:2L-1]."""
+    for x, nm in ((r, "r"), (ainf, "ainf"), (binf, "binf")):
+        _f64_dev(x, nm)
+    if r.numel() < 2 * L - 1:
+        raise ValueError("r must hold the 2L - 1 values of the linear convolution")
+    q = torch.empty(L, dtype=torch.float64, device=r.device)
+    q_inf = torch.empty(1, dtype=torch.float64, device=r.device)
+    _check(lib().dprc_pld_fold(r.data_ptr(), L, ainf.data_ptr(), binf.data_ptr(), q.data_ptr(), q_inf.data_ptr(),
+                               _stream(r.device)))
+    return q, q_inf
+
+
+def dprc_pld_delta(q, h, q_inf, eps):
+    """delta(eps) for a batch of eps values (fp64 GPU tensor): returns delta [len(eps)]."""
+    for x, nm in ((q, "q"), (q_inf, "q_inf"), (eps, "eps")):
+        _f64_dev(x, nm)
+    out = torch.empty(eps.numel(), dtype=torch.float64, device=q.device)
+    _check(lib().dprc_pld_delta(q.data_ptr(), q.numel(), float(h), q_inf.data_ptr(), eps.data_ptr(), eps.numel(),
+                                out.data_ptr(), _stream(q.device)))
+    return out
+
+
 def dprc_probe_gaussian(seed, layer_id, m, k, device="cuda", out=None):
     """Gaussian probe values [k, m] (fp32): out[j, u] = probe entry (u, j)."""
     if out is None:
@@ -308,7 +372,7 @@ KERNEL_NAMES = {1: "project", 2: "token_reduce", 3: "qr", 4: "hutchpp_final", 5:
                 6: "accumulate", 7: "splitk_reduce", 8: "noise", 9: "probe_bits", 10: "project_f32",
                 11: "token_reduce_f32", 12: "sample_sq", 13: "accumulate_f32",
                 14: "token_splits", 15: "sample_sum", 16: "qr_combine", 17: "qr_expand", 18: "hutchpp_sum",
-                19: "probe_gauss", 20: "adamw", 21: "envelope", 22: "chi2_cdf"}
+                19: "probe_gauss", 20: "adamw", 21: "envelope", 22: "chi2_cdf", 23: "pld"}
 
 
 def dprc_trace_launches(events_ptr, kinds_ptr, capacity, count_ptr):

@@ -104,3 +104,57 @@ def test_noise_multiplier_brackets_the_target(mods):
     _, A = mods
     s = A.noise_multiplier(2.0, 1000, 50, 2, 1e-5, tol=1e-3)
     assert A.epsilon(s, 1000, 50, 2, 1e-5) <= 2.0 < A.epsilon(s - 2e-3, 1000, 50, 2, 1e-5)
+
+
+def test_envelope_bins_kernel_matches_oracle(mods):
+    # the binning kernel on a smooth CDF (chi^2(k)/k), a step CDF and a CDF with a dip
+    D, _ = mods
+    k, y_max = 32, 1.0 + 12.0 * math.sqrt(2.0 / 32)
+    for n in (7, 1000, 4000, 70000):
+        ys = np.linspace(0.0, y_max, n + 1)
+        F = np.array([ac.vertex_cdf(y, k) for y in ys])
+        ybar, w = D.dprc_envelope_bins(_t(F), 0.0, y_max)
+        yr, wr = ac.envelope_bins(lambda v: ac.vertex_cdf(v, k), 0.0, y_max, n)
+        assert np.allclose(ybar.cpu().numpy(), yr, rtol=0, atol=1e-13), n
+        assert np.max(np.abs(w.cpu().numpy() - wr)) < 1e-14, n
+    vals = np.array([0.0, 0.4, 0.39, 0.4, 1.0])
+    ybar, w = D.dprc_envelope_bins(_t(vals), 0.0, 4.0)
+    assert np.allclose(w.cpu().numpy(), [0.4, 0.0, 0.0, 0.6], atol=1e-15)
+    step = (np.linspace(0.0, 3.0, 301) >= 0.3141).astype(np.float64)
+    _, w = D.dprc_envelope_bins(_t(step), 0.0, 3.0)
+    w = w.cpu().numpy()
+    assert w[31] == 1.0 and np.count_nonzero(w) == 1
+
+
+@pytest.mark.parametrize("sigma,p,envelope", [(0.8, 0.25, False), (1.1, 0.05, True), (2.0, 1.0, False),
+                                              (0.9, 1.0, True)])
+def test_step_pld_kernel_matches_oracle(mods, sigma, p, envelope):
+    D, A = mods
+    h, t_max = 1e-3, 20.0
+    y = w = None
+    if envelope:
+        y, w = A.envelope_law(8, 4, n_bins=300, n_lambda=7)
+    q, qi = D.dprc_pld_step(sigma, p, h, int(round(t_max / h)), y, w)
+    grid, qr, qir = ac.single_step_pld(sigma, p, h, t_max, None if y is None else y.cpu().numpy(),
+                                       None if w is None else w.cpu().numpy())
+    got = q.cpu().numpy()
+    assert got.shape == qr.shape
+    assert np.max(np.abs(got - qr)) < 1e-13
+    assert abs(qi.item() - qir) < 1e-13
+    assert abs(got.sum() + qi.item() - 1.0) < 1e-12
+
+
+def test_pld_fold_and_delta_kernels_match_oracle(mods):
+    # one composition and delta(eps) at a batch of eps values against the oracle's numpy steps
+    D, A = mods
+    h, t_max = 1e-3, 8.0
+    q, qi = D.dprc_pld_step(0.7, 0.3, h, int(round(t_max / h)))
+    grid, qr, qir = ac.single_step_pld(0.7, 0.3, h, t_max)
+    q2, qi2 = A._compose2(q, qi, q, qi)
+    r2, ri2 = ac._conv_truncated(qr, qir, qr, qir)
+    assert np.max(np.abs(q2.cpu().numpy() - r2)) < 1e-12
+    assert abs(qi2.item() - ri2) < 1e-12
+    eps = np.array([0.0, 0.1, 0.5, 1.0, 2.5, 7.9995, 8.5])
+    got = D.dprc_pld_delta(q2, h, qi2, _t(eps)).cpu().numpy()
+    ref = np.array([ac.delta_of_eps(grid, r2, ri2, e) for e in eps])
+    assert np.max(np.abs(got - ref)) < 1e-12

@@ -207,3 +207,28 @@ def test_static_scratch_entry_point_limits():
     assert L.dprc_norm_hutch_workspace(big, 1, 256, 0, 0) > limit
     assert L.dprc_norm_hutch_clip_static(big, 1, 256, 0, 0, 0, 1.0, 0x40000, 0x50000, None, 0, None) == 5
     assert L.dprc_status_string(5).decode().startswith("DPRC_ERROR_SCRATCH_LIMIT")
+
+
+def test_accountant_entry_points_validation():
+    L = dprc.lib()
+    P = 0x10000
+    assert L.dprc_envelope_bins(P, 0, 0.0, 1.0, P, P, None) == 1          # no bins
+    assert L.dprc_envelope_bins(P, 4, 1.0, 1.0, P, P, None) == 1          # empty range
+    assert L.dprc_envelope_bins(None, 4, 0.0, 1.0, P, P, None) == 1
+    assert L.dprc_pld_step_workspace(0) == 0
+    need = L.dprc_pld_step_workspace(1000)
+    assert need >= 2000 * 8
+    args = lambda **kw: dict(dict(sigma=1.0, p=0.1, h=1e-3, n=1000, ybar=None, w=None, nb=0, ws_bytes=need), **kw)
+
+    def step(a):
+        return L.dprc_pld_step(a["sigma"], a["p"], a["h"], a["n"], a["ybar"], a["w"], a["nb"], P, P + 8192,
+                               0x40000, a["ws_bytes"], None)
+    assert step(args(sigma=0.0)) == 1
+    assert step(args(p=0.0)) == 1
+    assert step(args(p=1.5)) == 1
+    assert step(args(h=-1.0)) == 1
+    assert step(args(nb=3)) == 1                                             # bins without arrays
+    assert step(args(ws_bytes=need - 1)) == 3
+    assert L.dprc_pld_fold(P, 10, P, P, P, P, None) == 1                     # even L
+    assert L.dprc_pld_delta(P, 11, 1e-3, P, P, 0, P, None) == 1              # no eps
+    assert L.dprc_pld_delta(P, 11, 0.0, P, P, 3, P, None) == 1               # h = 0
