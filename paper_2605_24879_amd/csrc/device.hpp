@@ -126,6 +126,13 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, 
 __device__ __forceinline__ uint4 buffer_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
   return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
 }
+// The same load marked non-temporal (cache policy NT): for operands streamed once, whose
+// lines need not stay in the caches.  A read-only probe over the stack workload's 54.7 GB
+// streamed 6.6 to 6.7 TB/s with it against 5.9 to 6.2 TB/s without.
+constexpr int kCachePolicyNT = 2;
+__device__ __forceinline__ uint4 buffer_load16_nt(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, kCachePolicyNT));
+}
 
 // The 8 bf16 values +-1 of one byte of probe signs (bit set -> -1) as a 16x16x32
 // B operand fragment.  `P` holds the byte in bits 0..7 of both 16-bit halves

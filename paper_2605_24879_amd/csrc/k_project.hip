@@ -116,7 +116,7 @@ __device__ __forceinline__ void project_body(const ProjectArgs& a, int bx, int b
       const int col = c0 + 8 * lpiece[j];
       if constexpr (FAST) {
         const bool ok = col < col_end;
-        dst[j] = buffer_load16(xr, ok ? roff[j] + 2u * (uint32_t)col : kOobOffset);
+        dst[j] = buffer_load16_nt(xr, ok ? roff[j] + 2u * (uint32_t)col : kOobOffset);
       } else {
         dst[j] = load8_elem(rowp[j], col, col_end, t0 + 4 * j + lrow < a.T);
       }

@@ -126,7 +126,7 @@ __device__ __forceinline__ void tokred_body(const TokredArgs& a, int bx, int by)
       const __amdgpu_buffer_rsrc_t xr =
           buffer_rsrc(xs + (int64_t)(rows > 0 ? t0 : 0) * a.ldx + j0, (uint32_t)rows * row_bytes);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) dst.x[q] = buffer_load16(xr, lane_off + (uint32_t)(16 * q) * row_bytes);
+      for (int q = 0; q < 4; ++q) dst.x[q] = buffer_load16_nt(xr, lane_off + (uint32_t)(16 * q) * row_bytes);
     } else {
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
