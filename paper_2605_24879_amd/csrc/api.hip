@@ -115,10 +115,11 @@ int rows_per_wg(int64_t rows, int ncols_pad, bool dense = false) {
 }
 
 int words_per_chunk(int64_t m, int nz) {
-  // whole 512-column stages of the projection kernel per chunk
+  // whole 512-column stages of the projection kernel per chunk; at most 4096 probe words
+  // (16 KB of LDS), so that three 32-row workgroups fit in a CU's 160 KB even at k = 32
   const int64_t all = round_up(ceil_div(m, 32), 16);
   if (nz <= 0) return (int)all;
-  return (int)std::min<int64_t>(all, std::max(16, (8192 / nz) & ~15));
+  return (int)std::min<int64_t>(all, std::max(16, (4096 / nz) & ~15));
 }
 
 // Token-reduction geometry for one (operand width n, columns) pass.
@@ -869,6 +870,25 @@ bool hutch_batched(const dprc_layer* layers, int32_t n) {
   return true;
 }
 
+// A batch whose token reductions have at least kUnsplitPairs (sample, tile) pairs fills the
+// GPU without token splits: every job then runs unsplit (one workgroup per pair over all
+// tokens, writing its tile sum directly), which halves the per-workgroup start and finish
+// costs of two-way splits and drops the split-sum launch.  The split partials the layout
+// reserved stay unused.
+constexpr int64_t kUnsplitPairs = 1024;
+void unsplit_large_batch(TokredBatch& bt) {
+  int64_t pairs = 0;
+  for (int q = 0; q < bt.njobs; ++q) pairs += (int64_t)bt.job[q].B * bt.job[q].ntiles;
+  if (pairs < kUnsplitPairs) return;
+  for (int q = 0; q < bt.njobs; ++q) {
+    TokredArgs& a = bt.job[q];
+    if (a.mode != 0) continue;
+    a.stages_per_split = a.S * a.stages_per_split;
+    a.S = 1;
+    a.part = nullptr;
+  }
+}
+
 // The collected projections (widest first, up to kProjMaxJobs per launch) and token
 // reductions (one launch per column count) of a batch of activation groups; work over
 // more than 64 columns takes one launch per layer or group.
@@ -1008,6 +1028,7 @@ static dprc_status norm_hutch(const dprc_layer* layers, int32_t num_layers, int3
         bt.job[bt.njobs++] = ta;
         l = le;
       }
+      if (batched) unsplit_large_batch(bt);       // (unbatched groups launched theirs already)
       if (batched && (s = hutch_launch_batched(pj, npj, bt, stream)) != DPRC_SUCCESS) return s;
       if ((s = run_splits_batch(bt.job, bt.njobs, stream)) != DPRC_SUCCESS) return s;
       const bool last = l == num_layers;

@@ -209,6 +209,29 @@ def test_hutch_many_groups_batched(D, k, probe):
         assert torch.equal(n2l, solo)
 
 
+@pytest.mark.parametrize("k", [32, 20])
+def test_hutch_large_batch_unsplit(D, k):
+    # a batch of eight layers with 1024 (sample, 128-column tile) pairs: its token reductions
+    # run without token splits (one workgroup per pair over all 200 tokens, a ragged last
+    # stage), the layers ragged in both widths; a second call of one layer runs split
+    B, T = 4, 200
+    shapes = [(4000, 300), (4096, 130), (4000, 520), (4096, 96), (4000, 72), (4096, 260), (4000, 1000), (4096, 40)]
+    pairs = []
+    for j, (d, p) in enumerate(shapes):
+        A, E = _draw(B, T, d, p, layer=200 + j)
+        pairs.append((A, E, j))
+    n2l = torch.zeros(len(pairs), B, device="cuda")
+    n2 = D.dprc_norm_hutch(pairs, k, 11, n2_layers=n2l)
+    refs = [est.hutch_layer(_np(A), _np(E), k, 11, j) for (A, E, j) in pairs]
+    got = n2l.cpu().numpy()
+    for j in range(len(pairs)):
+        assert np.all(_rel(got[j], refs[j]) < NORM_RTOL), j
+    assert np.all(_rel(n2.cpu().numpy(), np.sum(refs, axis=0)) < NORM_RTOL)
+    A, E, j = pairs[0]
+    solo = D.dprc_norm_hutch([(A, E, j)], k, 11).cpu().numpy()     # 128 pairs: four token splits
+    assert np.all(_rel(got[0], solo) < 1e-5)
+
+
 @pytest.mark.parametrize("B,T,p,k", [(1, 64, 4100, 16), (2, 40, 2600, 5), (1, 200, 4096, 32)])
 def test_hutch_few_rows_wide_sketch(D, B, T, p, k):
     # few token rows and a wide sketched side (many 512-column stages per workgroup, ragged end)
