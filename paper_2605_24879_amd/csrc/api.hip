@@ -5,7 +5,6 @@
 #include <cmath>
 #include <cstring>
 #include <mutex>
-#include <vector>
 
 #include "../../include/dprc.h"
 #include "kernels.hpp"
@@ -926,9 +925,28 @@ dprc_status hutch_launch_batched(ProjectArgs* pj, int npj, const TokredBatch& gr
   return DPRC_SUCCESS;
 }
 
+// The tile sums of an activation group (layers l .. le - 1) of a batched call,
+// [nseg][B][ntiles] doubles, kept until the per-sample sums at the end of the call: the
+// bytes of its slice, and of all groups' slices in order.
+size_t group_tilesq_bytes(const dprc_layer* layers, int32_t l, int32_t le, dprc_side side) {
+  const View v0 = view_of(layers[l], side);
+  const TokPlan tp = tok_plan(v0.B, v0.T, v0.n);
+  return ((size_t)(le - l) * v0.B * tp.ntiles * sizeof(double) + kAlign - 1) / kAlign * kAlign;
+}
+
+size_t hutch_tilesq_bytes(const dprc_layer* layers, int32_t n, int32_t k, dprc_side side) {
+  size_t off = 0;
+  for (int32_t l = 0; l < n;) {
+    const int32_t le = group_end(layers, l, n, k, side);
+    off += group_tilesq_bytes(layers, l, le, side);
+    l = le;
+  }
+  return off;
+}
+
 // Up to kTokMaxJobs consecutive activation groups starting at layer l0: their bounds in
-// ends[], their own buffers carved from ws (own may be null) after the shared scratch.
-// Returns the bytes used.
+// ends[], their own buffers (token-split partials and Y; the tile sums are the call's)
+// carved from ws (own may be null) after the shared scratch.  Returns the bytes used.
 size_t hutch_batch_layout(const dprc_layer* layers, int32_t l0, int32_t n, int32_t k, int probe, dprc_side side,
                           void* ws, int32_t* ends, int* ngroups, TokBufs* own) {
   View v[kMaxGroup];
@@ -952,8 +970,6 @@ size_t hutch_batch_layout(const dprc_layer* layers, int32_t l0, int32_t n, int32
     const size_t pf = tp.S > 1 ? (size_t)v0.B * tp.ntiles * tp.S * pad_cols(G * k) * kTile : 0;
     if (own) own[q].part = base && pf ? reinterpret_cast<float*>(base + off) : nullptr;
     off = (off + pf * sizeof(float) + kAlign - 1) / kAlign * kAlign;
-    if (own) own[q].tilesq = base ? reinterpret_cast<double*>(base + off) : nullptr;
-    off = (off + (size_t)G * v0.B * tp.ntiles * sizeof(double) + kAlign - 1) / kAlign * kAlign;
     if (probe != DPRC_PROBE_GAUSSIAN) {          // its own Y: the groups' launches are batched
       if (own) own[q].Y = base ? reinterpret_cast<uint16_t*>(base + off) : nullptr;
       off = (off + (size_t)2 * pad_cols(G * k) * v0.B * tp.T_pad * sizeof(uint16_t) + kAlign - 1) / kAlign * kAlign;
@@ -986,6 +1002,7 @@ size_t dprc_norm_hutch_workspace(const dprc_layer* layers, int32_t num_layers, i
       need = std::max(need, hutch_batch_layout(layers, l, num_layers, k, (int)probe, side, nullptr, ends, &ng, nullptr));
       l = ends[ng - 1];
     }
+    need += hutch_tilesq_bytes(layers, num_layers, k, side);   // the call's tile sums come first
   }
   return need;
 }
@@ -1007,11 +1024,34 @@ static dprc_status norm_hutch(const dprc_layer* layers, int32_t num_layers, int3
   const int64_t B = layers[0].B;
   View v[kMaxGroup];
   if (hutch_batched(layers, num_layers)) {
+    // every group's tile sums for the whole call at the front, then the batches' scratch;
+    // the per-sample sums run once at the end over all groups (kSampleMaxGroups per launch)
+    char* tq = static_cast<char*>(ws);
+    ws = tq + hutch_tilesq_bytes(layers, num_layers, k, side);
+    SampleSumArgs ss{};
+    int launched = 0;
+    auto flush = [&](bool last) -> dprc_status {
+      if (ss.ngroups == 0) return DPRC_SUCCESS;
+      ss.B = (int32_t)B;
+      ss.n2 = n2;
+      ss.accumulate = (accumulate || launched > 0) ? 1 : 0;
+      ss.clip_C = clipC;
+      ss.clip_c = last ? clip_c : nullptr;
+      if (traced(DPRC_KERNEL_SAMPLE_SUM, stream, [&] { return launch_sample_sums(ss, stream); }) != hipSuccess)
+        return DPRC_ERROR_HIP;
+      ++launched;
+      ss.ngroups = 0;
+      return DPRC_SUCCESS;
+    };
     for (int32_t l = 0; l < num_layers;) {
       int32_t ends[kTokMaxJobs];
       int ng = 0;
       TokBufs own[kTokMaxJobs];
       hutch_batch_layout(layers, l, num_layers, k, (int)probe, side, ws, ends, &ng, own);
+      for (int q = 0, lq = l; q < ng; lq = ends[q++]) {
+        own[q].tilesq = reinterpret_cast<double*>(tq);
+        tq += group_tilesq_bytes(layers, lq, ends[q], side);
+      }
       TokredBatch bt{};
       const bool batched = own[0].Y != nullptr;
       ProjectArgs pj[kTokMaxJobs * kMaxGroup];
@@ -1031,12 +1071,14 @@ static dprc_status norm_hutch(const dprc_layer* layers, int32_t num_layers, int3
       if (batched) unsplit_large_batch(bt);       // (unbatched groups launched theirs already)
       if (batched && (s = hutch_launch_batched(pj, npj, bt, stream)) != DPRC_SUCCESS) return s;
       if ((s = run_splits_batch(bt.job, bt.njobs, stream)) != DPRC_SUCCESS) return s;
-      const bool last = l == num_layers;
-      if (traced(DPRC_KERNEL_SAMPLE_SUM, stream, [&] {
-            return launch_tokred_sample_batch(bt, clipC, last ? clip_c : nullptr, stream); }) != hipSuccess)
-        return DPRC_ERROR_HIP;
+      for (int q = 0; q < bt.njobs; ++q) {
+        if (ss.ngroups == kSampleMaxGroups && (s = flush(false)) != DPRC_SUCCESS) return s;
+        const TokredArgs& a = bt.job[q];
+        ss.scale = a.scale;                        // 1/k for every group of the call
+        ss.g[ss.ngroups++] = SampleGroup{a.tilesq, a.n2_layer, a.ntiles, a.nseg};
+      }
     }
-    return DPRC_SUCCESS;
+    return flush(true);
   }
   for (int32_t l = 0; l < num_layers;) {
     const int32_t le = group_end(layers, l, num_layers, k, side);

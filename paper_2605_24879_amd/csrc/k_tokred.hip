@@ -400,37 +400,55 @@ __global__ __launch_bounds__(kBlock) void tokred_sample_kernel(TokredArgs a) {
   }
 }
 
-// Estimates of several token reductions (mode 0) in one launch: sample i walks the jobs
-// in order, each job's layers in order, adding each layer's estimate (tile sums in tile
-// order) to n2 as separate launches would; the clip factor follows the last one.
-__global__ __launch_bounds__(kBlock) void tokred_sample_batch_kernel(TokredBatch bt, float clip_C, float* clip_c) {
-  __shared__ double dred[4];
-  const int i = blockIdx.x;
-  const TokredArgs& a0 = bt.job[0];
-  float n2 = a0.accumulate ? a0.n2[i] : 0.f;
-  for (int j = 0; j < bt.njobs; ++j) {
-    const TokredArgs& a = bt.job[j];
-    for (int g = 0; g < a.nseg; ++g) {
-      const double* ts = a.tilesq + ((int64_t)g * a.B + i) * a.ntiles;
-      double t = 0.0;
-      for (int k = threadIdx.x; k < a.ntiles; k += kBlock) t += ts[k];
-      t = block_sum_d(t, dred);
-      const float est = (float)(t * (double)a.scale);
-      n2 += est;
-      if (threadIdx.x == 0 && a.n2_layer) a.n2_layer[(int64_t)g * a.B + i] = est;
+// Per-sample sums of a whole call's token reductions in one launch (one workgroup of 16
+// waves per sample).  Wave w takes the layers w, w + 16, ... and sums each layer's tile
+// sums exactly as block_sum_d does in tokred_sample_kernel (thread t's strided partial,
+// then per wave of 64 such partials, then (w0 + w1) + (w2 + w3)), so the estimates are the
+// same bit for bit; the layers' estimates then go to n2 in layer order, as a launch per
+// group would add them.
+constexpr int kSampleMaxLayers = kSampleMaxGroups * kMaxGroup;
+constexpr int kSampleWaves = 16;
+__global__ __launch_bounds__(64 * kSampleWaves) void sample_sums_kernel(SampleSumArgs a) {
+  __shared__ float est[kSampleMaxLayers];
+  const int i = blockIdx.x, lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  int flat = 0;
+  for (int q = 0; q < a.ngroups; ++q) {
+    const SampleGroup& gr = a.g[q];
+    for (int s = 0; s < gr.nseg; ++s, ++flat) {
+      if (flat % kSampleWaves != wv) continue;
+      const double* ts = gr.tilesq + ((int64_t)s * a.B + i) * gr.ntiles;
+      double p[4];
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        double t = 0.0;
+        for (int k = 64 * w + lane; k < gr.ntiles; k += kBlock) t += ts[k];
+        p[w] = wave_sum(t);
+      }
+      const double t = (p[0] + p[1]) + (p[2] + p[3]);
+      const float e = (float)(t * (double)a.scale);
+      if (lane == 0) {
+        est[flat] = e;
+        if (gr.n2_layer) gr.n2_layer[(int64_t)s * a.B + i] = e;
+      }
     }
   }
+  __syncthreads();
   if (threadIdx.x == 0) {
-    a0.n2[i] = n2;
-    if (clip_c) clip_c[i] = clip_factor(n2, clip_C);
+    float n2 = a.accumulate ? a.n2[i] : 0.f;
+    for (int l = 0; l < flat; ++l) n2 += est[l];
+    a.n2[i] = n2;
+    if (a.clip_c) a.clip_c[i] = clip_factor(n2, a.clip_C);
   }
 }
 
-hipError_t launch_tokred_sample_batch(const TokredBatch& bt, float clip_C, float* clip_c, hipStream_t st) {
-  if (bt.njobs < 1 || bt.njobs > kTokMaxJobs) return hipErrorInvalidValue;
-  DPRC_LAUNCH(tokred_sample_batch_kernel, dim3((unsigned)bt.job[0].B), dim3(kBlock), 0, st, bt, clip_C, clip_c);
+hipError_t launch_sample_sums(const SampleSumArgs& a, hipStream_t st) {
+  if (a.ngroups < 1 || a.ngroups > kSampleMaxGroups || a.B < 1) return hipErrorInvalidValue;
+  for (int q = 0; q < a.ngroups; ++q)
+    if (a.g[q].nseg < 1 || a.g[q].nseg > kMaxGroup || a.g[q].ntiles < 1) return hipErrorInvalidValue;
+  DPRC_LAUNCH(sample_sums_kernel, dim3((unsigned)a.B), dim3(64 * kSampleWaves), 0, st, a);
   return hipGetLastError();
 }
+
 
 hipError_t launch_tokred_splits(const TokredArgs& a, hipStream_t st) {
   const dim3 grid((unsigned)a.ntiles, (unsigned)a.B);

@@ -116,6 +116,25 @@ struct TokredBatch {
   TokredArgs job[kTokMaxJobs];   // S > 1
 };
 
+// Per-sample sums of a call's token reductions (mode 0), up to kSampleMaxGroups groups in
+// one launch: sample i walks the groups in order, each group's layers in order, adding each
+// layer's estimate (its tile sums summed in the order of tokred_sample_kernel) to n2.
+constexpr int kSampleMaxGroups = 128;
+struct SampleGroup {
+  const double* tilesq;   // [nseg][B][ntiles]
+  float* n2_layer;        // [nseg][B] estimates per layer (may be null)
+  int32_t ntiles, nseg;
+};
+struct SampleSumArgs {
+  int32_t ngroups, B;
+  float scale;            // estimate = scale * sum of the layer's tile sums
+  float clip_C;
+  float* n2;              // [B]
+  float* clip_c;          // [B] clip factors from the final n2 (may be null)
+  int32_t accumulate;     // add to n2 (else start from zero)
+  SampleGroup g[kSampleMaxGroups];
+};
+
 struct GemmArgs {
   const uint16_t* A;
   int64_t lda, a_ss;
@@ -304,7 +323,7 @@ hipError_t launch_tokred(const TokredArgs& a, hipStream_t st);
 hipError_t launch_tokred_splits(const TokredArgs& a, hipStream_t st);   // S > 1
 hipError_t launch_tokred_splits_batch(const TokredBatch& bt, hipStream_t st);
 // mode 0: the estimates of the jobs' layers added to n2 in order, then the clip factor (clip_c may be null)
-hipError_t launch_tokred_sample_batch(const TokredBatch& bt, float clip_C, float* clip_c, hipStream_t st);
+hipError_t launch_sample_sums(const SampleSumArgs& a, hipStream_t st);
 hipError_t launch_tokred_sample(const TokredArgs& a, hipStream_t st);   // mode 0
 hipError_t launch_project_f32(const ProjectF32Args& a, hipStream_t st);
 hipError_t launch_tokred_f32(const TokredF32Args& a, hipStream_t st);

@@ -209,6 +209,33 @@ def test_hutch_many_groups_batched(D, k, probe):
         assert torch.equal(n2l, solo)
 
 
+@pytest.mark.parametrize("accumulate", [False, True])
+def test_hutch_more_groups_than_one_sample_sum(D, accumulate):
+    # 131 single-layer groups (the per-sample sums of a call take 128 groups per launch, so
+    # a second launch continues n2), ragged widths; each layer's estimate equals that of a
+    # call of its own bit for bit, n2 their sum in layer order, the clip factors follow n2
+    B, T, k, C = 3, 70, 16, 0.5
+    pairs = []
+    for j in range(131):
+        d, p = 40 + 8 * (j % 5), 24 + 16 * (j % 7)
+        A, E = _draw(B, T, d, p, layer=300 + j)
+        pairs.append((A, E, j))
+    n2l = torch.zeros(len(pairs), B, device="cuda")
+    n2 = torch.full((B,), 0.25, device="cuda")
+    c = torch.zeros(B, device="cuda")
+    D.dprc_norm_hutch_clip(pairs, k, 9, C, n2=n2, c=c, n2_layers=n2l, accumulate=accumulate)
+    solo = torch.stack([D.dprc_norm_hutch([(A, E, j)], k, 9) for (A, E, j) in pairs])
+    assert torch.equal(n2l, solo)
+    ref = np.full(B, 0.25 if accumulate else 0.0, dtype=np.float32)
+    for j in range(len(pairs)):                       # float adds in layer order
+        ref = (ref + solo[j].cpu().numpy()).astype(np.float32)
+    assert np.array_equal(n2.cpu().numpy(), ref)
+    assert np.allclose(c.cpu().numpy(), est.clip_scale(ref.astype(np.float64), C), rtol=1e-6)
+    for j in (0, 64, 127, 128, 130):                  # against the oracle
+        A, E, _ = pairs[j]
+        assert np.all(_rel(n2l[j].cpu().numpy(), est.hutch_layer(_np(A), _np(E), k, 9, j)) < NORM_RTOL), j
+
+
 @pytest.mark.parametrize("k", [32, 20])
 def test_hutch_large_batch_unsplit(D, k):
     # a batch of eight layers with 1024 (sample, 128-column tile) pairs: its token reductions
