@@ -858,10 +858,10 @@ dprc_status dprc_trace_launches(hipEvent_t* events, int32_t* kinds, int32_t capa
 }
 
 // Calls whose layers are all bf16 finish up to kTokMaxJobs activation groups at once: the
-// projections and token reductions of every group, one split-sum launch, then one launch
-// that adds every layer's estimate to n2 in layer order (the clip factors follow the last
-// group of the call).  Each group keeps its own token-split partials and tile sums; the
-// rest of the scratch is shared.
+// projections and token reductions of every group, then one split-sum launch.  Each group
+// keeps its own token-split partials (the rest of the per-batch scratch is shared) and its
+// tile sums, which stay until the end of the call: one launch there adds every layer's
+// estimate to n2 in layer order and writes the clip factors.
 bool hutch_batched(const dprc_layer* layers, int32_t n) {
   if (n < 2) return false;
   for (int32_t l = 0; l < n; ++l)
