@@ -105,12 +105,14 @@ typedef struct {
  *   k in [1, 256] (GAUSSIAN probes: k <= 32, else DPRC_ERROR_NOT_SUPPORTED).
  *   All layers must have the same B.
  * Workspace: dprc_norm_hutch_workspace() bytes for the same arguments (0 when
- * they are invalid).  When every layer is bf16, up to eight groups of layers
- * keep their own token-split partials in it at once (their split sums and
- * estimates take one launch each), and with RADEMACHER or HADAMARD probes also
- * their own projected Y (B x T rounded up to 64, x 2 x the group's columns
- * rounded up to 16, bf16), so their projections and token reductions are
- * batched too; it grows with the number of layers up to that many groups. */
+ * they are invalid).  When every layer is bf16, up to sixteen groups of layers
+ * keep their own token-split partials in it at once (their split sums take one
+ * launch), and with RADEMACHER or HADAMARD probes also their own projected Y
+ * (B x T rounded up to 64, x 2 x the group's columns rounded up to 16, bf16),
+ * so their projections and token reductions are batched too; it grows with the
+ * number of layers up to that many groups.  Every group's tile sums (B x
+ * ceil(reduced width / 128) doubles per layer) stay in it until the per-sample
+ * sums of all layers at the end of the call. */
 size_t dprc_norm_hutch_workspace(const dprc_layer* layers, int32_t num_layers, int32_t k,
                                  dprc_probe probe, dprc_side side);
 dprc_status dprc_norm_hutch(const dprc_layer* layers, int32_t num_layers, int32_t k,

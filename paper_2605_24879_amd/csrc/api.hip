@@ -869,25 +869,6 @@ bool hutch_batched(const dprc_layer* layers, int32_t n) {
   return true;
 }
 
-// A batch whose token reductions have at least kUnsplitPairs (sample, tile) pairs fills the
-// GPU without token splits: every job then runs unsplit (one workgroup per pair over all
-// tokens, writing its tile sum directly), which halves the per-workgroup start and finish
-// costs of two-way splits and drops the split-sum launch.  The split partials the layout
-// reserved stay unused.
-constexpr int64_t kUnsplitPairs = 1024;
-void unsplit_large_batch(TokredBatch& bt) {
-  int64_t pairs = 0;
-  for (int q = 0; q < bt.njobs; ++q) pairs += (int64_t)bt.job[q].B * bt.job[q].ntiles;
-  if (pairs < kUnsplitPairs) return;
-  for (int q = 0; q < bt.njobs; ++q) {
-    TokredArgs& a = bt.job[q];
-    if (a.mode != 0) continue;
-    a.stages_per_split = a.S * a.stages_per_split;
-    a.S = 1;
-    a.part = nullptr;
-  }
-}
-
 // The collected projections (widest first, up to kProjMaxJobs per launch) and token
 // reductions (one launch per column count) of a batch of activation groups; work over
 // more than 64 columns takes one launch per layer or group.
@@ -925,6 +906,25 @@ dprc_status hutch_launch_batched(ProjectArgs* pj, int npj, const TokredBatch& gr
   return DPRC_SUCCESS;
 }
 
+// A batch whose token reductions have at least kUnsplitPairs (sample, tile) pairs fills the
+// GPU without token splits: every job then runs unsplit (one workgroup per pair over all
+// tokens, writing its tile sum directly), which halves the per-workgroup start and finish
+// costs of two-way splits and drops the split-sum launch.  The batch layout reserves no
+// split partials for such a batch.
+constexpr int64_t kUnsplitPairs = 1024;
+void unsplit_large_batch(TokredBatch& bt) {
+  int64_t pairs = 0;
+  for (int q = 0; q < bt.njobs; ++q) pairs += (int64_t)bt.job[q].B * bt.job[q].ntiles;
+  if (pairs < kUnsplitPairs) return;
+  for (int q = 0; q < bt.njobs; ++q) {
+    TokredArgs& a = bt.job[q];
+    if (a.mode != 0) continue;
+    a.stages_per_split = a.S * a.stages_per_split;
+    a.S = 1;
+    a.part = nullptr;
+  }
+}
+
 // The tile sums of an activation group (layers l .. le - 1) of a batched call,
 // [nseg][B][ntiles] doubles, kept until the per-sample sums at the end of the call: the
 // bytes of its slice, and of all groups' slices in order.
@@ -960,6 +960,13 @@ size_t hutch_batch_layout(const dprc_layer* layers, int32_t l0, int32_t n, int32
     ends[ng++] = le;
     l = le;
   }
+  // a batch whose launches are batched and unsplit (unsplit_large_batch) needs no partials
+  int64_t pairs = 0;
+  for (int q = 0, lq = l0; q < ng; lq = ends[q++]) {
+    const View v0 = view_of(layers[lq], side);
+    pairs += v0.B * tok_plan(v0.B, v0.T, v0.n).ntiles;
+  }
+  const bool unsplit = probe != DPRC_PROBE_GAUSSIAN && pairs >= kUnsplitPairs;
   char* base = static_cast<char*>(ws);
   size_t off = (shared + kAlign - 1) / kAlign * kAlign;
   l = l0;
@@ -967,7 +974,7 @@ size_t hutch_batch_layout(const dprc_layer* layers, int32_t l0, int32_t n, int32
     const View v0 = view_of(layers[l], side);
     const int G = ends[q] - l;
     const TokPlan tp = tok_plan(v0.B, v0.T, v0.n);
-    const size_t pf = tp.S > 1 ? (size_t)v0.B * tp.ntiles * tp.S * pad_cols(G * k) * kTile : 0;
+    const size_t pf = !unsplit && tp.S > 1 ? (size_t)v0.B * tp.ntiles * tp.S * pad_cols(G * k) * kTile : 0;
     if (own) own[q].part = base && pf ? reinterpret_cast<float*>(base + off) : nullptr;
     off = (off + pf * sizeof(float) + kAlign - 1) / kAlign * kAlign;
     if (probe != DPRC_PROBE_GAUSSIAN) {          // its own Y: the groups' launches are batched
