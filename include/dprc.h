@@ -105,7 +105,7 @@ typedef struct {
  *   k in [1, 256] (GAUSSIAN probes: k <= 32, else DPRC_ERROR_NOT_SUPPORTED).
  *   All layers must have the same B.
  * Workspace: dprc_norm_hutch_workspace() bytes for the same arguments (0 when
- * they are invalid).  When every layer is bf16, up to sixteen groups of layers
+ * they are invalid).  When every layer is bf16, up to 32 groups of layers
  * keep their own token-split partials in it at once (their split sums take one
  * launch), and with RADEMACHER or HADAMARD probes also their own projected Y
  * (B x T rounded up to 64, x 2 x the group's columns rounded up to 16, bf16),
@@ -136,7 +136,7 @@ dprc_status dprc_norm_hutch_clip(const dprc_layer* layers, int32_t num_layers, i
  * object holds on every device it runs on until the process ends; the call allocates
  * nothing and frees nothing.  A call whose dprc_norm_hutch_workspace() exceeds that
  * size returns DPRC_ERROR_SCRATCH_LIMIT and enqueues nothing (the 113-layer
- * Llama-3.2-1B stack at B = 8, T = 4096, k = 32 needs 68 MiB).  `stream` must belong
+ * Llama-3.2-1B stack at B = 8, T = 4096, k = 32 needs 136 MiB).  `stream` must belong
  * to the current device (else DPRC_ERROR_INVALID_VALUE); the first call on a device
  * looks up that device's copy of the array (hipGetSymbolAddress) and keeps its
  * address for the process, so make that first call outside graph capture.  Every
@@ -144,7 +144,7 @@ dprc_status dprc_norm_hutch_clip(const dprc_layer* layers, int32_t num_layers, i
  * streams, or host threads without ordering between their streams) race on it and
  * must be serialised by the caller.  Nothing in it needs to start cleared; it keeps
  * the last call's contents. */
-#define DPRC_STATIC_SCRATCH_BYTES (128u << 20)
+#define DPRC_STATIC_SCRATCH_BYTES (256u << 20)
 dprc_status dprc_norm_hutch_clip_static(const dprc_layer* layers, int32_t num_layers, int32_t k,
                                         dprc_probe probe, uint64_t seed, dprc_side side, float C,
                                         float* n2, float* c, float* n2_layers, int32_t accumulate,

@@ -70,7 +70,7 @@ struct ProjectArgs {
 
 // Projections of several layers in one launch (one kernel instantiation: same columns,
 // same dense-column count, same rows per workgroup).
-constexpr int kProjMaxJobs = 16;      // 2.7 KB of kernel arguments
+constexpr int kProjMaxJobs = 32;      // 5.5 KB of kernel arguments
 struct ProjectBatch {
   int32_t njobs, blocks;         // blocks and blk0 are set by the launcher
   int32_t blk0[kProjMaxJobs];
@@ -109,7 +109,7 @@ struct TokredArgs {
 };
 
 // Token-split sums of several layers' passes in one launch.
-constexpr int kTokMaxJobs = 16;       // 3.6 KB of kernel arguments
+constexpr int kTokMaxJobs = 32;       // 7.3 KB of kernel arguments
 struct TokredBatch {
   int32_t njobs, blocks;
   int32_t blk0[kTokMaxJobs];     // first block of each job (ntiles * B blocks each)

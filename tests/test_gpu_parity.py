@@ -181,7 +181,7 @@ def test_hutch_shared_activations_mixed_sides(D):
 @pytest.mark.parametrize("k,probe", [(16, "rademacher"), (12, "hadamard"), (40, "rademacher"),
                                      (100, "rademacher")])
 def test_hutch_many_groups_batched(D, k, probe):
-    # 15 bf16 layers in 11 activation groups (one batch of up to sixteen): shared groups of
+    # 15 bf16 layers in 11 activation groups (one batch of up to 32): shared groups of
     # three and two layers between single layers, so one batch holds more than eight
     # projections and token reductions of several column counts (k = 40: groups over 64
     # columns; k = 100: projections over 64 columns, one launch each)
