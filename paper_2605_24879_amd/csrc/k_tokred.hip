@@ -401,41 +401,74 @@ __global__ __launch_bounds__(kBlock) void tokred_sample_kernel(TokredArgs a) {
 }
 
 // Per-sample sums of a whole call's token reductions in one launch (one workgroup of 16
-// waves per sample).  Wave w takes the layers w, w + 16, ... and sums each layer's tile
-// sums exactly as block_sum_d does in tokred_sample_kernel (thread t's strided partial,
-// then per wave of 64 such partials, then (w0 + w1) + (w2 + w3)), so the estimates are the
-// same bit for bit; the layers' estimates then go to n2 in layer order, as a launch per
-// group would add them.
+// waves per sample).  The layers' (tile sums, count, estimate slot) are first listed in LDS
+// in layer order; wave w then takes the layers w, w + 16, ..., four at a time with all their
+// loads issued together, and sums each layer's tile sums exactly as block_sum_d does in
+// tokred_sample_kernel (thread t's strided partial, then per wave of 64 such partials, then
+// (w0 + w1) + (w2 + w3)), so the estimates are the same bit for bit; the layers' estimates
+// then go to n2 in layer order, as a launch per group would add them.
 constexpr int kSampleMaxLayers = kSampleMaxGroups * kMaxGroup;
 constexpr int kSampleWaves = 16;
 __global__ __launch_bounds__(64 * kSampleWaves) void sample_sums_kernel(SampleSumArgs a) {
   __shared__ float est[kSampleMaxLayers];
+  __shared__ const double* lts[kSampleMaxLayers];
+  __shared__ float* ln2[kSampleMaxLayers];
+  __shared__ int lnt[kSampleMaxLayers];
+  __shared__ int gseg[kSampleMaxGroups];
+  __shared__ int nflat;
   const int i = blockIdx.x, lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  int flat = 0;
-  for (int q = 0; q < a.ngroups; ++q) {
+  if ((int)threadIdx.x < a.ngroups) gseg[threadIdx.x] = a.g[threadIdx.x].nseg;
+  __syncthreads();
+  if ((int)threadIdx.x < a.ngroups) {            // group q lists its layers at its offset
+    const int q = threadIdx.x;
+    int f = 0;
+    for (int u = 0; u < q; ++u) f += gseg[u];
     const SampleGroup& gr = a.g[q];
-    for (int s = 0; s < gr.nseg; ++s, ++flat) {
-      if (flat % kSampleWaves != wv) continue;
-      const double* ts = gr.tilesq + ((int64_t)s * a.B + i) * gr.ntiles;
+    for (int s = 0; s < gr.nseg; ++s) {
+      lts[f + s] = gr.tilesq + ((int64_t)s * a.B + i) * gr.ntiles;
+      ln2[f + s] = gr.n2_layer ? gr.n2_layer + (int64_t)s * a.B + i : nullptr;
+      lnt[f + s] = gr.ntiles;
+    }
+    if (q == a.ngroups - 1) nflat = f + gr.nseg;
+  }
+  __syncthreads();
+  const int nl = nflat;
+  constexpr int U = 4;                           // layers of a wave whose loads go out together
+  for (int l0 = wv; l0 < nl; l0 += U * kSampleWaves) {
+    double v[U][4];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int l = l0 + u * kSampleWaves;
+      const int nt = l < nl ? lnt[l] : 0;
+      const double* ts = l < nl ? lts[l] : nullptr;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) v[u][w] = 64 * w + lane < nt ? ts[64 * w + lane] : 0.0;
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int l = l0 + u * kSampleWaves;
+      if (l >= nl) break;                          // wave-uniform
+      const int nt = lnt[l];
+      const double* ts = lts[l];
       double p[4];
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
-        double t = 0.0;
-        for (int k = 64 * w + lane; k < gr.ntiles; k += kBlock) t += ts[k];
+        double t = v[u][w];
+        for (int k = 64 * w + lane + kBlock; k < nt; k += kBlock) t += ts[k];   // beyond 256 tiles
         p[w] = wave_sum(t);
       }
       const double t = (p[0] + p[1]) + (p[2] + p[3]);
       const float e = (float)(t * (double)a.scale);
       if (lane == 0) {
-        est[flat] = e;
-        if (gr.n2_layer) gr.n2_layer[(int64_t)s * a.B + i] = e;
+        est[l] = e;
+        if (ln2[l]) *ln2[l] = e;
       }
     }
   }
   __syncthreads();
   if (threadIdx.x == 0) {
     float n2 = a.accumulate ? a.n2[i] : 0.f;
-    for (int l = 0; l < flat; ++l) n2 += est[l];
+    for (int l = 0; l < nl; ++l) n2 += est[l];
     a.n2[i] = n2;
     if (a.clip_c) a.clip_c[i] = clip_factor(n2, a.clip_C);
   }
