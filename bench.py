@@ -202,11 +202,16 @@ def kernel_bytes_per_step(cfg):
 TRAFFIC_KERNELS = {"project": (("project_kernel", "project_batch_kernel"), "paper_2605_24879_amd/csrc/k_project.hip"),
                    "token_reduce": (("tokred_kernel", "tokred_batch_kernel"), "paper_2605_24879_amd/csrc/k_tokred.hip"),
                    "accumulate": (("gemm_kernel",), "paper_2605_24879_amd/csrc/k_gemm.hip")}
+# sources every launch's traffic depends on besides its kernel's own file
+TRAFFIC_SHARED_SOURCES = ("paper_2605_24879_amd/csrc/device.hpp", "paper_2605_24879_amd/csrc/kernels.hpp",
+                          "paper_2605_24879_amd/csrc/api.hip")
 
 
 def measured_traffic(workload, kernel):
     """HBM bytes per launch (read + write) from the committed rocprofv3 counter summary, or None
-    when there is none for this workload or the kernel source changed since it was taken."""
+    when there is none for this workload or when the kernel's source, the shared device header,
+    the launch-side headers or the host code that groups layers into launches changed since the
+    counters were taken."""
     import hashlib
     root = os.path.dirname(os.path.abspath(__file__))
     path = os.path.join(root, "profiles", f"{workload}_hbm_traffic.json")
@@ -218,9 +223,9 @@ def measured_traffic(workload, kernel):
     if not recs:
         return None
     sha = lambda p: hashlib.sha256(open(os.path.join(root, p), "rb").read()).hexdigest()[:16]
+    want = {p: sha(p) for p in (src,) + TRAFFIC_SHARED_SOURCES}
     for rec in recs:
-        if rec.get("source_sha256_16") != sha(src) or \
-                rec.get("device_hpp_sha256_16") != sha("paper_2605_24879_amd/csrc/device.hpp"):
+        if rec.get("sources_sha256_16") != want:
             return None
     # per launch, averaged over the dispatches of the kind's kernel families
     n = sum(rec.get("dispatches", 1) for rec in recs)
