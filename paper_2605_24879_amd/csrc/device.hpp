@@ -53,13 +53,16 @@ __device__ __forceinline__ u32x4 rademacher_block(uint32_t key0, uint32_t key1, 
   return philox4x32_10(u32x4{blk, col, layer, stream}, key0, key1);
 }
 
-// Word w (rows 32w .. 32w+31) of column j of the Sylvester-Hadamard sign pattern.
+// Word w (rows 32w .. 32w+31) of column j of the Sylvester-Hadamard sign pattern.  The
+// sign of entry (r, j) is the parity of popcount(r & j).  Within a word, bit k of r
+// (k < 5) follows a fixed 32-bit pattern, so the word is the XOR of the patterns of the set
+// bits of j & 31, inverted when popcount(32 w & j) is odd.
 __device__ __forceinline__ uint32_t hadamard_word(uint32_t w, uint32_t col) {
+  constexpr uint32_t kBitPattern[5] = {0xAAAAAAAAu, 0xCCCCCCCCu, 0xF0F0F0F0u, 0xFF00FF00u, 0xFFFF0000u};
   uint32_t pat = 0;
 #pragma unroll
-  for (uint32_t b = 0; b < 32; ++b) pat |= (uint32_t)(__popc(b & col) & 1) << b;
-  const uint32_t hi = (uint32_t)(__popc((w << 5) & col) & 1);
-  return hi ? ~pat : pat;
+  for (int k = 0; k < 5; ++k) pat ^= ((col >> k) & 1u) ? kBitPattern[k] : 0u;
+  return (__popc((w << 5) & col) & 1) ? ~pat : pat;
 }
 
 __device__ __forceinline__ uint32_t tail_mask(int64_t m, int64_t w) {

@@ -66,6 +66,7 @@ struct ProjectArgs {
   uint32_t* zero_ptr;       // counters cleared by workgroup (0,0) (may be null)
   int32_t zero_count;
   int32_t vec;              // token rows of X are 16-byte aligned: 16-byte loads
+  int32_t rblocks;          // row blocks per workgroup (set by the launcher)
 };
 
 // Projections of several layers in one launch (one kernel instantiation: same columns,
