@@ -36,6 +36,19 @@ __device__ __forceinline__ double block_sum_d(double v, double* red4) {
   return (red4[0] + red4[1]) + (red4[2] + red4[3]);
 }
 
+// The same sum over each group of four waves of a workgroup of 4 TT waves (red holds
+// 4 TT values): every thread gets its own group's total, added as by block_sum_d.
+template <int TT>
+__device__ __forceinline__ double quad_sum_d(double v, double* red) {
+  v = wave_sum(v);
+  const int tid = threadIdx.x;
+  __syncthreads();
+  if ((tid & 63) == 0) red[tid >> 6] = v;
+  __syncthreads();
+  const double* r4 = red + 4 * (tid >> 8);
+  return (r4[0] + r4[1]) + (r4[2] + r4[3]);
+}
+
 __device__ __forceinline__ void store4(const TokredArgs& a, int i, int c, int j, const float v[4]) {
   if (c >= a.ncols) return;
   if (a.M && c >= a.m_col0) {
@@ -66,14 +79,18 @@ __device__ __forceinline__ void seg_add(const TokredArgs& a, int c, double v, do
     if (c >= g * a.seg && c < (g + 1) * a.seg) sq[g] += v;
 }
 
-__device__ __forceinline__ void seg_publish(const TokredArgs& a, int64_t tslot, double (&sq)[kMaxGroup],
-                                            double* dred) {
+// Tile sums of a workgroup of TT tiles: the four waves of tile h (tslot0 + h) add their
+// squares as a workgroup of one tile does; a tile past the operand's last is not written.
+template <int TT>
+__device__ __forceinline__ void seg_publish(const TokredArgs& a, int64_t tslot0, int tile0,
+                                            double (&sq)[kMaxGroup], double* dred) {
   const int64_t lstride = (int64_t)a.B * a.ntiles;
+  const int h = threadIdx.x >> 8;
 #pragma unroll
   for (int g = 0; g < kMaxGroup; ++g) {
     if (g >= a.nseg) break;
-    const double t = block_sum_d(sq[g], dred);
-    if (threadIdx.x == 0) a.tilesq[g * lstride + tslot] = t;
+    const double t = quad_sum_d<TT>(sq[g], dred);
+    if ((threadIdx.x & 255) == 0 && tile0 + h < a.ntiles) a.tilesq[g * lstride + tslot0 + h] = t;
   }
 }
 
@@ -82,39 +99,46 @@ struct Int {
   static constexpr int value = V;
 };
 
-template <int NB, bool FAST>
+// TT = 2 (unsplit squared-norm launches with an even number of 16-column blocks): a
+// workgroup of eight waves reduces two adjacent 128-column tiles, so each Y stage read
+// from L2 serves twice the columns.  Waves 4h .. 4h + 3 work on tile h exactly as the
+// four waves of a one-tile workgroup do.
+template <int NB, bool FAST, int TT = 1>
 __device__ __forceinline__ void tokred_body(const TokredArgs& a, int bx, int by) {
+  static_assert(TT == 1 || (NB % 2 == 0 && NB <= 4), "two-tile workgroups stage Y through LDS, two halves");
   // Y stages go through LDS with X (one 16-byte load per thread per 16 columns)
   // when they are small; wider Y is read straight from global memory at use.
   constexpr bool YLDS = NB <= 4;
   constexpr int YLd = kStage + 8;                       // padded LDS row of one Y column (144 bytes)
-  __shared__ __attribute__((aligned(16))) uint16_t lds[2][kStage * kLdsLd];
+  constexpr int XLd = TT * kTile + 16;                  // padded LDS row of the X stage
+  constexpr int YN = YLDS ? NB / TT : 1;                // Y loads per thread per stage
+  __shared__ __attribute__((aligned(16))) uint16_t lds[2][kStage * XLd];
   __shared__ __attribute__((aligned(16))) uint16_t ylds[YLDS ? 2 : 1][YLDS ? 2 * 16 * NB * YLd : 8];
-  __shared__ double dred[4];
+  __shared__ double dred[4 * TT];
   constexpr int P = 4;                                  // stages in flight in registers, one more in LDS
   static_assert(P == 4, "the stage loop below is written out for four ring slots");
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int g = lane >> 4, l16 = lane & 15, r4 = l16 >> 2, c4 = lane & 3;
   const int i = by;
-  const int tile = bx / a.S, s = bx - tile * a.S;
-  const int j0 = tile * kTile;
+  const int tile = bx / a.S, s = bx - tile * a.S;      // (TT = 2: bx is the tile pair)
+  const int j0 = tile * TT * kTile;
   const int tb = s * a.stages_per_split * kStage;
   const int te = min(a.T, tb + a.stages_per_split * kStage);
   const int nst = te > tb ? (te - tb + kStage - 1) / kStage : 0;
 
-  const int lr0 = tid >> 4, lc = (tid & 15) * 8;
+  const int lr0 = tid >> (3 + TT), lc = (tid & (16 * TT - 1)) * 8;
   const uint16_t* xs = a.X + (int64_t)i * a.x_ss;
   // FAST: one buffer resource per stage (64 token rows from column j0); rows past
   // the split and columns past n read as zero through out-of-range offsets
   const uint32_t row_bytes = (uint32_t)a.ldx * 2u;
   const uint32_t lane_off = j0 + lc < a.n ? (uint32_t)lr0 * row_bytes + 2u * lc : kOobOffset;
   const uint16_t* ys = a.Yt + (int64_t)i * a.T_pad;
-  // Y stage loads: column-half ch = tid / 8 + 32 r (h = ch / ncols16, c = ch % ncols16), tokens 8 (tid % 8) ..
+  // Y stage loads: column-half ch = tid / 8 + 32 TT r (h = ch / ncols16, c = ch % ncols16), tokens 8 (tid % 8) ..
   const int ych = tid >> 3, ytk = (tid & 7) * 8;
 
   struct Stage {
     uint4 x[4];
-    uint4 y[YLDS ? NB : 1];
+    uint4 y[YN];
   };
   // Stages past the split (st >= nst) are issued too, with an empty range (X) or
   // clamped to the last stage (Y): the load sequence is the same in every stage,
@@ -138,8 +162,8 @@ __device__ __forceinline__ void tokred_body(const TokredArgs& a, int bx, int by)
     if constexpr (YLDS) {
       const int ytok = tb + min(st, nst - 1) * kStage + ytk;
 #pragma unroll
-      for (int r = 0; r < NB; ++r) {
-        const int ch = ych + 32 * r, h = ch / (16 * NB), c = ch - h * 16 * NB;
+      for (int r = 0; r < YN; ++r) {
+        const int ch = ych + 32 * TT * r, h = ch / (16 * NB), c = ch - h * 16 * NB;
         dst.y[r] = *reinterpret_cast<const uint4*>(ys + ((int64_t)h * a.ncols_pad + c) * a.yt_ld + ytok);
       }
     }
@@ -147,11 +171,11 @@ __device__ __forceinline__ void tokred_body(const TokredArgs& a, int bx, int by)
   auto swrite = [&](const Stage& src, int buf) __attribute__((always_inline)) {
 #pragma unroll
     for (int q = 0; q < 4; ++q)
-      *reinterpret_cast<uint4*>(&lds[buf][(lr0 + 16 * q) * kLdsLd + lds_swz(lr0 + 16 * q, lc)]) = src.x[q];
+      *reinterpret_cast<uint4*>(&lds[buf][(lr0 + 16 * q) * XLd + lds_swz(lr0 + 16 * q, lc)]) = src.x[q];
     if constexpr (YLDS) {
 #pragma unroll
-      for (int r = 0; r < NB; ++r)
-        *reinterpret_cast<uint4*>(&ylds[buf][(ych + 32 * r) * YLd + ytk]) = src.y[r];
+      for (int r = 0; r < YN; ++r)
+        *reinterpret_cast<uint4*>(&ylds[buf][(ych + 32 * TT * r) * YLd + ytk]) = src.y[r];
     }
   };
 
@@ -182,8 +206,8 @@ __device__ __forceinline__ void tokred_body(const TokredArgs& a, int bx, int by)
       for (int x = 0; x < 2; ++x) {
         const int mb = 2 * wv + x;
         // rows 32ks + 8g + r4 (+4) all have bit 3 equal to g & 1
-        const uint16_t* p = &lds[buf][(32 * ks + 8 * g + r4) * kLdsLd + ((16 * mb + 4 * c4) ^ ((g & 1) << 6))];
-        const uint4 av = make_u4(lds_read_tr16(p), lds_read_tr16(p + 4 * kLdsLd));
+        const uint16_t* p = &lds[buf][(32 * ks + 8 * g + r4) * XLd + ((16 * mb + 4 * c4) ^ ((g & 1) << 6))];
+        const uint4 av = make_u4(lds_read_tr16(p), lds_read_tr16(p + 4 * XLd));
 #pragma unroll
         for (int h = 0; h < 2; ++h)
 #pragma unroll
@@ -229,6 +253,19 @@ __device__ __forceinline__ void tokred_body(const TokredArgs& a, int bx, int by)
       for (int q = 0; q < 4; ++q) w[x][nb][q] = acc[x][0][nb][q] + acc[x][1][nb][q];
 
   const int64_t tslot = (int64_t)i * a.ntiles + tile;
+  if constexpr (TT > 1) {                              // unsplit squared norms only
+    double sq[kMaxGroup] = {};
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        const int c = 16 * nb + l16;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) seg_add(a, c, (double)(w[x][nb][q] * w[x][nb][q]), sq);
+      }
+    seg_publish<TT>(a, (int64_t)i * a.ntiles + TT * tile, TT * tile, sq, dred);
+    return;
+  }
   if (a.S == 1) {
     if (a.mode == 0) {
       double sq[kMaxGroup] = {};
@@ -240,7 +277,7 @@ __device__ __forceinline__ void tokred_body(const TokredArgs& a, int bx, int by)
 #pragma unroll
           for (int q = 0; q < 4; ++q) seg_add(a, c, (double)(w[x][nb][q] * w[x][nb][q]), sq);
         }
-      seg_publish(a, tslot, sq, dred);
+      seg_publish<1>(a, tslot, tile, sq, dred);
     } else {
 #pragma unroll
       for (int x = 0; x < 2; ++x)
@@ -276,8 +313,8 @@ __global__ __launch_bounds__(kBlock) void tokred_kernel(TokredArgs a) {
 // splits the runs were slower (mlp layers, 5%) and ids map to blocks directly.  The grid
 // is padded to whole windows.
 constexpr int kXcdRun = 16;
-template <int NB, bool FAST>
-__global__ __launch_bounds__(kBlock) void tokred_batch_kernel(TokredBatch bt) {
+template <int NB, bool FAST, int TT>
+__global__ __launch_bounds__(kBlock * TT) void tokred_batch_kernel(TokredBatch bt) {
   constexpr int W = 8 * kXcdRun;
   const int id = (int)blockIdx.x;
   const int b = bt.job[0].S == 1 ? id / W * W + (id & 7) * kXcdRun + (id % W) / 8 : id;
@@ -286,10 +323,11 @@ __global__ __launch_bounds__(kBlock) void tokred_batch_kernel(TokredBatch bt) {
 #pragma unroll
   for (int q = 1; q < kTokMaxJobs; ++q) jb += (q < bt.njobs && b >= bt.blk0[q]) ? 1 : 0;
   const TokredArgs& a = bt.job[jb];
-  const int gx = a.ntiles * a.S;
+  const int nt = (a.ntiles + TT - 1) / TT;           // tiles, or tile pairs
+  const int gx = nt * a.S;
   const int rel = b - bt.blk0[jb], idx = rel % gx;
-  const int split = idx / a.ntiles, tile = idx - split * a.ntiles;
-  tokred_body<NB, FAST>(a, tile * a.S + split, rel / gx);
+  const int split = idx / nt, tile = idx - split * nt;
+  tokred_body<NB, FAST, TT>(a, tile * a.S + split, rel / gx);
 }
 
 // Sum of the token splits of one tile, in split order: its squared norm (mode 0)
@@ -348,7 +386,7 @@ __device__ __forceinline__ void tokred_splits_block(const TokredArgs& a, int til
       }
     }
   }
-  if (a.mode == 0) seg_publish(a, tslot, sq, dred);
+  if (a.mode == 0) seg_publish<1>(a, tslot, tile, sq, dred);
 }
 
 template <int U>
@@ -498,30 +536,39 @@ hipError_t launch_tokred_sample(const TokredArgs& a, hipStream_t st) {
 
 hipError_t launch_tokred_batch(TokredBatch bt, hipStream_t st) {
   if (bt.njobs < 1 || bt.njobs > kTokMaxJobs) return hipErrorInvalidValue;
-  bool fast = true;
-  bt.blocks = 0;
+  bool fast = true, pairs = bt.job[0].ncols_pad % 32 == 0;
   for (int j = 0; j < bt.njobs; ++j) {
     const TokredArgs& a = bt.job[j];
     if (a.ncols_pad != bt.job[0].ncols_pad) return hipErrorInvalidValue;   // one instantiation
     // buffer offsets within one 64-row stage stay below 2^31
     fast = fast && a.vec && a.n % 8 == 0 && (int64_t)kStage * a.ldx * 2 < ((int64_t)1 << 31);
+    pairs = pairs && a.S == 1 && a.mode == 0;       // unsplit squared norms: two tiles per workgroup
+  }
+  const int tt = pairs ? 2 : 1;
+  bt.blocks = 0;
+  for (int j = 0; j < bt.njobs; ++j) {
+    const TokredArgs& a = bt.job[j];
     bt.blk0[j] = bt.blocks;
-    bt.blocks += a.ntiles * a.S * a.B;
+    bt.blocks += (a.ntiles + tt - 1) / tt * a.S * a.B;
   }
   const dim3 grid((unsigned)round_up(bt.blocks, 8 * kXcdRun));   // whole windows (see the kernel)
-#define DPRC_TOKRED_BATCH_CASE(NB)                                                             \
-  case NB:                                                                                     \
-    if (fast) DPRC_LAUNCH((tokred_batch_kernel<NB, true>), grid, dim3(kBlock), 0, st, bt);     \
-    else DPRC_LAUNCH((tokred_batch_kernel<NB, false>), grid, dim3(kBlock), 0, st, bt);         \
-    break;
+#define DPRC_TOKRED_BATCH_LAUNCH(NB, TT)                                                                  \
+  if (fast) DPRC_LAUNCH((tokred_batch_kernel<NB, true, TT>), grid, dim3(kBlock * TT), 0, st, bt);        \
+  else DPRC_LAUNCH((tokred_batch_kernel<NB, false, TT>), grid, dim3(kBlock * TT), 0, st, bt);
   switch (bt.job[0].ncols_pad / 16) {
-    DPRC_TOKRED_BATCH_CASE(1)
-    DPRC_TOKRED_BATCH_CASE(2)
-    DPRC_TOKRED_BATCH_CASE(3)
-    DPRC_TOKRED_BATCH_CASE(4)
+    case 1: DPRC_TOKRED_BATCH_LAUNCH(1, 1) break;
+    case 2:
+      if (tt == 2) { DPRC_TOKRED_BATCH_LAUNCH(2, 2) }
+      else { DPRC_TOKRED_BATCH_LAUNCH(2, 1) }
+      break;
+    case 3: DPRC_TOKRED_BATCH_LAUNCH(3, 1) break;
+    case 4:
+      if (tt == 2) { DPRC_TOKRED_BATCH_LAUNCH(4, 2) }
+      else { DPRC_TOKRED_BATCH_LAUNCH(4, 1) }
+      break;
     default: return hipErrorInvalidValue;
   }
-#undef DPRC_TOKRED_BATCH_CASE
+#undef DPRC_TOKRED_BATCH_LAUNCH
   return hipGetLastError();
 }
 

@@ -238,11 +238,12 @@ def test_hutch_more_groups_than_one_sample_sum(D, accumulate):
 
 @pytest.mark.parametrize("k", [32, 20])
 def test_hutch_large_batch_unsplit(D, k):
-    # a batch of eight layers with 1024 (sample, 128-column tile) pairs: its token reductions
-    # run without token splits (one workgroup per pair over all 200 tokens, a ragged last
-    # stage), the layers ragged in both widths; a second call of one layer runs split
+    # a batch of eight layers with 1028 (sample, 128-column tile) pairs: its token reductions
+    # run without token splits (one workgroup per pair of tiles over all 200 tokens, a ragged
+    # last stage; the last layer has an odd number of tiles, its last one 8 columns wide), the
+    # layers ragged in both widths; a second call of one layer runs split
     B, T = 4, 200
-    shapes = [(4000, 300), (4096, 130), (4000, 520), (4096, 96), (4000, 72), (4096, 260), (4000, 1000), (4096, 40)]
+    shapes = [(4000, 300), (4096, 130), (4000, 520), (4096, 96), (4000, 72), (4096, 260), (4000, 1000), (4104, 40)]
     pairs = []
     for j, (d, p) in enumerate(shapes):
         A, E = _draw(B, T, d, p, layer=200 + j)
