@@ -2,8 +2,8 @@
 // Hutchinson estimator, Algorithm 2; also the W_S, O S and [U | W_P] steps of
 // Hutch++), followed by either the squared-norm estimate or a store of M_i.
 //
-// A workgroup owns one sample, a 128-column tile of X and a contiguous range of
-// tokens.  X tiles (64 tokens x 128 columns, 256 bytes per token row) are
+// A workgroup owns one sample, a 128-column tile of X (two adjacent tiles, eight waves,
+// in unsplit squared-norm launches) and a contiguous range of tokens.  X tiles (64 tokens x 128 columns, 256 bytes per token row) are
 // loaded with coalesced 16-byte reads, double-buffered through LDS and read
 // back token-contiguous with the gfx950 LDS transpose read, which is the
 // operand layout of the MFMA (the contraction runs over tokens, X is stored
