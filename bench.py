@@ -123,11 +123,21 @@ def step_fn(cfg, D, torch, ws_norm, grads, ws_acc):
         if marks is not None:
             marks[1].record()
         if cfg["accumulate"]:
-            for (A, E, li), g in zip(layers, grads):
-                D.dprc_clip_accumulate(A, E, c, grad=g, ws=ws_acc)
-                if cfg["noise_sigma"] is not None:
-                    D.dprc_add_noise(g, cfg["noise_sigma"], C, 0, li)
+            accumulate_layers(cfg, D, layers, c, grads, ws_acc)
     return step
+
+
+def accumulate_layers(cfg, D, layers, c, grads, ws_acc):
+    """The clipped accumulation of every layer (bf16: one call for all of them, so the small
+    layers share launches instead of splitting over tokens), then the noise of each."""
+    if cfg["dtype"] == "bf16":
+        D.dprc_clip_accumulate_layers(layers, c, grads=grads)
+    else:
+        for (A, E, li), g in zip(layers, grads):
+            D.dprc_clip_accumulate(A, E, c, grad=g, ws=ws_acc)
+    if cfg["noise_sigma"] is not None:
+        for (A, E, li), g in zip(layers, grads):
+            D.dprc_add_noise(g, cfg["noise_sigma"], cfg["C"], 0, li)
 
 
 class LaunchTrace:
@@ -201,7 +211,7 @@ def kernel_bytes_per_step(cfg):
 # launch kind -> the kernel families it dispatches (single-layer and batched) and their source
 TRAFFIC_KERNELS = {"project": (("project_kernel", "project_batch_kernel"), "paper_2605_24879_amd/csrc/k_project.hip"),
                    "token_reduce": (("tokred_kernel", "tokred_batch_kernel"), "paper_2605_24879_amd/csrc/k_tokred.hip"),
-                   "accumulate": (("gemm_kernel",), "paper_2605_24879_amd/csrc/k_gemm.hip")}
+                   "accumulate": (("gemm_kernel", "gemm_batch_kernel"), "paper_2605_24879_amd/csrc/k_gemm.hip")}
 # sources every launch's traffic depends on besides its kernel's own file
 TRAFFIC_SHARED_SOURCES = ("paper_2605_24879_amd/csrc/device.hpp", "paper_2605_24879_amd/csrc/kernels.hpp",
                           "paper_2605_24879_amd/csrc/api.hip")
@@ -552,10 +562,7 @@ def step_norm_only(cfg, D, layers, n2, c, ws_n):
 
 def step_rest_only(cfg, D, layers, c, grads, ws_acc):
     if cfg["accumulate"]:
-        for (A, E, li), g in zip(layers, grads):
-            D.dprc_clip_accumulate(A, E, c, grad=g, ws=ws_acc)
-            if cfg["noise_sigma"] is not None:
-                D.dprc_add_noise(g, cfg["noise_sigma"], cfg["C"], 0, li)
+        accumulate_layers(cfg, D, layers, c, grads, ws_acc)
 
 
 LLAMA_STEP = dict(B=2, T=2048, k=16, C=1.0, sigma=0.8, lr=1e-4)

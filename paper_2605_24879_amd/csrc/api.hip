@@ -1284,6 +1284,59 @@ dprc_status dprc_clip_accumulate(const dprc_layer* L, const float* c, float* gra
   return DPRC_SUCCESS;
 }
 
+dprc_status dprc_clip_accumulate_layers(const dprc_layer* layers, int32_t num_layers, const float* c,
+                                        float* const* grads, const int64_t* ldg, int32_t accumulate,
+                                        hipStream_t stream) {
+  if (num_layers < 0 || (num_layers > 0 && (!layers || !grads || !ldg || !c))) return DPRC_ERROR_INVALID_VALUE;
+  for (int32_t l = 0; l < num_layers; ++l) {
+    const dprc_layer& L = layers[l];
+    const dprc_status s = check_layer(L);
+    if (s != DPRC_SUCCESS) return s;
+    if (L.B != layers[0].B || !grads[l] || ldg[l] < L.p) return DPRC_ERROR_INVALID_VALUE;
+    if (L.dtype != DPRC_BF16 || L.d * L.p > (1LL << 40)) return DPRC_ERROR_NOT_SUPPORTED;
+  }
+  auto args_of = [&](int32_t l) {
+    const dprc_layer& L = layers[l];
+    const GemmPlan g = gemm_plan(L);
+    GemmArgs a;
+    a.A = (const uint16_t*)L.A; a.lda = L.lda; a.a_ss = L.T * L.lda;
+    a.E = (const uint16_t*)L.E; a.lde = L.lde; a.e_ss = L.T * L.lde;
+    a.B = (int32_t)L.B; a.T = (int32_t)L.T; a.d = (int32_t)L.d; a.p = (int32_t)L.p;
+    a.c = c; a.out = grads[l]; a.ldo = ldg[l]; a.accumulate = accumulate;
+    a.S = 1; a.stages_per_sample = g.sps; a.stages_per_split = (int32_t)(L.B * g.sps);
+    a.part = nullptr;
+    a.vec_a = rows16(L.A, L.lda);
+    a.vec_e = rows16(L.E, L.lde);
+    return a;
+  };
+  // A layer with a whole round of tiles (one per CU) runs in a launch of its own, all its
+  // tiles in step through the tokens (they share operand slabs in L2); the smaller ones
+  // share launches, up to kGemmMaxJobs at a time, instead of splitting over tokens.
+  GemmBatch bt{};
+  auto flush = [&]() -> dprc_status {
+    if (bt.njobs == 0) return DPRC_SUCCESS;
+    std::stable_sort(bt.job, bt.job + bt.njobs, [](const GemmArgs& x, const GemmArgs& y) {
+      return ceil_div(x.d, 256) * ceil_div(x.p, 256) > ceil_div(y.d, 256) * ceil_div(y.p, 256); });
+    const hipError_t e = traced(DPRC_KERNEL_ACCUMULATE, stream, [&] { return launch_gemm_batch(bt, stream); });
+    bt.njobs = 0;
+    return e == hipSuccess ? DPRC_SUCCESS : DPRC_ERROR_HIP;
+  };
+  for (int32_t l = 0; l < num_layers; ++l) {
+    const GemmArgs a = args_of(l);
+    if (ceil_div(a.d, 256) * ceil_div(a.p, 256) >= kGemmRoundTiles) {
+      if (traced(DPRC_KERNEL_ACCUMULATE, stream, [&] { return launch_gemm(a, stream); }) != hipSuccess)
+        return DPRC_ERROR_HIP;
+      continue;
+    }
+    bt.job[bt.njobs++] = a;
+    if (bt.njobs == kGemmMaxJobs) {
+      const dprc_status s = flush();
+      if (s != DPRC_SUCCESS) return s;
+    }
+  }
+  return flush();
+}
+
 dprc_status dprc_add_noise(float* grad, int64_t numel, float sigma, float C, uint64_t seed, uint32_t tensor_id,
                            hipStream_t stream) {
   if (numel < 0 || (numel > 0 && !grad)) return DPRC_ERROR_INVALID_VALUE;

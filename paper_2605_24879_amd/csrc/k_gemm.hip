@@ -41,8 +41,9 @@ struct GInt {
   static constexpr int value = V;
 };
 
+// wg: the tile (before the XCD reordering), split: the token split.
 template <int NW, int NS, bool FAST>
-__global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmArgs a) {
+__device__ __forceinline__ void gemm_body(const GemmArgs& a, int wg, int split) {
   constexpr int kThreads = 64 * NW;
   constexpr int WN = NW == 8 ? 64 : 128;             // wave tile columns
   constexpr int YB = WN / 32;                        // 32-column MFMA blocks per wave
@@ -57,12 +58,11 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmArgs a) {
   // tile of this workgroup: consecutive ids of one XCD walk the smaller dimension first
   const int tm_n = (a.d + kGM - 1) / kGM, tn_n = (a.p + kGM - 1) / kGM;
   const int ntiles = tm_n * tn_n;
-  const int wg = blockIdx.x;
   // a bijection on [0, ntiles) when ntiles is a multiple of 8; identity otherwise
   const int lin = (ntiles & 7) == 0 ? (wg & 7) * (ntiles >> 3) + (wg >> 3) : wg;
   int tm, tn;
   if (a.d <= a.p) { tm = lin % tm_n; tn = lin / tm_n; } else { tn = lin % tn_n; tm = lin / tn_n; }
-  const int d0 = tm * kGM, p0 = tn * kGM, split = blockIdx.y;
+  const int d0 = tm * kGM, p0 = tn * kGM;
 
   const int sps = a.stages_per_sample;
   const int gs_begin = split * a.stages_per_split;
@@ -252,6 +252,26 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmArgs a) {
     }
 }
 
+template <int NW, int NS, bool FAST>
+__global__ __launch_bounds__(64 * NW, 1) void gemm_kernel(GemmArgs a) {
+  gemm_body<NW, NS, FAST>(a, blockIdx.x, blockIdx.y);
+}
+
+// Several layers in one launch, each unsplit (S = 1): job j owns blocks blk0[j] ..
+// blk0[j] + ntiles_j - 1, and blk0[j] is a multiple of 8, so that a job's blocks are
+// dealt to the XCDs as those of a launch of its own; blocks up to the next multiple of
+// 8 are idle.
+template <int NW, int NS, bool FAST>
+__global__ __launch_bounds__(64 * NW, 1) void gemm_batch_kernel(GemmBatch bt) {
+  int jb = 0;
+#pragma unroll 8
+  for (int q = 1; q < kGemmMaxJobs; ++q) jb += (q < bt.njobs && (int)blockIdx.x >= bt.blk0[q]) ? 1 : 0;
+  const GemmArgs& a = bt.job[jb];
+  const int wg = (int)blockIdx.x - bt.blk0[jb];
+  if (wg >= (int)(((int64_t)a.d + kGM - 1) / kGM * (((int64_t)a.p + kGM - 1) / kGM))) return;
+  gemm_body<NW, NS, FAST>(a, wg, 0);
+}
+
 GemmPlan gemm_plan_v2(int64_t B, int64_t T, int64_t d, int64_t p) {
   GemmPlan g;
   g.sps = (int32_t)ceil_div(T, kGK);
@@ -275,6 +295,26 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t st) {
     DPRC_LAUNCH((gemm_kernel<NW, NS, true>), grid, dim3(64 * NW), 0, st, a);
   else
     DPRC_LAUNCH((gemm_kernel<NW, NS, false>), grid, dim3(64 * NW), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_batch(GemmBatch bt, hipStream_t st) {
+  if (bt.njobs < 1 || bt.njobs > kGemmMaxJobs) return hipErrorInvalidValue;
+  constexpr int NW = 8, NS = 2;
+  bool fast = true;
+  int64_t blocks = 0;
+  for (int j = 0; j < bt.njobs; ++j) {
+    const GemmArgs& a = bt.job[j];
+    if (a.S != 1) return hipErrorInvalidValue;
+    fast = fast && a.vec_a && a.vec_e && a.d % 8 == 0 && a.p % 8 == 0 &&
+           (int64_t)kGK * std::max(a.lda, a.lde) * 2 < ((int64_t)1 << 31);
+    bt.blk0[j] = (int32_t)blocks;
+    blocks += round_up(ceil_div(a.d, kGM) * ceil_div(a.p, kGM), 8);
+  }
+  if (blocks >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)blocks);
+  if (fast) DPRC_LAUNCH((gemm_batch_kernel<NW, NS, true>), grid, dim3(64 * NW), 0, st, bt);
+  else DPRC_LAUNCH((gemm_batch_kernel<NW, NS, false>), grid, dim3(64 * NW), 0, st, bt);
   return hipGetLastError();
 }
 

@@ -150,6 +150,14 @@ struct GemmArgs {
   float* part;            // [S][d][p] (S > 1)
   int32_t vec_a, vec_e;   // token rows 16-byte aligned
 };
+// Unsplit accumulations of several layers in one launch (the launcher sets blk0).
+constexpr int kGemmMaxJobs = 64;     // 8.7 KB of kernel arguments
+constexpr int64_t kGemmRoundTiles = 256;   // 256 x 256 tiles that occupy every CU once
+struct GemmBatch {
+  int32_t njobs;
+  int32_t blk0[kGemmMaxJobs];
+  GemmArgs job[kGemmMaxJobs];
+};
 struct GemmPlan {
   int32_t S, sps, spl, tiles;   // splits, slabs per sample, slabs per split, output tiles
 };
@@ -343,6 +351,7 @@ hipError_t launch_hpp_rows_batch(const FinalBatch& bt, hipStream_t st);
 hipError_t launch_hpp_sum_batch(const FinalBatch& bt, hipStream_t st);
 hipError_t launch_clip_scale(const float* n2, int64_t B, float C, float* c, hipStream_t st);
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t st);
+hipError_t launch_gemm_batch(GemmBatch bt, hipStream_t st);
 hipError_t launch_gemm_f32(const float* A, int64_t lda, int64_t a_ss, const float* E, int64_t lde,
                            int64_t e_ss, int32_t B, int32_t T, int32_t d, int32_t p,
                            const float* c, float* out, int64_t ldo, int accumulate,

@@ -24,7 +24,7 @@ STREAM_PROBE, STREAM_SKETCH, STREAM_NOISE = 0, 1, 2
 
 EXPORTS = ["dprc_norm_hutch_workspace", "dprc_norm_hutch", "dprc_norm_hutch_clip", "dprc_norm_hutch_clip_static", "dprc_norm_hutchpp_workspace",
            "dprc_norm_hutchpp", "dprc_clip_scale", "dprc_clip_accumulate_workspace",
-           "dprc_clip_accumulate", "dprc_add_noise", "dprc_probe_bits", "dprc_probe_gaussian", "dprc_private_adamw", "dprc_envelope_middle_workspace",
+           "dprc_clip_accumulate", "dprc_clip_accumulate_layers", "dprc_add_noise", "dprc_probe_bits", "dprc_probe_gaussian", "dprc_private_adamw", "dprc_envelope_middle_workspace",
            "dprc_envelope_middle", "dprc_chi2_cdf", "dprc_envelope_bins", "dprc_pld_step_workspace",
            "dprc_pld_step", "dprc_pld_fold", "dprc_pld_delta", "dprc_status_string",
            "dprc_version", "dprc_trace_launches"]
@@ -69,6 +69,7 @@ def lib():
             "dprc_clip_scale": (ctypes.c_int, [P, I64, F, P, P]),
             "dprc_clip_accumulate_workspace": (SZ, [LP]),
             "dprc_clip_accumulate": (ctypes.c_int, [LP, P, P, I64, I32, P, SZ, P]),
+            "dprc_clip_accumulate_layers": (ctypes.c_int, [LP, I32, P, P, P, I32, P]),
             "dprc_add_noise": (ctypes.c_int, [P, I64, F, F, U64, U32, P]),
             "dprc_probe_bits": (ctypes.c_int, [ctypes.c_int, U64, U32, U32, I64, I32, P, P]),
             "dprc_probe_gaussian": (ctypes.c_int, [U64, U32, I64, I32, P, P]),
@@ -237,6 +238,26 @@ def dprc_clip_accumulate(A, E, c, grad=None, accumulate=False, ws=None):
                                       int(bool(accumulate)), ws.data_ptr() if ws is not None else None,
                                       need, _stream(A.device)))
     return grad
+
+
+def dprc_clip_accumulate_layers(pairs, c, grads=None, accumulate=False):
+    """grads[l] [d_l, p_l] (fp32) (=|+=) sum_i c_i A_i^T E_i for every (A, E) of pairs (bf16), in
+    one launch per 64 layers.  Returns the list of gradients."""
+    pairs = [(A, E) for (A, E, *_) in pairs]
+    n = len(pairs)
+    if grads is None:
+        grads = [torch.empty(A.shape[2], E.shape[2], dtype=torch.float32, device=A.device) for (A, E) in pairs]
+    if len(grads) != n:
+        raise ValueError("one gradient per layer")
+    for g in grads:
+        if g.stride(1) != 1:
+            raise ValueError("grad must have contiguous rows")
+    arr = (Layer * n)(*[make_layer(A, E, 0) for (A, E) in pairs])
+    ptrs = (ctypes.c_void_p * n)(*[g.data_ptr() for g in grads])
+    lds = (ctypes.c_int64 * n)(*[g.stride(0) for g in grads])
+    dev = pairs[0][0].device if n else c.device
+    _check(lib().dprc_clip_accumulate_layers(arr, n, c.data_ptr(), ptrs, lds, int(bool(accumulate)), _stream(dev)))
+    return grads
 
 
 def dprc_add_noise(grad, sigma, C, seed, tensor_id):

@@ -494,6 +494,47 @@ def test_clip_accumulate_parity(D, B, T, d, p, dtype):
     assert err2 < GRAD_RTOL
 
 
+@pytest.mark.parametrize("aligned", [True, False])
+def test_clip_accumulate_layers_parity(D, aligned):
+    # several layers of one batch in one launch, no token splits: each layer's gradient against
+    # the oracle and against a call of its own (which splits the small ones over tokens); 8 and
+    # 15 tiles (the XCD ordering, ragged edges), T free per layer; with a 1001-wide layer the
+    # launch takes element loads; then accumulation onto existing gradients
+    B = 3
+    shapes = [(150, 1024, 512), (100, 520, 1032), (64, 64, 48), (77, 256, 256), (150, 2048, 512)]
+    if not aligned:
+        shapes.append((90, 1001, 96))
+    pairs = [(*_draw(B, T, d, p, layer=500 + j), j) for j, (T, d, p) in enumerate(shapes)]
+    cvals = [0.25, 0.0, 0.8]
+    c = torch.tensor(cvals, dtype=torch.float32, device="cuda")
+    grads = D.dprc_clip_accumulate_layers(pairs, c)
+    for (A, E, j), g in zip(pairs, grads):
+        ref = est.clip_accumulate(_np(A), _np(E), np.array(cvals, dtype=np.float32).astype(np.float64))
+        got = g.cpu().numpy()
+        assert np.linalg.norm(got - ref) / np.linalg.norm(ref) < GRAD_RTOL, j
+        solo = D.dprc_clip_accumulate(A, E, c).cpu().numpy()
+        assert np.linalg.norm(got - solo) / np.linalg.norm(solo) < 1e-5, j
+    g0 = [torch.full_like(g, 0.5) for g in grads]
+    D.dprc_clip_accumulate_layers(pairs, c, grads=g0, accumulate=True)
+    for g, gacc in zip(grads, g0):
+        assert torch.allclose(gacc, g + 0.5, rtol=1e-6, atol=1e-6)
+
+
+def test_clip_accumulate_layers_two_launches(D):
+    # 70 layers (64 per launch), gradients with row strides wider than p
+    B, pairs, grads = 2, [], []
+    for j in range(70):
+        d, p = 40 + 8 * (j % 4), 24 + 8 * (j % 5)
+        A, E = _draw(B, 30 + j, d, p, layer=600 + j)
+        pairs.append((A, E, j))
+        grads.append(torch.zeros(d, p + 8, device="cuda")[:, :p])
+    c = torch.tensor([0.6, 1.0], device="cuda")
+    D.dprc_clip_accumulate_layers(pairs, c, grads=grads)
+    for (A, E, j), g in zip(pairs, grads):
+        solo = D.dprc_clip_accumulate(A, E, c).cpu().numpy()
+        assert np.linalg.norm(g.cpu().numpy() - solo) / np.linalg.norm(solo) < 1e-5, j
+
+
 def test_clip_accumulate_zero_factor_drops_nonfinite_sample(D):
     A, E = _draw(2, 100, 64, 64, layer=10)
     A[1, 3, 5] = float("nan")

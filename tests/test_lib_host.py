@@ -114,6 +114,21 @@ def test_hutchpp_and_accumulate_validation():
     lay = _fake_layer()
     assert L.dprc_clip_accumulate(ctypes.byref(lay), None, 0x50000, 48, 0, None, 0, None) == 1
     assert L.dprc_clip_accumulate(ctypes.byref(lay), 0x60000, 0x50000, 47, 0, None, 0, None) == 1
+    # several layers in one call: validated before any launch
+    two = (dprc.Layer * 2)(_fake_layer(), _fake_layer())
+    ptrs = (ctypes.c_void_p * 2)(0x50000, 0x58000)
+    lds = (ctypes.c_int64 * 2)(48, 48)
+    acc = L.dprc_clip_accumulate_layers
+    assert acc(two, 2, None, ptrs, lds, 0, None) == 1                      # no clip factors
+    assert acc(two, 2, 0x60000, None, lds, 0, None) == 1                   # no gradient list
+    assert acc(two, -1, 0x60000, ptrs, lds, 0, None) == 1
+    assert acc(two, 2, 0x60000, ptrs, (ctypes.c_int64 * 2)(48, 47), 0, None) == 1   # ldg < p
+    assert acc(two, 2, 0x60000, (ctypes.c_void_p * 2)(0x50000, None), lds, 0, None) == 1
+    other_b = (dprc.Layer * 2)(_fake_layer(), _fake_layer(B=3))
+    assert acc(other_b, 2, 0x60000, ptrs, lds, 0, None) == 1               # one batch
+    f32 = (dprc.Layer * 2)(_fake_layer(), _fake_layer(dtype=dprc.F32, A=0x10000))
+    assert acc(f32, 2, 0x60000, ptrs, lds, 0, None) == 2
+    assert acc(two, 0, 0x60000, ptrs, lds, 0, None) == 0                   # nothing to do
 
 
 def test_clip_noise_bits_validation():
