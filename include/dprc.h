@@ -185,11 +185,11 @@ dprc_status dprc_clip_accumulate(const dprc_layer* layer, const float* c, float*
                                  int64_t ldg, int32_t accumulate, void* ws, size_t ws_bytes,
                                  hipStream_t stream);
 
-/* The same for num_layers bf16 layers of one batch (same B; T, d and p free) in as few
- * launches as possible (up to 64 layers each): grads[l][j*ldg[l] + u] (=|+=) the sum
- * above for layer l.  No layer is split over its tokens, so no workspace is needed;
- * layers with few 256 x 256 output tiles run next to the others' instead (a step's
- * small projections and its split-K reductions fold into the launch).  grads and ldg
+/* The same for num_layers bf16 layers of one batch (same B; T, d and p free):
+ * grads[l][j*ldg[l] + u] (=|+=) the sum above for layer l.  No layer is split over its
+ * tokens, so no workspace is needed: a layer with at least 256 output tiles of
+ * 256 x 256 takes a launch of its own, and the smaller ones share launches (up to 64
+ * layers each) where dprc_clip_accumulate would split them.  grads and ldg
  * are host arrays of num_layers entries (device pointers, row strides >= p); the
  * gradients must not overlap.  Each layer's result is the one dprc_clip_accumulate
  * gives with one token split, up to the order of the fp32 sums.  Any fp32 layer gives
