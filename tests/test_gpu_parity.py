@@ -260,8 +260,8 @@ def test_hutch_large_batch_unsplit(D, k):
     assert np.all(_rel(got[0], solo) < 1e-5)
 
 
-@pytest.mark.parametrize("case", ["narrow", "chunked"])
-def test_hutch_row_blocks_per_workgroup(D, case):
+@pytest.mark.parametrize("case,probe", [("narrow", "rademacher"), ("chunked", "rademacher"), ("narrow", "hadamard")])
+def test_hutch_row_blocks_per_workgroup(D, case, probe):
     # a batch of 32 layers with enough row blocks that each projection workgroup streams
     # several of them (narrow: 512-wide E, four 32-row blocks per workgroup, one probe chunk
     # per row; chunked: 8200-wide E, four 16-row blocks per workgroup, three probe chunks per
@@ -275,16 +275,17 @@ def test_hutch_row_blocks_per_workgroup(D, case):
     for j in range(32):
         A, E = _draw(B, T, d, p, layer=400 + j)
         pairs.append((A, E, j))
+    pid = D.PROBE_HADAMARD if probe == "hadamard" else D.PROBE_RADEMACHER
     n2l = torch.zeros(len(pairs), B, device="cuda")
-    n2 = D.dprc_norm_hutch(pairs, k, 21, n2_layers=n2l)
+    n2 = D.dprc_norm_hutch(pairs, k, 21, n2_layers=n2l, probe=pid)
     torch.cuda.synchronize()
     got = n2l.cpu().numpy()
-    solo = torch.stack([D.dprc_norm_hutch([(A, E, j)], k, 21) for (A, E, j) in pairs]).cpu().numpy()
+    solo = torch.stack([D.dprc_norm_hutch([(A, E, j)], k, 21, probe=pid) for (A, E, j) in pairs]).cpu().numpy()
     assert np.all(_rel(got, solo) < 1e-5)
     assert np.all(_rel(n2.cpu().numpy(), got.astype(np.float64).sum(axis=0)) < 1e-5)
     for j in check:
         A, E, _ = pairs[j]
-        assert np.all(_rel(got[j], est.hutch_layer(_np(A), _np(E), k, 21, j)) < NORM_RTOL), j
+        assert np.all(_rel(got[j], est.hutch_layer(_np(A), _np(E), k, 21, j, probe=probe)) < NORM_RTOL), j
 
 
 @pytest.mark.parametrize("B,T,p,k", [(1, 64, 4100, 16), (2, 40, 2600, 5), (1, 200, 4096, 32)])
