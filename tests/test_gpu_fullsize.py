@@ -69,12 +69,14 @@ def _tile_rows(d, li):
     return [t * 256 + (37 * t + 11 * li) % min(256, d - t * 256) for t in range((d + 255) // 256)]
 
 
-def _check_rows(D, A, E, c, li, cn, samples_f64=None):
+def _check_rows(D, A, E, c, li, cn, samples_f64=None, g=None):
     """grad rows (one per tile row, all columns) against the oracle; samples_f64 may hold
-    the fp64 host copies of (A_i, E_i) already made."""
+    the fp64 host copies of (A_i, E_i) already made; g, the layer's gradient from a call
+    for several layers (else a call of its own computes it)."""
     d = A.shape[2]
     rows = _tile_rows(d, li)
-    g = D.dprc_clip_accumulate(A, E, c)
+    if g is None:
+        g = D.dprc_clip_accumulate(A, E, c)
     got = g[rows].cpu().numpy().astype(np.float64)
     del g
     ref = np.zeros_like(got)
@@ -213,6 +215,13 @@ def test_stack_full(D):
     c = D.dprc_clip_scale(n2, cfg["C"])
     cn = c.cpu().numpy().astype(np.float64)
     assert np.allclose(cn, est.clip_scale(n2.cpu().numpy().astype(np.float64), cfg["C"]), rtol=1e-6)
+    # the gradients as the bench's step computes them: one call for every layer
+    grads = D.dprc_clip_accumulate_layers(pairs, c)
+    for li in (0, 1):                                              # q and k, split when alone
+        A, E, _ = pairs[li]
+        solo = D.dprc_clip_accumulate(A, E, c)
+        assert ((grads[li] - solo).norm() / solo.norm()).item() < 1e-5
+        del solo
     worst_n = worst_g = 0.0
     for (A, E, li) in pairs:
         # every sample's estimate of this layer, then its gradient rows, from one host copy
@@ -225,7 +234,8 @@ def test_stack_full(D):
             assert r < NORM_RTOL, (li, i, r)
             worst_n = max(worst_n, r)
             del Ai, Ei
-        worst_g = max(worst_g, _check_rows(D, A, E, c, li, cn, host))
+        worst_g = max(worst_g, _check_rows(D, A, E, c, li, cn, host, g=grads[li]))
+        grads[li] = None
         del host
         if li % 16 == 15 or li == L - 1:
             print(f"[stack parity] layers 0..{li}: worst norm rel {worst_n:.2e}, worst grad rel {worst_g:.2e}",
