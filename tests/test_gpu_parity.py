@@ -536,6 +536,30 @@ def test_clip_accumulate_layers_two_launches(D):
         assert np.linalg.norm(g.cpu().numpy() - solo) / np.linalg.norm(solo) < 1e-5, j
 
 
+def test_clip_accumulate_layers_edges(D):
+    # a layer with a whole round of tiles (a launch of its own) between small ones, a
+    # one-token layer, and all-zero factors (nothing added, accumulation leaves the
+    # gradients as they were)
+    B = 2
+    shapes = [(64, 40, 24), (64, 4096, 4096), (1, 8, 8), (33, 300, 72)]
+    pairs = [(*_draw(B, T, d, p, layer=700 + j), j) for j, (T, d, p) in enumerate(shapes)]
+    c = torch.tensor([0.3, 0.9], device="cuda")
+    grads = D.dprc_clip_accumulate_layers(pairs, c)
+    for (A, E, j), g in zip(pairs, grads):
+        solo = D.dprc_clip_accumulate(A, E, c)
+        assert ((g - solo).norm() / solo.norm()).item() < 1e-5, j
+        rows = [0, A.shape[2] // 2, A.shape[2] - 1]
+        ref = est.clip_accumulate_rows(_np(A), _np(E), np.array([0.3, 0.9], dtype=np.float32).astype(np.float64), rows)
+        got = g[rows].cpu().numpy().astype(np.float64)
+        assert np.linalg.norm(got - ref) / np.linalg.norm(ref) < GRAD_RTOL, j
+    zero = torch.zeros(B, device="cuda")
+    fresh = D.dprc_clip_accumulate_layers(pairs, zero)
+    assert all(torch.count_nonzero(g) == 0 for g in fresh)
+    before = [g.clone() for g in grads]
+    D.dprc_clip_accumulate_layers(pairs, zero, grads=grads, accumulate=True)
+    assert all(torch.equal(g, b) for g, b in zip(grads, before))
+
+
 def test_clip_accumulate_zero_factor_drops_nonfinite_sample(D):
     A, E = _draw(2, 100, 64, 64, layer=10)
     A[1, 3, 5] = float("nan")
