@@ -595,7 +595,7 @@ def run_llama_step(args, torch, D):
         key = dpsgd.step_seed(0, drv.steps)
         n2, c = D.dprc_norm_hutch_clip(pairs, k, key, C)
         mark(2)
-        grads = [D.dprc_clip_accumulate(A, E, c, ws=drv._ws_acc) for (A, E, _) in pairs]
+        grads = drv.clipped_sums(pairs, c)
         mark(3)
         del pairs
         drv.update(grads, B, key)            # noise + 1/B + AdamW + bf16 weights, one pass per layer

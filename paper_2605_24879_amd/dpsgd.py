@@ -12,7 +12,7 @@ Per step:
    squared gradient norm summed over the layers; adjacent layers that read
    the same activations (q, k, v; gate, up) share one pass over A;
 4. ``dprc_clip_scale``: c_i = min(1, C / sqrt(n_i));
-5. ``dprc_clip_accumulate``: each layer's clipped gradient sum_i c_i A_i^T E_i
+5. ``dprc_clip_accumulate_layers``: each layer's clipped gradient sum_i c_i A_i^T E_i
    is formed directly on the matrix cores.  For a linear layer it equals the
    weight gradient of the scaled loss sum_i c_i L_i, i.e. the algorithm's
    second backward pass, without running it;
@@ -116,16 +116,21 @@ class DPSGDRC:
         else:
             n2 = D.dprc_norm_hutchpp(pairs, self.s, self.r, key, side=self.side)
             c = D.dprc_clip_scale(n2, self.C)
+        grads = self.clipped_sums(pairs, c)
+        if noise and self.sigma > 0:
+            for (A, E, j), g in zip(pairs, grads):
+                D.dprc_add_noise(g, self.sigma, self.C, key, j)
+        return n2, c, grads
+
+    def clipped_sums(self, pairs, c):
+        """Step 5 for every layer: one call when all are bf16 (the small layers share
+        launches), else one call per layer."""
+        if all(A.dtype == torch.bfloat16 and E.dtype == torch.bfloat16 for (A, E, _) in pairs):
+            return D.dprc_clip_accumulate_layers(pairs, c)
         need = max(D.dprc_clip_accumulate_workspace(A, E) for (A, E, _) in pairs)
         if self._ws_acc is None or self._ws_acc.numel() < need:
-            self._ws_acc = torch.empty(max(need, 1), dtype=torch.uint8, device=n2.device)
-        grads = []
-        for (A, E, j) in pairs:
-            g = D.dprc_clip_accumulate(A, E, c, ws=self._ws_acc)
-            if noise and self.sigma > 0:
-                D.dprc_add_noise(g, self.sigma, self.C, key, j)
-            grads.append(g)
-        return n2, c, grads
+            self._ws_acc = torch.empty(max(need, 1), dtype=torch.uint8, device=c.device)
+        return [D.dprc_clip_accumulate(A, E, c, ws=self._ws_acc) for (A, E, _) in pairs]
 
     def update(self, clipped, batch, key):
         """Steps 6-7 fused: per layer, noise + 1/batch + AdamW + bf16 weight write in one pass."""
