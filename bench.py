@@ -763,8 +763,7 @@ def llama_context_steps(torch, D, dpsgd, drv, loss_fn, model, B, T, k, C, sigma,
         key = dpsgd.step_seed(0, drv.steps)
         n2 = D.dprc_norm_hutch(pairs, k, key)
         c = D.dprc_clip_scale(n2, C)
-        for (A, E, j), m in zip(pairs, masters):
-            g = D.dprc_clip_accumulate(A, E, c, ws=drv._ws_acc)
+        for (A, E, j), m, g in zip(pairs, masters, drv.clipped_sums(pairs, c)):
             D.dprc_add_noise(g, sigma, C, key, j)
             m.grad = g.div_(B)
         del pairs
